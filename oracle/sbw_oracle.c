@@ -1,0 +1,302 @@
+/*
+ * CPU oracle for Stateless Bernoulli Watermarking (SBW).
+ *
+ * TEST INFRASTRUCTURE ONLY.  This file is the plain, slow, obviously correct
+ * statement of what the watermark and detect hot path compute.  Only the test
+ * suite, the smoke check and the CPU-baseline leg of the benchmark load it.  It
+ * shares no source, header, table or helper with the HIP library, and the HIP
+ * library never calls it.
+ *
+ * Every function evaluates the paper's definitions element by element, in the
+ * order the paper states them, with no blocking, fusion or reuse between
+ * elements.  Integer arithmetic is exact (uint32/uint64 wraparound is the
+ * modular arithmetic the definitions use); floating point follows the
+ * precision the definitions fix (one fp32 add; fp64 for the z-score).
+ *
+ * Readings taken where the paper is silent (each one is listed, with its
+ * alternatives, in the design notes of the repository):
+ *   R1  CBRNG(v, r) is the v-th 32-bit output of the Philox4x32-10 stream with
+ *       key r and counter starting at 0: word (v mod 4) of the block at
+ *       counter (floor(v/4), 0, 0, 0).
+ *   R2  "CBRNG(v, r) < gamma" is the exact real comparison x * 2^-32 < gamma,
+ *       i.e. x < ceil(gamma * 2^32).
+ *   R3  Context seed ("additive" PRF, width 1): r = K * p mod 2^64.
+ *   R4  The Jenkins integer hash is Robert Jenkins' six-step 32-bit mix.
+ *   R5  Self-salt seed ("anchored minhash" over {p, v}, anchored on the
+ *       candidate v): r = min_u64(K*J(p)*J(v), K*J(v)*J(v)), products mod 2^64,
+ *       unsigned minimum.
+ *   R6  Detection scores positions 1..L-1, T = L-1, no de-duplication.
+ *   R7  bf16 bias: exact upcast, one fp32 add rounded to nearest even, one
+ *       round-to-nearest-even down-conversion; NaN stays NaN.
+ *   R8  Tokens are taken as their 32-bit pattern (no range check).
+ *
+ * Parity unpinned: jenkins32() has no printed value in the paper and no
+ * independent implementation is available to compare against; it is checked
+ * only through its properties (bijectivity, avalanche, uniformity).
+ */
+#include <math.h>
+#include <stdint.h>
+#include <string.h>
+
+/* ------------------------------------------------------------------------- */
+/* Philox4x32-10 (Salmon, Moraes, Dror, Shaw, "Parallel random numbers: as    */
+/* easy as 1, 2, 3", SC'11), the CBRNG named in Sec. 2.2.                      */
+/* ------------------------------------------------------------------------- */
+
+/* Round multipliers and key-schedule (Weyl) increments as published. */
+static const uint32_t PHILOX_MULT_A = 0xD2511F53u; /* applied to counter word 0 */
+static const uint32_t PHILOX_MULT_B = 0xCD9E8D57u; /* applied to counter word 2 */
+static const uint32_t PHILOX_WEYL_0 = 0x9E3779B9u; /* golden ratio */
+static const uint32_t PHILOX_WEYL_1 = 0xBB67AE85u; /* sqrt(3) - 1  */
+
+/* One Philox S-box: the full 64-bit product of two 32-bit words, split. */
+static void mul_hi_lo(uint32_t a, uint32_t b, uint32_t *hi, uint32_t *lo)
+{
+    uint64_t product = (uint64_t)a * (uint64_t)b;
+    *hi = (uint32_t)(product >> 32);
+    *lo = (uint32_t)product;
+}
+
+/* Ten rounds; the key is bumped by the Weyl constants before rounds 2..10. */
+void oracle_philox4x32_10(const uint32_t counter[4], const uint32_t key[2],
+                          uint32_t out[4])
+{
+    uint32_t c0 = counter[0], c1 = counter[1], c2 = counter[2], c3 = counter[3];
+    uint32_t k0 = key[0], k1 = key[1];
+    for (int round = 0; round < 10; ++round) {
+        if (round > 0) {
+            k0 += PHILOX_WEYL_0;
+            k1 += PHILOX_WEYL_1;
+        }
+        uint32_t hi_a, lo_a, hi_b, lo_b;
+        mul_hi_lo(PHILOX_MULT_A, c0, &hi_a, &lo_a);
+        mul_hi_lo(PHILOX_MULT_B, c2, &hi_b, &lo_b);
+        uint32_t n0 = hi_b ^ c1 ^ k0;
+        uint32_t n1 = lo_b;
+        uint32_t n2 = hi_a ^ c3 ^ k1;
+        uint32_t n3 = lo_a;
+        c0 = n0; c1 = n1; c2 = n2; c3 = n3;
+    }
+    out[0] = c0; out[1] = c1; out[2] = c2; out[3] = c3;
+}
+
+/* CBRNG(v, r), Sec. 2.2: the value at position v of the stream seeded by r,
+ * without computing any earlier position (reading R1). */
+uint32_t oracle_cbrng(uint32_t v, uint64_t r)
+{
+    uint32_t counter[4] = { v / 4u, 0u, 0u, 0u };
+    uint32_t key[2] = { (uint32_t)r, (uint32_t)(r >> 32) };
+    uint32_t block[4];
+    oracle_philox4x32_10(counter, key, block);
+    return block[v % 4u];
+}
+
+/* Membership threshold for "CBRNG(v, r) < gamma", Sec. 2.2, Eq. 1 (reading R2):
+ * ceil(gamma * 2^32), clamped to [0, 2^32].  gamma * 2^32 is exact in binary64. */
+uint64_t oracle_threshold(double gamma)
+{
+    double scaled = ceil(gamma * 4294967296.0);
+    if (!(scaled > 0.0)) return 0u;               /* also catches NaN */
+    if (scaled >= 4294967296.0) return 4294967296ull;
+    return (uint64_t)scaled;
+}
+
+/* ------------------------------------------------------------------------- */
+/* Seeds, Sec. 2.2 (seed from the preceding context via a PRF) and Sec. 2.3    */
+/* (Jenkins integer hash for token ids).                                       */
+/* ------------------------------------------------------------------------- */
+
+/* Robert Jenkins' 32-bit integer hash (reading R4).  Parity unpinned. */
+uint32_t oracle_jenkins32(uint32_t a)
+{
+    a = (a + 0x7ed55d16u) + (a << 12);
+    a = (a ^ 0xc761c23cu) ^ (a >> 19);
+    a = (a + 0x165667b1u) + (a << 5);
+    a = (a + 0xd3a2646cu) ^ (a << 9);
+    a = (a + 0xfd7046c5u) + (a << 3);
+    a = (a ^ 0xb55a4f09u) ^ (a >> 16);
+    return a;
+}
+
+/* Context seeding, additive PRF of width 1 (SBW-1; scheme table in App. D):
+ * r = K * p mod 2^64 (reading R3). */
+uint64_t oracle_seed_context(uint64_t key, uint32_t prev)
+{
+    return key * (uint64_t)prev;
+}
+
+/* Full-vocabulary self-salt seeding (Sec. 5.2; "anchored minhash" in App. D),
+ * at width 1 over the window {p, v}, anchored on the candidate v (reading R5). */
+uint64_t oracle_seed_self_salt(uint64_t key, uint32_t prev, uint32_t cand)
+{
+    uint64_t hp = (uint64_t)oracle_jenkins32(prev);
+    uint64_t hv = (uint64_t)oracle_jenkins32(cand);
+    uint64_t with_prev = key * hp * hv;
+    uint64_t with_self = key * hv * hv;
+    return with_prev < with_self ? with_prev : with_self;
+}
+
+/* Seeding scheme codes (the oracle's own; numerically equal to the library's
+ * by agreement, checked by the tests, not by sharing a header). */
+enum { ORACLE_SEED_CONTEXT = 0, ORACLE_SEED_SELF_SALT = 1 };
+
+uint64_t oracle_seed(uint64_t key, uint32_t prev, uint32_t cand, int seeding)
+{
+    if (seeding == ORACLE_SEED_SELF_SALT) return oracle_seed_self_salt(key, prev, cand);
+    return oracle_seed_context(key, prev);
+}
+
+/* v in G_t  <=>  CBRNG(v, r_t) < gamma   (Sec. 2.2, Eq. 1). */
+int oracle_is_green(uint64_t key, uint32_t prev, uint32_t cand, uint64_t threshold,
+                    int seeding)
+{
+    uint64_t r = oracle_seed(key, prev, cand, seeding);
+    return (uint64_t)oracle_cbrng(cand, r) < threshold;
+}
+
+/* Array form of oracle_is_green for the workload sampler and the tests. */
+void oracle_is_green_many(uint64_t key, const int32_t *prev, const int32_t *cand,
+                          int64_t n, double gamma, int seeding, uint8_t *out)
+{
+    uint64_t threshold = oracle_threshold(gamma);
+    for (int64_t i = 0; i < n; ++i)
+        out[i] = (uint8_t)oracle_is_green(key, (uint32_t)prev[i], (uint32_t)cand[i],
+                                          threshold, seeding);
+}
+
+/* ------------------------------------------------------------------------- */
+/* Logit bias, Sec. 2.2, Eq. 2: l' = l + delta on G_t, l' = l elsewhere.       */
+/* ------------------------------------------------------------------------- */
+
+static float f32_from_bits(uint32_t bits) { float f; memcpy(&f, &bits, 4); return f; }
+static uint32_t bits_from_f32(float f) { uint32_t u; memcpy(&u, &f, 4); return u; }
+
+/* fp32 -> bf16, round to nearest, ties to even; NaN stays NaN (reading R7). */
+uint16_t oracle_f32_to_bf16(float f)
+{
+    uint32_t bits = bits_from_f32(f);
+    if (isnan(f)) return (uint16_t)((bits >> 16) | 0x0040u);
+    uint32_t upper = bits >> 16;
+    uint32_t lower = bits & 0xFFFFu;
+    if (lower > 0x8000u || (lower == 0x8000u && (upper & 1u))) upper += 1u;
+    return (uint16_t)upper;
+}
+
+float oracle_bias_f32(float logit, float delta) { return logit + delta; }
+
+uint16_t oracle_bias_bf16(uint16_t logit, float delta)
+{
+    float widened = f32_from_bits((uint32_t)logit << 16);
+    return oracle_f32_to_bf16(widened + delta);
+}
+
+/* In place over logits[b * row_stride + v], b < B, v < V. */
+void oracle_watermark_f32(float *logits, int64_t B, int64_t V, int64_t row_stride,
+                          const int32_t *prev, uint64_t key, double gamma, float delta,
+                          int seeding)
+{
+    uint64_t threshold = oracle_threshold(gamma);
+    for (int64_t b = 0; b < B; ++b) {
+        for (int64_t v = 0; v < V; ++v) {
+            if (oracle_is_green(key, (uint32_t)prev[b], (uint32_t)v, threshold, seeding)) {
+                float *l = &logits[b * row_stride + v];
+                *l = oracle_bias_f32(*l, delta);
+            }
+        }
+    }
+}
+
+void oracle_watermark_bf16(uint16_t *logits, int64_t B, int64_t V, int64_t row_stride,
+                           const int32_t *prev, uint64_t key, double gamma, float delta,
+                           int seeding)
+{
+    uint64_t threshold = oracle_threshold(gamma);
+    for (int64_t b = 0; b < B; ++b) {
+        for (int64_t v = 0; v < V; ++v) {
+            if (oracle_is_green(key, (uint32_t)prev[b], (uint32_t)v, threshold, seeding)) {
+                uint16_t *l = &logits[b * row_stride + v];
+                *l = oracle_bias_bf16(*l, delta);
+            }
+        }
+    }
+}
+
+/* Green list G_t as a bit set: bit (v % 32) of word bits[b * ceil(V/32) + v/32]. */
+void oracle_green_mask(uint32_t *bits, int64_t B, int64_t V, const int32_t *prev,
+                       uint64_t key, double gamma, int seeding)
+{
+    uint64_t threshold = oracle_threshold(gamma);
+    int64_t words = (V + 31) / 32;
+    for (int64_t i = 0; i < B * words; ++i) bits[i] = 0u;
+    for (int64_t b = 0; b < B; ++b)
+        for (int64_t v = 0; v < V; ++v)
+            if (oracle_is_green(key, (uint32_t)prev[b], (uint32_t)v, threshold, seeding))
+                bits[b * words + v / 32] |= 1u << (v % 32);
+}
+
+/* ------------------------------------------------------------------------- */
+/* Detection, Sec. 2.2 (O(1) per-token test) and Sec. 3 (z-score).             */
+/* ------------------------------------------------------------------------- */
+
+/* z = (W - T*gamma) / sqrt(T*gamma*(1-gamma)) in binary64, Sec. 3. */
+double oracle_z_score(int64_t green_count, int64_t T, double gamma)
+{
+    double t = (double)T;
+    double numerator = (double)green_count - t * gamma;
+    double denominator = sqrt(t * gamma * (1.0 - gamma));
+    return numerator / denominator;
+}
+
+/* For each sequence n: W = #{ i in 1..L-1 : tok[i] in G(tok[i-1]) } (R6). */
+void oracle_detect(const int32_t *tokens, int64_t N, int64_t L, int64_t row_stride,
+                   uint64_t key, double gamma, int seeding, int32_t *green_counts,
+                   double *z)
+{
+    uint64_t threshold = oracle_threshold(gamma);
+    int64_t T = L > 1 ? L - 1 : 0;
+    for (int64_t n = 0; n < N; ++n) {
+        const int32_t *row = tokens + n * row_stride;
+        int64_t count = 0;
+        for (int64_t i = 1; i < L; ++i)
+            count += oracle_is_green(key, (uint32_t)row[i - 1], (uint32_t)row[i],
+                                     threshold, seeding);
+        green_counts[n] = (int32_t)count;
+        z[n] = oracle_z_score(count, T, gamma);
+    }
+}
+
+/* ------------------------------------------------------------------------- */
+/* Array forms of the scalar definitions above, for the tests.                 */
+/* ------------------------------------------------------------------------- */
+
+void oracle_cbrng_many(const uint32_t *v, const uint64_t *r, int64_t n, uint32_t *out)
+{
+    for (int64_t i = 0; i < n; ++i) out[i] = oracle_cbrng(v[i], r[i]);
+}
+
+void oracle_jenkins32_many(const uint32_t *a, int64_t n, uint32_t *out)
+{
+    for (int64_t i = 0; i < n; ++i) out[i] = oracle_jenkins32(a[i]);
+}
+
+void oracle_seed_many(uint64_t key, const int32_t *prev, const int32_t *cand, int64_t n,
+                      int seeding, uint64_t *out)
+{
+    for (int64_t i = 0; i < n; ++i)
+        out[i] = oracle_seed(key, (uint32_t)prev[i], (uint32_t)cand[i], seeding);
+}
+
+void oracle_bias_f32_many(const float *in, int64_t n, float delta, float *out)
+{
+    for (int64_t i = 0; i < n; ++i) out[i] = oracle_bias_f32(in[i], delta);
+}
+
+void oracle_bias_bf16_many(const uint16_t *in, int64_t n, float delta, uint16_t *out)
+{
+    for (int64_t i = 0; i < n; ++i) out[i] = oracle_bias_bf16(in[i], delta);
+}
+
+void oracle_f32_to_bf16_many(const float *in, int64_t n, uint16_t *out)
+{
+    for (int64_t i = 0; i < n; ++i) out[i] = oracle_f32_to_bf16(in[i]);
+}
