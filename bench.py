@@ -1,0 +1,246 @@
+"""Benchmark of the SBW hot path on one MI355X.
+
+One step = one pass of the whole hot path over one batch:
+  1. watermark, full-vocabulary self-salt, B=256 x V=152064 fp32 logits
+     (3*N(0,1) + 8 on 5 % of entries), gamma=0.25, delta=2, in place
+  2. watermark, context seeding, same shape and parameters
+  3. detect, self-salt, N=4096 x L=512 token ids over V=128256 (half null,
+     half watermarked)
+  4. detect, context seeding, the same batch shape
+Each launch is bracketed by HIP events on the stream it runs on.  Logits
+rotate over enough buffers (> 4 x 156 MB) that the 256 MB Infinity Cache cannot
+serve a launch from the previous one: every watermark launch reads HBM.
+
+`value` is the self-salt watermark throughput in Gelem/s (B*V / launch time),
+the configuration the metric names; the context-seeded launch (the HBM-bound
+one) and the detect launches are reported beside it.  All inputs are synthetic
+and resident in HBM before the timed region starts.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+import workloads  # noqa: E402
+
+HBM_PEAK_GBPS = 8000.0                 # MI355X HBM3E
+CUS, LANES, CLOCK_GHZ = 256, 64, 2.4   # MI355X compute units, wave width, peak clock
+# 32x32->64-bit products (v_mad_u64_u32) issue at a quarter of the full VALU rate.
+WIDE_MUL_PEAK_TOPS = CUS * LANES * CLOCK_GHZ / 4 / 1000.0
+PHILOX_PRODUCTS_PER_BLOCK = 20        # 2 per round, 10 rounds
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--buffers", type=int, default=6)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    return ap.parse_args()
+
+
+def percentile(xs, q):
+    return float(np.percentile(np.asarray(xs), q))
+
+
+def gpu_membership(sbw, torch, dev, key, gamma, seeding):
+    """Green-list membership of (prev, cand) pairs through the library's detect
+    entry point: a 2-token sequence [prev, cand] scores 1 iff cand is green."""
+    def member(p, v):
+        pairs = torch.from_numpy(np.stack([p, v], axis=1).astype(np.int32)).to(dev)
+        counts, _ = sbw.detect(pairs, key, gamma, seeding)
+        return (counts == 1).cpu().numpy()
+    return member
+
+
+def cpu_baseline(x, prev, tok_ss, seconds):
+    """The CPU oracle, untuned and single-threaded, on a bounded sample."""
+    import oracle
+    c = workloads.C4
+    rows = 64
+    sample = np.ascontiguousarray(x[:rows])
+    p = prev[:rows]
+    passes, t0 = 0, time.perf_counter()
+    while True:
+        oracle.watermark(sample, p, workloads.PAPER_KEY, c["gamma"], c["delta"], "self_salt")
+        passes += 1
+        if time.perf_counter() - t0 >= 0.8 * seconds:
+            break
+    wm_s = time.perf_counter() - t0
+    det_passes, t1 = 0, time.perf_counter()
+    while True:
+        oracle.detect(tok_ss, workloads.PAPER_KEY, workloads.C5["gamma"], "self_salt")
+        det_passes += 1
+        if time.perf_counter() - t1 >= 0.2 * seconds:
+            break
+    det_s = time.perf_counter() - t1
+    elems = passes * rows * x.shape[1]
+    return {
+        "value": elems / wm_s / 1e9,
+        "unit": "Gelem/s",
+        "cores": 1,
+        "kind": "oracle",
+        "sample": (f"self-salt watermark of c4 rows 0-{rows - 1} (64 x {x.shape[1]} fp32), "
+                   f"{passes} passes in {wm_s:.1f} s; self-salt detect of the c5 batch "
+                   f"({tok_ss.shape[0]} x {tok_ss.shape[1]}), {det_passes} passes in {det_s:.1f} s"),
+        "detect_seq_per_s": det_passes * tok_ss.shape[0] / det_s,
+        "cpu": _cpu_model(),
+        "nproc": os.cpu_count(),
+    }
+
+
+def _cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU; --gpus must be 1",
+                          "n_gpus": args.gpus}))
+        sys.exit(2)
+
+    import torch
+    import paper_2609_03844_amd as sbw
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    c4, c5 = workloads.C4, workloads.C5
+    key = workloads.PAPER_KEY
+    B, V = c4["B"], c4["V"]
+
+    # --- inputs, resident in HBM before timing --------------------------------
+    x, prev = workloads.watermark_inputs("c4")
+    base = torch.from_numpy(x).to(dev)
+    bufs = [base.clone() for _ in range(args.buffers)]
+    prev_d = torch.from_numpy(prev).to(dev)
+    toks = {}
+    for seeding in ("self_salt", "context"):
+        member = gpu_membership(sbw, torch, dev, key, c5["gamma"], seeding)
+        toks[seeding] = workloads.detect_inputs(c5["N"], c5["L"], c5["V"], c5["gamma"],
+                                                c5["delta"], seeding, member)
+    tok_d = {s: torch.from_numpy(t).to(dev) for s, t in toks.items()}
+    counts = {s: torch.empty(c5["N"], dtype=torch.int32, device=dev) for s in toks}
+    zs = {s: torch.empty(c5["N"], dtype=torch.float64, device=dev) for s in toks}
+    torch.cuda.synchronize()
+
+    launches = [("wm_self_salt", "self_salt"), ("wm_context", "context"),
+                ("det_self_salt", "self_salt"), ("det_context", "context")]
+
+    def step(i, ev=None):
+        for k, (name, seeding) in enumerate(launches):
+            if ev is not None:
+                ev[k][0].record()
+            if name.startswith("wm"):
+                buf = bufs[(2 * i + k) % len(bufs)]
+                sbw.watermark(buf, prev_d, key, c4["gamma"], c4["delta"], seeding)
+            else:
+                sbw.detect(tok_d[seeding], key, c5["gamma"], seeding, counts=counts[seeding],
+                           z=zs[seeding])
+            if ev is not None:
+                ev[k][1].record()
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+
+    evs = [[[torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)]
+            for _ in launches] for _ in range(args.steps)]
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    t_start.record()
+    for i in range(args.steps):
+        step(i, evs[i])
+    t_end.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    total_ms = t_start.elapsed_time(t_end)
+    per = {name: [evs[i][k][0].elapsed_time(evs[i][k][1]) for i in range(args.steps)]
+           for k, (name, _) in enumerate(launches)}
+    mean_ms = {n: float(np.mean(v)) for n, v in per.items()}
+
+    elems = B * V
+    bytes_wm = 8 * elems + 4 * B          # read + write each logit, read prev tokens
+    bytes_det = 4 * c5["N"] * c5["L"] + 12 * c5["N"]
+
+    def wm_stats(name):
+        ms = mean_ms[name]
+        return {"gelem_per_s": elems / (ms * 1e-3) / 1e9,
+                "hbm_gbps": bytes_wm / (ms * 1e-3) / 1e9,
+                "hbm_frac": bytes_wm / (ms * 1e-3) / 1e9 / HBM_PEAK_GBPS,
+                "us_mean": ms * 1e3, "us_p50": percentile(per[name], 50) * 1e3,
+                "us_p95": percentile(per[name], 95) * 1e3, "us_p99": percentile(per[name], 99) * 1e3}
+
+    def det_stats(name):
+        ms = mean_ms[name]
+        return {"seq_per_s": c5["N"] / (ms * 1e-3), "us_mean": ms * 1e3,
+                "us_p50": percentile(per[name], 50) * 1e3,
+                "us_p99": percentile(per[name], 99) * 1e3,
+                "gbps": bytes_det / (ms * 1e-3) / 1e9}
+
+    ss = wm_stats("wm_self_salt")
+    ctx = wm_stats("wm_context")
+    ss_products = PHILOX_PRODUCTS_PER_BLOCK * elems / (mean_ms["wm_self_salt"] * 1e-3) / 1e12
+
+    out = {
+        "metric": "watermarked logits Gelem/s + achieved HBM GB/s (B=256,V=152064); detect seq/s",
+        "value": ss["gelem_per_s"],
+        "unit": "Gelem/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": total_ms / args.steps,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": ("c4: watermark B=256 x V=152064 fp32 logits 3*N(0,1)+8*[U<0.05], "
+                                "gamma=0.25, delta=2, full-vocabulary self-salt (value); context "
+                                "seeding at the same shape; detect c5 N=4096 x L=512, V=128256, "
+                                "both seedings"),
+                   "B": B, "V": V, "gamma": c4["gamma"], "delta": c4["delta"],
+                   "detect_N": c5["N"], "detect_L": c5["L"], "rotating_buffers": args.buffers,
+                   "parallelism": "single GPU"},
+        "hbm_gbps": ss["hbm_gbps"],
+        "detect_seq_per_s": det_stats("det_self_salt")["seq_per_s"],
+        "watermark": {"self_salt": ss, "context": ctx},
+        "detect": {"self_salt": det_stats("det_self_salt"), "context": det_stats("det_context")},
+        "roofline": {"bound": "alu", "kernel": "watermark_vec_kernel<float, self-salt>",
+                     "achieved": ss_products, "peak": WIDE_MUL_PEAK_TOPS,
+                     "unit": "T 32x32->64-bit products/s", "frac": ss_products / WIDE_MUL_PEAK_TOPS,
+                     "traffic": None,
+                     "algorithmic_per_launch": f"{PHILOX_PRODUCTS_PER_BLOCK} x B x V Philox products"},
+        "roofline_context": {"bound": "hbm", "kernel": "watermark_vec_kernel<float, context>",
+                             "achieved": ctx["hbm_gbps"], "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                             "frac": ctx["hbm_frac"], "traffic": None,
+                             "algorithmic_per_launch": f"{bytes_wm} bytes"},
+        "wall_s_timed": wall,
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(x, prev, toks["self_salt"], args.cpu_seconds)
+    print(json.dumps(out))
+
+
+if __name__ == "__main__":
+    main()

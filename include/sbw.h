@@ -1,0 +1,149 @@
+/*
+ * sbw.h -- C ABI of libsbw, the MI355X (gfx950) hot path of Stateless Bernoulli
+ * Watermarking ("Flip, Don't Shuffle", arXiv 2609.03844).
+ *
+ * Two operations, each one hand-written HIP kernel launch on the caller's stream:
+ *
+ *   watermark  For every row b of a decode batch and every token v of the
+ *              vocabulary: derive the seed r from the row's previous token (and,
+ *              for self-salt, from v), draw x = CBRNG(v, r), and add delta to the
+ *              logit when x < gamma (Sec. 2.2, Eq. 1 and Eq. 2; full-vocabulary
+ *              self-salt, Sec. 5.2).  In place, one read and one write per logit.
+ *   detect     For every sequence: count the positions whose token is green
+ *              under the seed of the token before it (O(1) per token, Sec. 2.2)
+ *              and return the count W and z = (W - T gamma)/sqrt(T gamma (1-gamma))
+ *              with T = L - 1 (Sec. 3).
+ *
+ * Definitions fixed by this library where the paper leaves them open:
+ *   CBRNG(v, r)   the v-th 32-bit output of the Philox4x32-10 stream keyed by r:
+ *                 word (v mod 4) of Philox4x32-10(key = (lo32 r, hi32 r),
+ *                 counter = (floor(v/4), 0, 0, 0))  (Sec. 2.2).
+ *   x < gamma     x < ceil(gamma * 2^32), the exact comparison x * 2^-32 < gamma.
+ *   context seed  r = key * p mod 2^64, p = previous token as uint32
+ *                 ("additive" PRF of width 1, scheme table of App. D).
+ *   self-salt     r = min_u64(key*J(p)*J(v), key*J(v)*J(v)) mod 2^64, J = Robert
+ *                 Jenkins' 32-bit integer hash (Sec. 2.3), unsigned minimum
+ *                 ("anchored minhash" over {p, v} anchored on v, App. D).
+ *   bias          fp32: l + delta, one fp32 add rounded to nearest even.
+ *                 bf16: round-to-nearest-even bf16 of (fp32(l) + delta); NaN
+ *                 stays NaN.  Tokens not in the green list keep their bits.
+ *
+ * Conventions shared by every entry point:
+ *   - Buffers belong to the caller.  Device pointers are HIP device (or managed)
+ *     memory; the library allocates nothing, on host or device (App. E, memory).
+ *   - Work is enqueued on `stream` (a hipStream_t; NULL = the null stream) and the
+ *     call returns without synchronising the host.  Functions hold no global
+ *     mutable state and are reentrant.
+ *   - All arguments are checked on the host before any HIP call, so an error
+ *     return means nothing was enqueued.  Token values are not checked (that
+ *     would need a device read): every definition holds for any 32-bit pattern.
+ *   - Empty work (B, V, N == 0) returns SBW_OK without a HIP call.
+ *   - SBW_ERR_NO_DEVICE: no usable HIP device.  SBW_ERR_HIP: a HIP call or the
+ *     kernel launch failed; sbw_last_hip_error() then names the HIP error of the
+ *     calling thread.
+ */
+#ifndef SBW_H
+#define SBW_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    SBW_SEED_CONTEXT = 0,   /* seed from the previous token only          */
+    SBW_SEED_SELF_SALT = 1  /* seed from the previous token and candidate */
+} sbw_seeding_t;
+
+typedef enum {
+    SBW_F32 = 0,            /* IEEE binary32 logits                        */
+    SBW_BF16 = 1            /* bfloat16 logits (upper half of binary32)    */
+} sbw_dtype_t;
+
+typedef enum {
+    SBW_OK = 0,
+    SBW_ERR_INVALID_ARG = 1, /* null pointer, negative size, stride too small */
+    SBW_ERR_GAMMA = 2,       /* gamma outside the allowed range              */
+    SBW_ERR_DELTA = 3,       /* delta not finite                            */
+    SBW_ERR_UNSUPPORTED = 4, /* unknown enum value, or sizes beyond limits   */
+    SBW_ERR_NO_DEVICE = 5,   /* no HIP device                                */
+    SBW_ERR_HIP = 6          /* HIP runtime or launch error                  */
+} sbw_status_t;
+
+/*
+ * sbw_watermark -- bias the green tokens of every row, in place
+ * (Sec. 2.2, Eq. 1 and Eq. 2; full-vocabulary self-salt, Sec. 5.2).
+ *
+ *   logits       device, [B, row_stride] elements of `dtype`; element (b, v) is
+ *                logits[b * row_stride + v] for b < B, v < V.  Read and written.
+ *                Elements with v >= V are neither read nor written.
+ *   dtype        SBW_F32 or SBW_BF16.
+ *   B, V         rows and vocabulary size; 0 is a no-op.  V < 2^32 (token ids are
+ *                32-bit), else SBW_ERR_UNSUPPORTED.
+ *   row_stride   elements between row starts, >= V.
+ *   prev_tokens  device, [B] int32: the token generated before this step, per row.
+ *   key          the 64-bit watermark key.
+ *   gamma        green-list fraction, 0 <= gamma <= 1 (0: nothing is green, the
+ *                call is a no-op; 1: everything is green).  Else SBW_ERR_GAMMA.
+ *   delta        bias added to green logits; must be finite, else SBW_ERR_DELTA.
+ *   seeding      SBW_SEED_CONTEXT or SBW_SEED_SELF_SALT.
+ *   stream       hipStream_t to enqueue on.
+ *
+ * Rows whose start is 16-byte aligned take 128-bit loads and stores; other
+ * layouts are correct but slower.
+ */
+sbw_status_t sbw_watermark(void *logits, sbw_dtype_t dtype, int64_t B, int64_t V,
+                           int64_t row_stride, const int32_t *prev_tokens, uint64_t key,
+                           double gamma, float delta, sbw_seeding_t seeding, void *stream);
+
+/*
+ * sbw_green_mask -- the green list G_t of every row as a bit set (Sec. 2.2, Eq. 1).
+ * A parity and debugging aid: the watermark never materialises it.
+ *
+ *   bits         device, [B, ceil(V/32)] uint32, written: bit (v % 32) of word
+ *                bits[b * ceil(V/32) + v / 32] is 1 iff v is green in row b.
+ *                Bits for v >= V in the last word of a row are 0.
+ *   B, V, prev_tokens, key, seeding   as for sbw_watermark.
+ *   gamma        0 <= gamma <= 1, else SBW_ERR_GAMMA.
+ */
+sbw_status_t sbw_green_mask(uint32_t *bits, int64_t B, int64_t V, const int32_t *prev_tokens,
+                            uint64_t key, double gamma, sbw_seeding_t seeding, void *stream);
+
+/*
+ * sbw_detect -- green count and z-score of every sequence (Sec. 2.2, O(1)
+ * membership per token; Sec. 3, z-score).
+ *
+ *   tokens       device, [N, row_stride] int32; sequence n is tokens[n*row_stride
+ *                + i], i < L.  May be NULL when L == 0.
+ *   N, L         sequences and tokens per sequence; N == 0 is a no-op.  Positions
+ *                1..L-1 are scored, each under the seed of the token before it,
+ *                so T = L - 1; for L < 2, T = 0, the count is 0 and z is NaN.
+ *   row_stride   elements between sequence starts, >= L.
+ *   key, seeding as for sbw_watermark.
+ *   gamma        0 < gamma < 1 (the z-score is undefined otherwise), else
+ *                SBW_ERR_GAMMA.
+ *   green_counts device, [N] int32, written: W per sequence.
+ *   z            device, [N] double, written: (W - T*gamma) / sqrt(T*gamma*(1-gamma)),
+ *                evaluated in binary64 in that order.
+ *   L is limited to 2^31 - 1 (SBW_ERR_UNSUPPORTED beyond).
+ */
+sbw_status_t sbw_detect(const int32_t *tokens, int64_t N, int64_t L, int64_t row_stride,
+                        uint64_t key, double gamma, sbw_seeding_t seeding,
+                        int32_t *green_counts, double *z, void *stream);
+
+/* Static description of a status code (never NULL). */
+const char *sbw_strerror(sbw_status_t status);
+
+/* Name of the last HIP error seen by an sbw_* call on the calling thread, or
+ * "hipSuccess".  Thread-local; not reset by later successful calls. */
+const char *sbw_last_hip_error(void);
+
+/* Library version string, "MAJOR.MINOR.PATCH". */
+const char *sbw_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SBW_H */

@@ -1,0 +1,183 @@
+"""Stateless Bernoulli Watermarking on MI355X (gfx950): Python binding of libsbw.
+
+A thin ctypes layer over the C ABI in ``include/sbw.h``; it only marshals
+arguments (device pointers, sizes, the current HIP stream).  Every step of the
+watermark and detect path runs in the HIP kernels of ``libsbw.so``.  There is no
+fallback: if the library is missing this module raises on import.
+
+    watermark(logits, prev_tokens, key, gamma, delta, seeding="context")   in place
+    green_mask(prev_tokens, V, key, gamma, seeding="context") -> int32 [B, ceil(V/32)]
+    detect(tokens, key, gamma, seeding="context") -> (counts int32 [N], z float64 [N])
+
+Tensors are torch tensors on the current HIP device; torch provides the memory
+and the stream, nothing else.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch  # loads torch's HIP runtime first, so libsbw binds to the same one
+
+from ._build import LIBRARY, build  # noqa: F401  (build is re-exported)
+
+__all__ = ["watermark", "green_mask", "detect", "SbwError", "version", "library_path",
+           "SEED_CONTEXT", "SEED_SELF_SALT"]
+
+SEED_CONTEXT = 0
+SEED_SELF_SALT = 1
+F32 = 0
+BF16 = 1
+
+_STATUS = {
+    0: "SBW_OK",
+    1: "SBW_ERR_INVALID_ARG",
+    2: "SBW_ERR_GAMMA",
+    3: "SBW_ERR_DELTA",
+    4: "SBW_ERR_UNSUPPORTED",
+    5: "SBW_ERR_NO_DEVICE",
+    6: "SBW_ERR_HIP",
+}
+
+EXPORTED = ("sbw_watermark", "sbw_green_mask", "sbw_detect", "sbw_strerror",
+            "sbw_last_hip_error", "sbw_version")
+
+
+class SbwError(RuntimeError):
+    def __init__(self, status: int, message: str, hip_error: str | None = None):
+        self.status = status
+        self.code = _STATUS.get(status, str(status))
+        self.hip_error = hip_error
+        text = f"{self.code}: {message}"
+        if hip_error and hip_error != "hipSuccess":
+            text += f" ({hip_error})"
+        super().__init__(text)
+
+
+def _load() -> ctypes.CDLL:
+    if not os.path.exists(LIBRARY):
+        raise ImportError(f"libsbw.so not built at {LIBRARY}; run __graft_entry__.build() "
+                          "or python -m paper_2609_03844_amd._build")
+    lib = ctypes.CDLL(LIBRARY)
+    P, i64, u64, f64, f32, i32 = (ctypes.c_void_p, ctypes.c_int64, ctypes.c_uint64,
+                                  ctypes.c_double, ctypes.c_float, ctypes.c_int)
+    lib.sbw_watermark.restype = i32
+    lib.sbw_watermark.argtypes = [P, i32, i64, i64, i64, P, u64, f64, f32, i32, P]
+    lib.sbw_green_mask.restype = i32
+    lib.sbw_green_mask.argtypes = [P, i64, i64, P, u64, f64, i32, P]
+    lib.sbw_detect.restype = i32
+    lib.sbw_detect.argtypes = [P, i64, i64, i64, u64, f64, i32, P, P, P]
+    lib.sbw_strerror.restype = ctypes.c_char_p
+    lib.sbw_strerror.argtypes = [i32]
+    lib.sbw_last_hip_error.restype = ctypes.c_char_p
+    lib.sbw_last_hip_error.argtypes = []
+    lib.sbw_version.restype = ctypes.c_char_p
+    lib.sbw_version.argtypes = []
+    return lib
+
+
+_lib = _load()
+
+
+def library_path() -> str:
+    return LIBRARY
+
+
+def version() -> str:
+    return _lib.sbw_version().decode()
+
+
+def raw() -> ctypes.CDLL:
+    """The ctypes handle of libsbw (the C ABI itself)."""
+    return _lib
+
+
+def _check(status: int) -> None:
+    if status != 0:
+        hip = _lib.sbw_last_hip_error().decode() if status == 6 else None
+        raise SbwError(status, _lib.sbw_strerror(status).decode(), hip)
+
+
+def _seeding(s) -> int:
+    if isinstance(s, str):
+        return {"context": SEED_CONTEXT, "self_salt": SEED_SELF_SALT}[s]
+    return int(s)
+
+
+def _stream(stream) -> int:
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+
+
+def _key(key: int) -> int:
+    return int(key) & 0xFFFFFFFFFFFFFFFF
+
+
+def watermark(logits: torch.Tensor, prev_tokens: torch.Tensor, key: int, gamma: float,
+              delta: float, seeding="context", stream=None) -> torch.Tensor:
+    """Adds delta to the green logits of every row, in place; returns ``logits``.
+
+    logits: [B, V] float32 or bfloat16 on the GPU, unit stride along V (rows may be
+    padded: stride(0) >= V).  prev_tokens: [B] int32 on the same device.
+    """
+    if logits.dim() != 2:
+        raise ValueError("logits must be [B, V]")
+    if logits.dtype == torch.float32:
+        dtype = F32
+    elif logits.dtype == torch.bfloat16:
+        dtype = BF16
+    else:
+        raise TypeError("logits must be float32 or bfloat16")
+    B, V = logits.shape
+    if B > 0 and V > 0 and logits.stride(1) != 1:
+        raise ValueError("logits must have unit stride along the vocabulary")
+    if prev_tokens.dtype != torch.int32 or prev_tokens.dim() != 1 or prev_tokens.shape[0] != B:
+        raise ValueError("prev_tokens must be int32 [B]")
+    if B > 0 and not prev_tokens.is_contiguous():
+        raise ValueError("prev_tokens must be contiguous")
+    row_stride = logits.stride(0) if B > 1 else max(V, logits.stride(0))
+    _check(_lib.sbw_watermark(logits.data_ptr(), dtype, B, V, row_stride,
+                              prev_tokens.data_ptr(), _key(key), float(gamma), float(delta),
+                              _seeding(seeding), _stream(stream)))
+    return logits
+
+
+def green_mask(prev_tokens: torch.Tensor, V: int, key: int, gamma: float, seeding="context",
+               out: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    """Green lists as bit sets: int32 [B, ceil(V/32)], bit v%32 of word v//32."""
+    if prev_tokens.dtype != torch.int32 or prev_tokens.dim() != 1:
+        raise ValueError("prev_tokens must be int32 [B]")
+    B = prev_tokens.shape[0]
+    words = (int(V) + 31) // 32
+    if out is None:
+        out = torch.empty((B, words), dtype=torch.int32, device=prev_tokens.device)
+    elif out.shape != (B, words) or out.dtype != torch.int32 or not out.is_contiguous():
+        raise ValueError("out must be contiguous int32 [B, ceil(V/32)]")
+    _check(_lib.sbw_green_mask(out.data_ptr(), B, int(V), prev_tokens.data_ptr(), _key(key),
+                               float(gamma), _seeding(seeding), _stream(stream)))
+    return out
+
+
+def detect(tokens: torch.Tensor, key: int, gamma: float, seeding="context",
+           counts: torch.Tensor | None = None, z: torch.Tensor | None = None, stream=None):
+    """Green count and z-score per sequence of tokens [N, L] int32 (unit stride along L)."""
+    if tokens.dtype != torch.int32 or tokens.dim() != 2:
+        raise ValueError("tokens must be int32 [N, L]")
+    N, L = tokens.shape
+    if N > 0 and L > 0 and tokens.stride(1) != 1:
+        raise ValueError("tokens must have unit stride along L")
+    dev = tokens.device
+    if counts is None:
+        counts = torch.empty(N, dtype=torch.int32, device=dev)
+    if z is None:
+        z = torch.empty(N, dtype=torch.float64, device=dev)
+    if counts.shape != (N,) or counts.dtype != torch.int32 or not counts.is_contiguous():
+        raise ValueError("counts must be contiguous int32 [N]")
+    if z.shape != (N,) or z.dtype != torch.float64 or not z.is_contiguous():
+        raise ValueError("z must be contiguous float64 [N]")
+    row_stride = tokens.stride(0) if N > 1 else max(L, tokens.stride(0))
+    _check(_lib.sbw_detect(tokens.data_ptr() if L > 0 else None, N, L, row_stride, _key(key),
+                           float(gamma), _seeding(seeding), counts.data_ptr(), z.data_ptr(),
+                           _stream(stream)))
+    return counts, z

@@ -1,0 +1,119 @@
+// Device-side primitives of the SBW hot path for gfx950: Philox4x32-10, the
+// Jenkins integer hash, the two seeding schemes, the membership test and the
+// bias arithmetic.  Everything is register-resident; nothing touches LDS or
+// global memory.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace sbw {
+
+// Philox4x32-10 round multipliers and key increments (Salmon et al., SC'11),
+// the CBRNG of Sec. 2.2.
+constexpr uint32_t kPhiloxMulA = 0xD2511F53u;  // multiplies counter word 0
+constexpr uint32_t kPhiloxMulB = 0xCD9E8D57u;  // multiplies counter word 2
+constexpr uint32_t kPhiloxWeyl0 = 0x9E3779B9u;
+constexpr uint32_t kPhiloxWeyl1 = 0xBB67AE85u;
+
+enum Seeding : int { kContext = 0, kSelfSalt = 1 };
+
+struct Key {
+  uint32_t lo, hi;
+};
+
+__device__ __forceinline__ Key key_of(uint64_t r) {
+  return Key{static_cast<uint32_t>(r), static_cast<uint32_t>(r >> 32)};
+}
+
+// 32 x 32 -> 64-bit product.  Written as a widening multiply so the backend can
+// use v_mad_u64_u32 (one instruction for both halves).
+__device__ __forceinline__ uint64_t wide_mul(uint32_t a, uint32_t b) {
+  return static_cast<uint64_t>(a) * static_cast<uint64_t>(b);
+}
+
+// Philox4x32-10 of the block at counter (c0, 0, 0, 0).  The three zero counter
+// words are constants, so the first round's product of word 2 folds away.  Only
+// the words the caller reads survive dead-code elimination of the last round.
+struct Block {
+  uint32_t w0, w1, w2, w3;
+};
+
+__device__ __forceinline__ Block philox_block(uint32_t c0, Key k) {
+  uint32_t x0 = c0, x1 = 0u, x2 = 0u, x3 = 0u;
+  uint32_t k0 = k.lo, k1 = k.hi;
+#pragma unroll
+  for (int round = 0; round < 10; ++round) {
+    const uint64_t pa = wide_mul(kPhiloxMulA, x0);
+    const uint64_t pb = wide_mul(kPhiloxMulB, x2);
+    const uint32_t y0 = static_cast<uint32_t>(pb >> 32) ^ x1 ^ k0;
+    const uint32_t y1 = static_cast<uint32_t>(pb);
+    const uint32_t y2 = static_cast<uint32_t>(pa >> 32) ^ x3 ^ k1;
+    const uint32_t y3 = static_cast<uint32_t>(pa);
+    x0 = y0; x1 = y1; x2 = y2; x3 = y3;
+    k0 += kPhiloxWeyl0;
+    k1 += kPhiloxWeyl1;
+  }
+  return Block{x0, x1, x2, x3};
+}
+
+__device__ __forceinline__ uint32_t block_word(const Block& b, uint32_t i) {
+  // i in [0, 4); a select chain, no dynamic register indexing.
+  const uint32_t lo = (i & 1u) ? b.w1 : b.w0;
+  const uint32_t hi = (i & 1u) ? b.w3 : b.w2;
+  return (i & 2u) ? hi : lo;
+}
+
+// CBRNG(v, r): position v of the Philox stream keyed by r (Sec. 2.2).
+__device__ __forceinline__ uint32_t cbrng(uint32_t v, uint64_t r) {
+  return block_word(philox_block(v >> 2, key_of(r)), v & 3u);
+}
+
+// Robert Jenkins' 32-bit integer hash (Sec. 2.3): six add/xor-shift steps.
+__device__ __forceinline__ uint32_t jenkins32(uint32_t a) {
+  a = (a + 0x7ed55d16u) + (a << 12);
+  a = (a ^ 0xc761c23cu) ^ (a >> 19);
+  a = (a + 0x165667b1u) + (a << 5);
+  a = (a + 0xd3a2646cu) ^ (a << 9);
+  a = (a + 0xfd7046c5u) + (a << 3);
+  a = (a ^ 0xb55a4f09u) ^ (a >> 16);
+  return a;
+}
+
+// Context seed: r = key * p mod 2^64.
+__device__ __forceinline__ uint64_t context_seed(uint64_t key, uint32_t p) {
+  return key * static_cast<uint64_t>(p);
+}
+
+// Self-salt seed with the row part precomputed: key_jp = key * J(p) mod 2^64.
+// r = min_u64(key*J(p)*J(v), key*J(v)*J(v)).
+__device__ __forceinline__ uint64_t self_salt_seed(uint64_t key, uint64_t key_jp,
+                                                   uint32_t v) {
+  const uint64_t jv = jenkins32(v);
+  const uint64_t with_prev = key_jp * jv;
+  const uint64_t with_self = (key * jv) * jv;
+  return with_prev < with_self ? with_prev : with_self;
+}
+
+// Membership: x < T with T = threshold_minus_1 + 1 in [1, 2^32].  T == 0 (gamma
+// == 0) never reaches a kernel that calls this.
+__device__ __forceinline__ bool is_green(uint32_t x, uint32_t threshold_minus_1) {
+  return x <= threshold_minus_1;
+}
+
+// fp32 bias: one IEEE add (the build disables contraction and keeps denormals),
+// and a select so that non-green values keep their exact bits.
+__device__ __forceinline__ float bias_f32(float l, float delta, bool green) {
+  return green ? l + delta : l;
+}
+
+// bf16 bias: exact widening, one fp32 add, round to nearest even; NaN stays NaN.
+__device__ __forceinline__ uint16_t bias_bf16(uint16_t l, float delta, bool green) {
+  const float s = __uint_as_float(static_cast<uint32_t>(l) << 16) + delta;
+  const uint32_t u = __float_as_uint(s);
+  const uint32_t rounded = (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
+  const uint32_t out = (s != s) ? ((u >> 16) | 0x40u) : rounded;
+  return green ? static_cast<uint16_t>(out) : l;
+}
+
+}  // namespace sbw

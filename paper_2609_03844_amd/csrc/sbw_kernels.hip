@@ -1,0 +1,451 @@
+// HIP kernels and C ABI of libsbw (declared in include/sbw.h) for MI355X / gfx950.
+//
+// watermark   one streaming pass over the logits: each lane owns 16-byte vectors
+//             of one row (4 fp32 or 8 bf16 logits), loads them, derives the green
+//             decision in registers (seed, Philox4x32-10 draw, threshold compare)
+//             and stores them back.  Row-uniform values (previous token, context
+//             seed, key * J(p)) are computed once per workgroup in scalar
+//             registers.  Context seeding shares one Philox block between the 4
+//             tokens of a counter; self-salt needs one block per token.
+// green_mask  one lane per 32-token word of the bit set.
+// detect      one wavefront per sequence; each lane scores positions i, i+64, ...
+//             and the wave counts green positions with a ballot + popcount.
+#include <hip/hip_runtime.h>
+#include <math.h>
+#include <stdint.h>
+
+#include "sbw.h"
+#include "sbw_device.hpp"
+
+namespace sbw {
+namespace {
+
+constexpr int kThreads = 256;     // 4 wavefronts of 64
+constexpr int kUnroll = 4;        // 16-byte vectors in flight per lane
+constexpr int64_t kMaxGrid = 1ll << 20;  // blocks; grid-stride loops cover the rest
+
+// Per-row state shared by all lanes of a workgroup.
+struct RowSeed {
+  uint64_t key;      // the watermark key
+  uint64_t seed;     // context: key * p;  self-salt: key * J(p)
+};
+
+template <int kSeeding>
+__device__ __forceinline__ RowSeed row_seed(uint64_t key, uint32_t prev) {
+  if (kSeeding == kContext) return RowSeed{key, context_seed(key, prev)};
+  return RowSeed{key, key * static_cast<uint64_t>(jenkins32(prev))};
+}
+
+template <int kSeeding>
+__device__ __forceinline__ uint32_t draw(const RowSeed& rs, uint32_t v) {
+  if (kSeeding == kContext) return cbrng(v, rs.seed);
+  return cbrng(v, self_salt_seed(rs.key, rs.seed, v));
+}
+
+// ---------------------------------------------------------------------------
+// Watermark, fp32, rows 16-byte aligned: a vector is the 4 tokens 4j..4j+3,
+// exactly the 4 words of the Philox block at counter j.
+// ---------------------------------------------------------------------------
+template <int kSeeding>
+__device__ __forceinline__ float4 bias_vec_f32(float4 l, uint32_t j, const RowSeed& rs,
+                                               uint32_t tm1, float delta) {
+  const uint32_t v = j * 4u;
+  uint32_t x0, x1, x2, x3;
+  if (kSeeding == kContext) {
+    const Block blk = philox_block(j, key_of(rs.seed));
+    x0 = blk.w0; x1 = blk.w1; x2 = blk.w2; x3 = blk.w3;
+  } else {
+    x0 = philox_block(j, key_of(self_salt_seed(rs.key, rs.seed, v + 0u))).w0;
+    x1 = philox_block(j, key_of(self_salt_seed(rs.key, rs.seed, v + 1u))).w1;
+    x2 = philox_block(j, key_of(self_salt_seed(rs.key, rs.seed, v + 2u))).w2;
+    x3 = philox_block(j, key_of(self_salt_seed(rs.key, rs.seed, v + 3u))).w3;
+  }
+  float4 o;
+  o.x = bias_f32(l.x, delta, is_green(x0, tm1));
+  o.y = bias_f32(l.y, delta, is_green(x1, tm1));
+  o.z = bias_f32(l.z, delta, is_green(x2, tm1));
+  o.w = bias_f32(l.w, delta, is_green(x3, tm1));
+  return o;
+}
+
+// bf16: a vector is the 8 tokens 8j..8j+7 = Philox blocks 2j and 2j+1.
+template <int kSeeding>
+__device__ __forceinline__ uint4 bias_vec_bf16(uint4 raw, uint32_t j, const RowSeed& rs,
+                                               uint32_t tm1, float delta) {
+  const uint32_t v = j * 8u;
+  uint32_t x[8];
+  if (kSeeding == kContext) {
+    const Key k = key_of(rs.seed);
+    const Block a = philox_block(2u * j, k);
+    const Block b = philox_block(2u * j + 1u, k);
+    x[0] = a.w0; x[1] = a.w1; x[2] = a.w2; x[3] = a.w3;
+    x[4] = b.w0; x[5] = b.w1; x[6] = b.w2; x[7] = b.w3;
+  } else {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const uint32_t t = v + static_cast<uint32_t>(e);
+      x[e] = block_word(philox_block(t >> 2, key_of(self_salt_seed(rs.key, rs.seed, t))),
+                        static_cast<uint32_t>(e & 3));
+    }
+  }
+  const uint32_t in[4] = {raw.x, raw.y, raw.z, raw.w};
+  uint32_t out[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const uint16_t lo = bias_bf16(static_cast<uint16_t>(in[q]), delta, is_green(x[2 * q], tm1));
+    const uint16_t hi =
+        bias_bf16(static_cast<uint16_t>(in[q] >> 16), delta, is_green(x[2 * q + 1], tm1));
+    out[q] = static_cast<uint32_t>(lo) | (static_cast<uint32_t>(hi) << 16);
+  }
+  return uint4{out[0], out[1], out[2], out[3]};
+}
+
+// One element of either dtype (row tails and unaligned rows).
+template <typename T>
+struct Elem;
+template <>
+struct Elem<float> {
+  static __device__ __forceinline__ float bias(float l, float d, bool g) { return bias_f32(l, d, g); }
+};
+template <>
+struct Elem<uint16_t> {
+  static __device__ __forceinline__ uint16_t bias(uint16_t l, float d, bool g) {
+    return bias_bf16(l, d, g);
+  }
+};
+
+template <typename T, int kSeeding>
+__device__ __forceinline__ void bias_one(T* row, uint32_t v, const RowSeed& rs, uint32_t tm1,
+                                         float delta) {
+  const uint32_t x = draw<kSeeding>(rs, v);
+  row[v] = Elem<T>::bias(row[v], delta, is_green(x, tm1));
+}
+
+// Vectorised watermark for rows whose start is 16-byte aligned.
+//   VecT: float4 (fp32, 4 per vector) or uint4 (bf16, 8 per vector).
+template <typename T, int kSeeding>
+__global__ void __launch_bounds__(kThreads)
+watermark_vec_kernel(T* __restrict__ logits, int64_t row_stride, uint32_t V,
+                     const int32_t* __restrict__ prev, uint64_t key, uint32_t tm1, float delta,
+                     uint32_t tiles_per_row, int64_t num_tiles) {
+  constexpr uint32_t kPer = 16u / sizeof(T);  // elements per 16-byte vector
+  const uint32_t full = V / kPer;             // complete vectors in a row
+  const uint32_t tail = V % kPer;
+  for (int64_t tile = blockIdx.x; tile < num_tiles; tile += gridDim.x) {
+    const int64_t row = tile / tiles_per_row;
+    const uint32_t first = static_cast<uint32_t>(tile - row * tiles_per_row) *
+                           (kThreads * kUnroll);
+    const RowSeed rs = row_seed<kSeeding>(key, static_cast<uint32_t>(prev[row]));
+    T* row_ptr = logits + row * row_stride;
+
+    if constexpr (sizeof(T) == 4) {
+      float4* vec = reinterpret_cast<float4*>(row_ptr);
+      float4 buf[kUnroll];
+#pragma unroll
+      for (int u = 0; u < kUnroll; ++u) {
+        const uint32_t j = first + u * kThreads + threadIdx.x;
+        if (j < full) buf[u] = vec[j];
+      }
+#pragma unroll
+      for (int u = 0; u < kUnroll; ++u) {
+        const uint32_t j = first + u * kThreads + threadIdx.x;
+        if (j < full) vec[j] = bias_vec_f32<kSeeding>(buf[u], j, rs, tm1, delta);
+      }
+    } else {
+      uint4* vec = reinterpret_cast<uint4*>(row_ptr);
+      uint4 buf[kUnroll];
+#pragma unroll
+      for (int u = 0; u < kUnroll; ++u) {
+        const uint32_t j = first + u * kThreads + threadIdx.x;
+        if (j < full) buf[u] = vec[j];
+      }
+#pragma unroll
+      for (int u = 0; u < kUnroll; ++u) {
+        const uint32_t j = first + u * kThreads + threadIdx.x;
+        if (j < full) vec[j] = bias_vec_bf16<kSeeding>(buf[u], j, rs, tm1, delta);
+      }
+    }
+    // The partial vector at the end of the row, element by element.
+    // Lane 0 of the tile that covers vector index `full` handles it.
+    if (tail != 0u && threadIdx.x == 0 && full >= first &&
+        full - first < static_cast<uint32_t>(kThreads * kUnroll)) {
+      for (uint32_t e = 0; e < tail; ++e)
+        bias_one<T, kSeeding>(row_ptr, full * kPer + e, rs, tm1, delta);
+    }
+  }
+}
+
+// Element-wise watermark for rows that are not 16-byte aligned.
+template <typename T, int kSeeding>
+__global__ void __launch_bounds__(kThreads)
+watermark_elem_kernel(T* __restrict__ logits, int64_t row_stride, uint32_t V,
+                      const int32_t* __restrict__ prev, uint64_t key, uint32_t tm1, float delta,
+                      uint32_t tiles_per_row, int64_t num_tiles) {
+  for (int64_t tile = blockIdx.x; tile < num_tiles; tile += gridDim.x) {
+    const int64_t row = tile / tiles_per_row;
+    const uint64_t v64 = static_cast<uint64_t>(tile - row * tiles_per_row) * kThreads + threadIdx.x;
+    if (v64 >= V) continue;
+    const RowSeed rs = row_seed<kSeeding>(key, static_cast<uint32_t>(prev[row]));
+    bias_one<T, kSeeding>(logits + row * row_stride, static_cast<uint32_t>(v64), rs, tm1, delta);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Green mask: one lane per 32-bit word (tokens 32w .. 32w+31).
+// ---------------------------------------------------------------------------
+template <int kSeeding>
+__global__ void __launch_bounds__(kThreads)
+green_mask_kernel(uint32_t* __restrict__ bits, uint32_t V, uint32_t words_per_row,
+                  const int32_t* __restrict__ prev, uint64_t key, uint32_t tm1, int none_green,
+                  int64_t num_words) {
+  for (int64_t w = static_cast<int64_t>(blockIdx.x) * kThreads + threadIdx.x; w < num_words;
+       w += static_cast<int64_t>(gridDim.x) * kThreads) {
+    const int64_t row = w / words_per_row;
+    const uint32_t word = static_cast<uint32_t>(w - row * words_per_row);
+    uint32_t out = 0u;
+    if (!none_green) {
+      const RowSeed rs = row_seed<kSeeding>(key, static_cast<uint32_t>(prev[row]));
+      const uint32_t v0 = word * 32u;
+      if (kSeeding == kContext) {
+        const Key k = key_of(rs.seed);
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+          const Block blk = philox_block(v0 / 4u + q, k);
+          const uint32_t xs[4] = {blk.w0, blk.w1, blk.w2, blk.w3};
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            out |= static_cast<uint32_t>(is_green(xs[e], tm1)) << (4 * q + e);
+        }
+      } else {
+#pragma unroll 4
+        for (int e = 0; e < 32; ++e)
+          out |= static_cast<uint32_t>(is_green(draw<kSeeding>(rs, v0 + e), tm1)) << e;
+      }
+      const uint32_t valid = V - v0;  // >= 1 for every word of the row
+      if (valid < 32u) out &= (1u << valid) - 1u;
+    }
+    bits[w] = out;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Detect: one wavefront per sequence, ballot + popcount.
+// ---------------------------------------------------------------------------
+constexpr int kWave = 64;
+constexpr int kWavesPerBlock = kThreads / kWave;
+
+template <int kSeeding>
+__global__ void __launch_bounds__(kThreads)
+detect_kernel(const int32_t* __restrict__ tokens, int64_t N, int64_t L, int64_t row_stride,
+              uint64_t key, uint32_t tm1, double gamma, int32_t* __restrict__ counts,
+              double* __restrict__ z) {
+  const int lane = threadIdx.x % kWave;
+  const int64_t wave0 = static_cast<int64_t>(blockIdx.x) * kWavesPerBlock + threadIdx.x / kWave;
+  for (int64_t n = wave0; n < N; n += static_cast<int64_t>(gridDim.x) * kWavesPerBlock) {
+    const int32_t* seq = tokens + n * row_stride;
+    uint32_t green = 0u;  // wave-uniform count
+    for (int64_t base = 1; base < L; base += kWave) {
+      const int64_t i = base + lane;
+      bool g = false;
+      if (i < L) {
+        const uint32_t p = static_cast<uint32_t>(seq[i - 1]);
+        const uint32_t v = static_cast<uint32_t>(seq[i]);
+        uint64_t r;
+        if (kSeeding == kContext) {
+          r = context_seed(key, p);
+        } else {
+          r = self_salt_seed(key, key * static_cast<uint64_t>(jenkins32(p)), v);
+        }
+        g = is_green(cbrng(v, r), tm1);
+      }
+      green += static_cast<uint32_t>(__popcll(__ballot(g)));
+    }
+    if (lane == 0) {
+      const int64_t T = L > 1 ? L - 1 : 0;
+      const double t = static_cast<double>(T);
+      const double numerator = static_cast<double>(green) - t * gamma;
+      const double denominator = sqrt(t * gamma * (1.0 - gamma));
+      counts[n] = static_cast<int32_t>(green);
+      z[n] = numerator / denominator;
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Host side.
+// ---------------------------------------------------------------------------
+thread_local hipError_t g_last_hip_error = hipSuccess;
+
+// ceil(gamma * 2^32) clamped to [0, 2^32] (the scaling by 2^32 is exact).
+uint64_t threshold_of(double gamma) {
+  const double scaled = ceil(gamma * 4294967296.0);
+  if (!(scaled > 0.0)) return 0u;
+  if (scaled >= 4294967296.0) return 4294967296ull;
+  return static_cast<uint64_t>(scaled);
+}
+
+sbw_status_t check_device() {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) {
+    g_last_hip_error = e;
+    (void)hipGetLastError();
+    return SBW_ERR_NO_DEVICE;
+  }
+  return SBW_OK;
+}
+
+sbw_status_t after_launch() {
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) {
+    g_last_hip_error = e;
+    return SBW_ERR_HIP;
+  }
+  return SBW_OK;
+}
+
+int64_t grid_for(int64_t work_groups) { return work_groups < kMaxGrid ? work_groups : kMaxGrid; }
+
+bool valid_seeding(int s) { return s == SBW_SEED_CONTEXT || s == SBW_SEED_SELF_SALT; }
+
+template <typename T, int kSeeding>
+void launch_watermark(void* logits, int64_t B, uint32_t V, int64_t row_stride,
+                      const int32_t* prev, uint64_t key, uint32_t tm1, float delta,
+                      bool aligned, hipStream_t stream) {
+  T* p = static_cast<T*>(logits);
+  if (aligned) {
+    constexpr uint32_t kPer = 16u / sizeof(T);
+    const uint64_t vectors = (static_cast<uint64_t>(V) + kPer - 1) / kPer;
+    const uint32_t tiles = static_cast<uint32_t>((vectors + kThreads * kUnroll - 1) /
+                                                 (kThreads * kUnroll));
+    const int64_t num_tiles = B * static_cast<int64_t>(tiles);
+    hipLaunchKernelGGL((watermark_vec_kernel<T, kSeeding>), dim3(grid_for(num_tiles)),
+                       dim3(kThreads), 0, stream, p, row_stride, V, prev, key, tm1, delta, tiles,
+                       num_tiles);
+  } else {
+    const uint32_t tiles = static_cast<uint32_t>((static_cast<uint64_t>(V) + kThreads - 1) / kThreads);
+    const int64_t num_tiles = B * static_cast<int64_t>(tiles);
+    hipLaunchKernelGGL((watermark_elem_kernel<T, kSeeding>), dim3(grid_for(num_tiles)),
+                       dim3(kThreads), 0, stream, p, row_stride, V, prev, key, tm1, delta, tiles,
+                       num_tiles);
+  }
+}
+
+}  // namespace
+}  // namespace sbw
+
+using namespace sbw;
+
+extern "C" {
+
+sbw_status_t sbw_watermark(void* logits, sbw_dtype_t dtype, int64_t B, int64_t V,
+                           int64_t row_stride, const int32_t* prev_tokens, uint64_t key,
+                           double gamma, float delta, sbw_seeding_t seeding, void* stream) {
+  if (B < 0 || V < 0 || row_stride < V) return SBW_ERR_INVALID_ARG;
+  if (dtype != SBW_F32 && dtype != SBW_BF16) return SBW_ERR_UNSUPPORTED;
+  if (!valid_seeding(seeding)) return SBW_ERR_UNSUPPORTED;
+  if (!(gamma >= 0.0 && gamma <= 1.0)) return SBW_ERR_GAMMA;
+  if (!isfinite(delta)) return SBW_ERR_DELTA;
+  if (V >= (int64_t{1} << 32)) return SBW_ERR_UNSUPPORTED;  // token ids are 32-bit
+  if (B == 0 || V == 0) return SBW_OK;
+  if (logits == nullptr || prev_tokens == nullptr) return SBW_ERR_INVALID_ARG;
+  if (B > INT64_MAX / 4 / row_stride) return SBW_ERR_UNSUPPORTED;
+  const uint64_t T = threshold_of(gamma);
+  if (T == 0) return SBW_OK;  // nothing is green: the logits stay as they are
+  sbw_status_t s = check_device();
+  if (s != SBW_OK) return s;
+
+  const size_t esize = dtype == SBW_F32 ? 4 : 2;
+  const bool aligned = (reinterpret_cast<uintptr_t>(logits) % 16 == 0) &&
+                       ((static_cast<uint64_t>(row_stride) * esize) % 16 == 0);
+  const uint32_t tm1 = static_cast<uint32_t>(T - 1);
+  const uint32_t v32 = static_cast<uint32_t>(V);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if (dtype == SBW_F32) {
+    if (seeding == SBW_SEED_CONTEXT)
+      launch_watermark<float, kContext>(logits, B, v32, row_stride, prev_tokens, key, tm1, delta, aligned, st);
+    else
+      launch_watermark<float, kSelfSalt>(logits, B, v32, row_stride, prev_tokens, key, tm1, delta, aligned, st);
+  } else {
+    if (seeding == SBW_SEED_CONTEXT)
+      launch_watermark<uint16_t, kContext>(logits, B, v32, row_stride, prev_tokens, key, tm1, delta, aligned, st);
+    else
+      launch_watermark<uint16_t, kSelfSalt>(logits, B, v32, row_stride, prev_tokens, key, tm1, delta, aligned, st);
+  }
+  return after_launch();
+}
+
+sbw_status_t sbw_green_mask(uint32_t* bits, int64_t B, int64_t V, const int32_t* prev_tokens,
+                            uint64_t key, double gamma, sbw_seeding_t seeding, void* stream) {
+  if (B < 0 || V < 0) return SBW_ERR_INVALID_ARG;
+  if (!valid_seeding(seeding)) return SBW_ERR_UNSUPPORTED;
+  if (!(gamma >= 0.0 && gamma <= 1.0)) return SBW_ERR_GAMMA;
+  if (V >= (int64_t{1} << 32)) return SBW_ERR_UNSUPPORTED;
+  if (B == 0 || V == 0) return SBW_OK;
+  if (bits == nullptr || prev_tokens == nullptr) return SBW_ERR_INVALID_ARG;
+  const int64_t words = (V + 31) / 32;
+  if (B > INT64_MAX / 4 / words) return SBW_ERR_UNSUPPORTED;
+  sbw_status_t s = check_device();
+  if (s != SBW_OK) return s;
+
+  const uint64_t T = threshold_of(gamma);
+  const uint32_t tm1 = T == 0 ? 0u : static_cast<uint32_t>(T - 1);
+  const int64_t num_words = B * words;
+  const int64_t blocks = grid_for((num_words + kThreads - 1) / kThreads);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if (seeding == SBW_SEED_CONTEXT)
+    hipLaunchKernelGGL(green_mask_kernel<kContext>, dim3(blocks), dim3(kThreads), 0, st, bits,
+                       static_cast<uint32_t>(V), static_cast<uint32_t>(words), prev_tokens, key,
+                       tm1, T == 0 ? 1 : 0, num_words);
+  else
+    hipLaunchKernelGGL(green_mask_kernel<kSelfSalt>, dim3(blocks), dim3(kThreads), 0, st, bits,
+                       static_cast<uint32_t>(V), static_cast<uint32_t>(words), prev_tokens, key,
+                       tm1, T == 0 ? 1 : 0, num_words);
+  return after_launch();
+}
+
+sbw_status_t sbw_detect(const int32_t* tokens, int64_t N, int64_t L, int64_t row_stride,
+                        uint64_t key, double gamma, sbw_seeding_t seeding,
+                        int32_t* green_counts, double* z, void* stream) {
+  if (N < 0 || L < 0 || row_stride < L) return SBW_ERR_INVALID_ARG;
+  if (!valid_seeding(seeding)) return SBW_ERR_UNSUPPORTED;
+  if (!(gamma > 0.0 && gamma < 1.0)) return SBW_ERR_GAMMA;
+  if (L > INT32_MAX) return SBW_ERR_UNSUPPORTED;
+  if (N == 0) return SBW_OK;
+  if (green_counts == nullptr || z == nullptr || (L > 0 && tokens == nullptr))
+    return SBW_ERR_INVALID_ARG;
+  if (row_stride > 0 && N > INT64_MAX / 4 / row_stride) return SBW_ERR_UNSUPPORTED;
+  sbw_status_t s = check_device();
+  if (s != SBW_OK) return s;
+
+  const uint64_t T = threshold_of(gamma);  // in [1, 2^32 - 1] for 0 < gamma < 1
+  const uint32_t tm1 = static_cast<uint32_t>(T - 1);
+  const int64_t blocks = grid_for((N + kWavesPerBlock - 1) / kWavesPerBlock);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if (seeding == SBW_SEED_CONTEXT)
+    hipLaunchKernelGGL(detect_kernel<kContext>, dim3(blocks), dim3(kThreads), 0, st, tokens, N, L,
+                       row_stride, key, tm1, gamma, green_counts, z);
+  else
+    hipLaunchKernelGGL(detect_kernel<kSelfSalt>, dim3(blocks), dim3(kThreads), 0, st, tokens, N,
+                       L, row_stride, key, tm1, gamma, green_counts, z);
+  return after_launch();
+}
+
+const char* sbw_strerror(sbw_status_t status) {
+  switch (status) {
+    case SBW_OK: return "success";
+    case SBW_ERR_INVALID_ARG: return "invalid argument (null pointer, negative size or stride too small)";
+    case SBW_ERR_GAMMA: return "gamma out of range";
+    case SBW_ERR_DELTA: return "delta is not finite";
+    case SBW_ERR_UNSUPPORTED: return "unsupported dtype, seeding or size";
+    case SBW_ERR_NO_DEVICE: return "no HIP device available";
+    case SBW_ERR_HIP: return "HIP runtime or launch error";
+  }
+  return "unknown status";
+}
+
+const char* sbw_last_hip_error(void) { return hipGetErrorName(g_last_hip_error); }
+
+const char* sbw_version(void) { return "0.1.0"; }
+
+}  // extern "C"

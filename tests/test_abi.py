@@ -1,0 +1,195 @@
+"""The C ABI on the CPU: the library loads, exports what include/sbw.h declares,
+and rejects bad arguments on the host before any HIP call.
+
+No test here launches a kernel: calls that would pass validation are only made
+where no GPU is visible (they must then return SBW_ERR_NO_DEVICE).
+"""
+import ctypes
+import math
+import os
+import re
+import subprocess
+
+import numpy as np
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "sbw.h")
+
+OK, INVALID, GAMMA, DELTA, UNSUPPORTED, NO_DEVICE, HIP = range(7)
+
+
+@pytest.fixture(scope="module")
+def sbw():
+    import paper_2609_03844_amd as sbw
+    return sbw
+
+
+@pytest.fixture(scope="module")
+def lib(sbw):
+    return sbw.raw()
+
+
+def _declared():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?[a-z_0-9]+\s*\*?\s*(sbw_[a-z_]+)\s*\(", text, re.M)))
+
+
+def test_header_declares_the_boundary():
+    assert _declared() == ["sbw_detect", "sbw_green_mask", "sbw_last_hip_error", "sbw_strerror",
+                           "sbw_version", "sbw_watermark"]
+
+
+def test_library_exports_every_declared_symbol(sbw, lib):
+    out = subprocess.run(["nm", "-D", "--defined-only", sbw.library_path()], capture_output=True,
+                         text=True, check=True).stdout
+    exported = set(re.findall(r"\sT\s(sbw_\w+)$", out, re.M))
+    for name in _declared():
+        assert name in exported, name
+        assert hasattr(lib, name)
+    assert set(sbw.EXPORTED) == set(_declared())
+
+
+def test_library_is_gfx950_code():
+    # the device code bundled into the library targets gfx950
+    import paper_2609_03844_amd as sbw
+    sections = subprocess.run(["readelf", "-S", "-W", sbw.library_path()], capture_output=True,
+                              text=True, check=True).stdout
+    assert ".hip_fatbin" in sections
+    assert b"amdgcn-amd-amdhsa--gfx950" in open(sbw.library_path(), "rb").read()
+
+
+def test_strerror_and_version(lib, sbw):
+    for code in range(7):
+        s = lib.sbw_strerror(code)
+        assert s and len(s) > 3
+    assert lib.sbw_strerror(99) == b"unknown status"
+    assert re.fullmatch(r"\d+\.\d+\.\d+", sbw.version())
+    assert lib.sbw_last_hip_error() == b"hipSuccess"
+
+
+# A dummy non-null pointer; validation rejects the call before it could be used.
+DUMMY = ctypes.c_void_p(0x1000)
+NULL = None
+KEY = 15485863
+
+
+def wm(lib, logits=DUMMY, dtype=0, B=2, V=8, stride=8, prev=DUMMY, gamma=0.25, delta=2.0,
+       seeding=0):
+    return lib.sbw_watermark(logits, dtype, B, V, stride, prev, KEY, gamma, delta, seeding, None)
+
+
+def gm(lib, bits=DUMMY, B=2, V=8, prev=DUMMY, gamma=0.25, seeding=0):
+    return lib.sbw_green_mask(bits, B, V, prev, KEY, gamma, seeding, None)
+
+
+def det(lib, tokens=DUMMY, N=2, L=8, stride=8, gamma=0.25, seeding=0, counts=DUMMY, z=DUMMY):
+    return lib.sbw_detect(tokens, N, L, stride, KEY, gamma, seeding, counts, z, None)
+
+
+def test_watermark_rejects_bad_arguments(lib):
+    assert wm(lib, B=-1) == INVALID
+    assert wm(lib, V=-1) == INVALID
+    assert wm(lib, stride=7) == INVALID
+    assert wm(lib, logits=NULL) == INVALID
+    assert wm(lib, prev=NULL) == INVALID
+    assert wm(lib, dtype=2) == UNSUPPORTED
+    assert wm(lib, dtype=-1) == UNSUPPORTED
+    assert wm(lib, seeding=2) == UNSUPPORTED
+    for g in (-0.1, 1.0000001, math.nan, math.inf, -math.inf):
+        assert wm(lib, gamma=g) == GAMMA, g
+    for d in (math.inf, -math.inf, math.nan):
+        assert wm(lib, delta=d) == DELTA, d
+    assert wm(lib, V=1 << 32, stride=1 << 32) == UNSUPPORTED
+    assert wm(lib, B=1 << 62, V=8, stride=1 << 20) == UNSUPPORTED
+
+
+def test_watermark_empty_and_noop_calls_succeed_without_hip(lib):
+    assert wm(lib, B=0) == OK
+    assert wm(lib, V=0, stride=0) == OK
+    assert wm(lib, B=0, logits=NULL, prev=NULL) == OK
+    # gamma = 0: nothing is green, nothing to do
+    assert wm(lib, gamma=0.0) == OK
+
+
+def test_green_mask_rejects_bad_arguments(lib):
+    assert gm(lib, B=-1) == INVALID
+    assert gm(lib, V=-1) == INVALID
+    assert gm(lib, bits=NULL) == INVALID
+    assert gm(lib, prev=NULL) == INVALID
+    assert gm(lib, seeding=7) == UNSUPPORTED
+    assert gm(lib, gamma=1.5) == GAMMA
+    assert gm(lib, gamma=math.nan) == GAMMA
+    assert gm(lib, V=1 << 32) == UNSUPPORTED
+    assert gm(lib, B=0) == OK
+    assert gm(lib, V=0) == OK
+
+
+def test_detect_rejects_bad_arguments(lib):
+    assert det(lib, N=-1) == INVALID
+    assert det(lib, L=-1) == INVALID
+    assert det(lib, stride=7) == INVALID
+    assert det(lib, tokens=NULL) == INVALID
+    assert det(lib, counts=NULL) == INVALID
+    assert det(lib, z=NULL) == INVALID
+    assert det(lib, seeding=3) == UNSUPPORTED
+    for g in (0.0, 1.0, -0.5, 2.0, math.nan):
+        assert det(lib, gamma=g) == GAMMA, g
+    assert det(lib, L=1 << 31, stride=1 << 31) == UNSUPPORTED
+    assert det(lib, N=0) == OK
+    assert det(lib, N=0, tokens=NULL, counts=NULL, z=NULL) == OK
+
+
+def _gpu_visible():
+    import torch
+    return torch.cuda.is_available()
+
+
+def test_no_device_is_reported():
+    import paper_2609_03844_amd as sbw
+    if _gpu_visible():
+        pytest.skip("a GPU is visible; the no-device path cannot be exercised")
+    lib = sbw.raw()
+    assert wm(lib) == NO_DEVICE
+    assert gm(lib) == NO_DEVICE
+    assert det(lib) == NO_DEVICE
+    assert det(lib, L=0, tokens=NULL, stride=0) == NO_DEVICE
+    assert lib.sbw_last_hip_error() != b"hipSuccess"
+
+
+def test_python_binding_validates_before_the_c_abi():
+    import torch
+    import paper_2609_03844_amd as sbw
+    with pytest.raises(ValueError):
+        sbw.watermark(torch.zeros(3), torch.zeros(1, dtype=torch.int32), KEY, 0.25, 2.0)
+    with pytest.raises(TypeError):
+        sbw.watermark(torch.zeros(1, 3, dtype=torch.float16), torch.zeros(1, dtype=torch.int32),
+                      KEY, 0.25, 2.0)
+    with pytest.raises(ValueError):
+        sbw.watermark(torch.zeros(2, 3), torch.zeros(2, dtype=torch.int64), KEY, 0.25, 2.0)
+    with pytest.raises(ValueError):
+        sbw.detect(torch.zeros(2, 3, dtype=torch.int64), KEY, 0.25)
+    with pytest.raises(KeyError):
+        sbw.watermark(torch.zeros(2, 3), torch.zeros(2, dtype=torch.int32), KEY, 0.25, 2.0,
+                      seeding="bogus")
+
+
+def test_error_codes_surface_as_exceptions():
+    import paper_2609_03844_amd as sbw
+    with pytest.raises(sbw.SbwError) as e:
+        sbw._check(GAMMA)
+    assert e.value.code == "SBW_ERR_GAMMA"
+
+
+def test_status_and_enum_values_match_the_header():
+    text = open(HEADER).read()
+    enums = dict((k, int(v)) for k, v in re.findall(r"(SBW_[A-Z0-9_]+)\s*=\s*(\d+)", text))
+    import paper_2609_03844_amd as sbw
+    assert enums["SBW_SEED_CONTEXT"] == sbw.SEED_CONTEXT
+    assert enums["SBW_SEED_SELF_SALT"] == sbw.SEED_SELF_SALT
+    assert enums["SBW_F32"] == sbw.F32 and enums["SBW_BF16"] == sbw.BF16
+    for code, name in sbw._STATUS.items():
+        assert enums[name] == code
+    # the oracle's scheme codes agree with the library's by value (no shared header)
+    import oracle
+    assert oracle.SEED_CONTEXT == sbw.SEED_CONTEXT and oracle.SEED_SELF_SALT == sbw.SEED_SELF_SALT
