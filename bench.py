@@ -35,9 +35,29 @@ import workloads  # noqa: E402
 
 HBM_PEAK_GBPS = 8000.0                 # MI355X HBM3E
 CUS, LANES, CLOCK_GHZ = 256, 64, 2.4   # MI355X compute units, wave width, peak clock
-# 32x32->64-bit products (v_mad_u64_u32) issue at a quarter of the full VALU rate.
-WIDE_MUL_PEAK_TOPS = CUS * LANES * CLOCK_GHZ / 4 / 1000.0
-PHILOX_PRODUCTS_PER_BLOCK = 20        # 2 per round, 10 rounds
+# One Philox4x32-10 block with a per-lane key needs at least 58 full-rate VALU lane-ops:
+# 20 32x32->64-bit products (v_mad_u64_u32), 20 three-input xors, 18 key-schedule adds.
+PHILOX_LANE_OPS = 58
+PHILOX_PEAK_GBLOCKS = CUS * LANES * CLOCK_GHZ / PHILOX_LANE_OPS
+PROFILE = os.path.join(ROOT, "profiles", "watermark_detect_c4_c5.json")
+KERNEL_SOURCES = ("paper_2609_03844_amd/csrc/sbw_kernels.hip",
+                  "paper_2609_03844_amd/csrc/sbw_device.hpp")
+
+
+def measured_traffic():
+    """HBM bytes per launch from the committed FETCH_SIZE / WRITE_SIZE summary, only
+    while the kernel sources are the ones the counters were taken on."""
+    import hashlib
+    try:
+        prof = json.load(open(PROFILE))
+    except (OSError, ValueError):
+        return {}
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES:
+        h.update(open(os.path.join(ROOT, f), "rb").read())
+    if prof.get("source_sha256") != h.hexdigest():
+        return {}
+    return {k: v["hbm_bytes"] for k, v in prof.get("kernels", {}).items()}
 
 
 def parse():
@@ -200,7 +220,9 @@ def main():
 
     ss = wm_stats("wm_self_salt")
     ctx = wm_stats("wm_context")
-    ss_products = PHILOX_PRODUCTS_PER_BLOCK * elems / (mean_ms["wm_self_salt"] * 1e-3) / 1e12
+    ss_blocks = elems / (mean_ms["wm_self_salt"] * 1e-3) / 1e9   # one Philox block per logit
+    traffic = measured_traffic()
+    wm_tiles = B * math.ceil(math.ceil(V / 4) / 1024)          # workgroups per launch
 
     out = {
         "metric": "watermarked logits Gelem/s + achieved HBM GB/s (B=256,V=152064); detect seq/s",
@@ -227,13 +249,15 @@ def main():
         "watermark": {"self_salt": ss, "context": ctx},
         "detect": {"self_salt": det_stats("det_self_salt"), "context": det_stats("det_context")},
         "roofline": {"bound": "alu", "kernel": "watermark_vec_kernel<float, self-salt>",
-                     "achieved": ss_products, "peak": WIDE_MUL_PEAK_TOPS,
-                     "unit": "T 32x32->64-bit products/s", "frac": ss_products / WIDE_MUL_PEAK_TOPS,
-                     "traffic": None,
-                     "algorithmic_per_launch": f"{PHILOX_PRODUCTS_PER_BLOCK} x B x V Philox products"},
+                     "achieved": ss_blocks, "peak": PHILOX_PEAK_GBLOCKS,
+                     "unit": "G Philox4x32-10 blocks/s", "frac": ss_blocks / PHILOX_PEAK_GBLOCKS,
+                     "traffic": traffic.get(f"sbw::watermark_vec_kernel<float, 1>@{wm_tiles}"),
+                     "algorithmic_per_launch": f"{elems} Philox blocks (one per logit), "
+                                               f"{bytes_wm} HBM bytes"},
         "roofline_context": {"bound": "hbm", "kernel": "watermark_vec_kernel<float, context>",
                              "achieved": ctx["hbm_gbps"], "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                             "frac": ctx["hbm_frac"], "traffic": None,
+                             "frac": ctx["hbm_frac"],
+                             "traffic": traffic.get(f"sbw::watermark_vec_kernel<float, 0>@{wm_tiles}"),
                              "algorithmic_per_launch": f"{bytes_wm} bytes"},
         "wall_s_timed": wall,
     }
