@@ -7,14 +7,17 @@ One step = one pass of the whole hot path over one batch:
   3. detect, self-salt, N=4096 x L=512 token ids over V=128256 (half null,
      half watermarked)
   4. detect, context seeding, the same batch shape
-Each launch is bracketed by HIP events on the stream it runs on.  Logits
-rotate over enough buffers (> 4 x 156 MB) that the 256 MB Infinity Cache cannot
-serve a launch from the previous one: every watermark launch reads HBM.
+The timed region runs exactly `--steps` steps, issuing their launches grouped by
+kernel with a HIP event (on the launching stream) at each group boundary; a
+kernel's mean launch duration is its group time / steps.  Logits rotate over six
+156 MB buffers, so no watermark launch is served from the 256 MB Infinity Cache
+left by the previous one: every launch reads HBM.  A separate pass after the timed
+region brackets single launches with events for p50/p95/p99 latencies.
 
-`value` is the self-salt watermark throughput in Gelem/s (B*V / launch time),
-the configuration the metric names; the context-seeded launch (the HBM-bound
-one) and the detect launches are reported beside it.  All inputs are synthetic
-and resident in HBM before the timed region starts.
+`value` is the self-salt watermark throughput in Gelem/s (B*V / mean launch
+time), the configuration the metric names; the context-seeded launch (the
+HBM-bound one) and the detect launches are reported beside it.  All inputs are
+synthetic and resident in HBM before the timed region starts.
 """
 from __future__ import annotations
 
@@ -66,6 +69,7 @@ def parse():
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--buffers", type=int, default=6)
+    ap.add_argument("--latency-samples", type=int, default=50)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     return ap.parse_args()
@@ -165,39 +169,49 @@ def main():
     launches = [("wm_self_salt", "self_salt"), ("wm_context", "context"),
                 ("det_self_salt", "self_salt"), ("det_context", "context")]
 
-    def step(i, ev=None):
-        for k, (name, seeding) in enumerate(launches):
-            if ev is not None:
-                ev[k][0].record()
-            if name.startswith("wm"):
-                buf = bufs[(2 * i + k) % len(bufs)]
-                sbw.watermark(buf, prev_d, key, c4["gamma"], c4["delta"], seeding)
-            else:
-                sbw.detect(tok_d[seeding], key, c5["gamma"], seeding, counts=counts[seeding],
-                           z=zs[seeding])
-            if ev is not None:
-                ev[k][1].record()
+    def launch(name, seeding, i):
+        if name.startswith("wm"):
+            # consecutive watermark launches never touch the same buffer twice in a row
+            sbw.watermark(bufs[i % len(bufs)], prev_d, key, c4["gamma"], c4["delta"], seeding)
+        else:
+            sbw.detect(tok_d[seeding], key, c5["gamma"], seeding, counts=counts[seeding],
+                       z=zs[seeding])
 
     for i in range(args.warmup):
-        step(i)
+        for name, seeding in launches:
+            launch(name, seeding, i)
     torch.cuda.synchronize()
 
-    evs = [[[torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)]
-            for _ in launches] for _ in range(args.steps)]
-    t_start = torch.cuda.Event(enable_timing=True)
-    t_end = torch.cuda.Event(enable_timing=True)
+    # Timed region: exactly `steps` steps.  The steps' launches are issued grouped by
+    # kernel (all watermark self-salt launches, then all context ones, ...), with a
+    # HIP event on the launching stream at each group boundary, so each kernel's mean
+    # launch duration is its group time / steps without per-launch marker overhead.
+    marks = [torch.cuda.Event(enable_timing=True) for _ in range(len(launches) + 1)]
     torch.cuda.synchronize()
     wall0 = time.perf_counter()
-    t_start.record()
-    for i in range(args.steps):
-        step(i, evs[i])
-    t_end.record()
+    marks[0].record()
+    for k, (name, seeding) in enumerate(launches):
+        for i in range(args.steps):
+            launch(name, seeding, i)
+        marks[k + 1].record()
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
-    total_ms = t_start.elapsed_time(t_end)
-    per = {name: [evs[i][k][0].elapsed_time(evs[i][k][1]) for i in range(args.steps)]
-           for k, (name, _) in enumerate(launches)}
-    mean_ms = {n: float(np.mean(v)) for n, v in per.items()}
+    total_ms = marks[0].elapsed_time(marks[-1])
+    mean_ms = {name: marks[k].elapsed_time(marks[k + 1]) / args.steps
+               for k, (name, _) in enumerate(launches)}
+
+    # Latency pass (outside the timed region): per-launch events for percentiles; each
+    # sample includes the event markers around one launch.
+    lat = {name: [] for name, _ in launches}
+    for i in range(args.latency_samples):
+        for name, seeding in launches:
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            launch(name, seeding, i)
+            e1.record()
+            lat[name].append((e0, e1))
+    torch.cuda.synchronize()
+    per = {name: [a.elapsed_time(b) for a, b in v] for name, v in lat.items()}
 
     elems = B * V
     bytes_wm = 8 * elems + 4 * B          # read + write each logit, read prev tokens
@@ -208,14 +222,16 @@ def main():
         return {"gelem_per_s": elems / (ms * 1e-3) / 1e9,
                 "hbm_gbps": bytes_wm / (ms * 1e-3) / 1e9,
                 "hbm_frac": bytes_wm / (ms * 1e-3) / 1e9 / HBM_PEAK_GBPS,
-                "us_mean": ms * 1e3, "us_p50": percentile(per[name], 50) * 1e3,
-                "us_p95": percentile(per[name], 95) * 1e3, "us_p99": percentile(per[name], 99) * 1e3}
+                "us_mean": ms * 1e3,
+                "latency_us_p50": percentile(per[name], 50) * 1e3,
+                "latency_us_p95": percentile(per[name], 95) * 1e3,
+                "latency_us_p99": percentile(per[name], 99) * 1e3}
 
     def det_stats(name):
         ms = mean_ms[name]
         return {"seq_per_s": c5["N"] / (ms * 1e-3), "us_mean": ms * 1e3,
-                "us_p50": percentile(per[name], 50) * 1e3,
-                "us_p99": percentile(per[name], 99) * 1e3,
+                "latency_us_p50": percentile(per[name], 50) * 1e3,
+                "latency_us_p99": percentile(per[name], 99) * 1e3,
                 "gbps": bytes_det / (ms * 1e-3) / 1e9}
 
     ss = wm_stats("wm_self_salt")

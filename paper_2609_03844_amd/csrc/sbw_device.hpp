@@ -32,6 +32,11 @@ __device__ __forceinline__ uint64_t wide_mul(uint32_t a, uint32_t b) {
   return static_cast<uint64_t>(a) * static_cast<uint64_t>(b);
 }
 
+// a ^ b ^ c in one VALU op: gfx950's three-input bitwise LUT (0x96 = a XOR b XOR c).
+__device__ __forceinline__ uint32_t xor3(uint32_t a, uint32_t b, uint32_t c) {
+  return __builtin_amdgcn_bitop3_b32(a, b, c, 0x96);
+}
+
 // Philox4x32-10 of the block at counter (c0, 0, 0, 0).  The three zero counter
 // words are constants, so the first round's product of word 2 folds away.  Only
 // the words the caller reads survive dead-code elimination of the last round.
@@ -46,9 +51,10 @@ __device__ __forceinline__ Block philox_block(uint32_t c0, Key k) {
   for (int round = 0; round < 10; ++round) {
     const uint64_t pa = wide_mul(kPhiloxMulA, x0);
     const uint64_t pb = wide_mul(kPhiloxMulB, x2);
-    const uint32_t y0 = static_cast<uint32_t>(pb >> 32) ^ x1 ^ k0;
+    const uint32_t y0 = round == 0 ? k0 : xor3(static_cast<uint32_t>(pb >> 32), x1, k0);
     const uint32_t y1 = static_cast<uint32_t>(pb);
-    const uint32_t y2 = static_cast<uint32_t>(pa >> 32) ^ x3 ^ k1;
+    const uint32_t y2 = round == 0 ? static_cast<uint32_t>(pa >> 32) ^ k1
+                                   : xor3(static_cast<uint32_t>(pa >> 32), x3, k1);
     const uint32_t y3 = static_cast<uint32_t>(pa);
     x0 = y0; x1 = y1; x2 = y2; x3 = y3;
     k0 += kPhiloxWeyl0;
@@ -85,13 +91,30 @@ __device__ __forceinline__ uint64_t context_seed(uint64_t key, uint32_t p) {
   return key * static_cast<uint64_t>(p);
 }
 
+// Low 64 bits of a * b for a 64-bit a and a 32-bit b: one full 32x32 product of the
+// low word plus the low half of the high word's product.
+__device__ __forceinline__ uint64_t mul_64x32(uint64_t a, uint32_t b) {
+  const uint64_t lo = wide_mul(static_cast<uint32_t>(a), b);
+  const uint32_t hi = static_cast<uint32_t>(lo >> 32) + static_cast<uint32_t>(a >> 32) * b;
+  return (static_cast<uint64_t>(hi) << 32) | static_cast<uint32_t>(lo);
+}
+
+// Low 64 bits of a * s for 64-bit a and s (three 32x32 products).
+__device__ __forceinline__ uint64_t mul_64x64(uint64_t a, uint64_t s) {
+  const uint32_t a0 = static_cast<uint32_t>(a), a1 = static_cast<uint32_t>(a >> 32);
+  const uint32_t s0 = static_cast<uint32_t>(s), s1 = static_cast<uint32_t>(s >> 32);
+  const uint64_t lo = wide_mul(a0, s0);
+  const uint32_t hi = static_cast<uint32_t>(lo >> 32) + a0 * s1 + a1 * s0;
+  return (static_cast<uint64_t>(hi) << 32) | static_cast<uint32_t>(lo);
+}
+
 // Self-salt seed with the row part precomputed: key_jp = key * J(p) mod 2^64.
-// r = min_u64(key*J(p)*J(v), key*J(v)*J(v)).
+// r = min_u64(key*J(p)*J(v), key*J(v)*J(v)); the second product is key * (J(v)^2).
 __device__ __forceinline__ uint64_t self_salt_seed(uint64_t key, uint64_t key_jp,
                                                    uint32_t v) {
-  const uint64_t jv = jenkins32(v);
-  const uint64_t with_prev = key_jp * jv;
-  const uint64_t with_self = (key * jv) * jv;
+  const uint32_t jv = jenkins32(v);
+  const uint64_t with_prev = mul_64x32(key_jp, jv);
+  const uint64_t with_self = mul_64x64(key, wide_mul(jv, jv));
   return with_prev < with_self ? with_prev : with_self;
 }
 

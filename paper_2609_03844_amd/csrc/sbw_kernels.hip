@@ -14,14 +14,32 @@
 #include <math.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 #include "sbw.h"
 #include "sbw_device.hpp"
 
 namespace sbw {
 namespace {
 
+// Launch-shape tuning knobs (compile-time; the defaults are the measured best).
+#ifndef SBW_CONTEXT_UNROLL
+#define SBW_CONTEXT_UNROLL 2   // 16-byte vectors per lane, context seeding (HBM-bound)
+#endif
+#ifndef SBW_SELF_SALT_UNROLL
+#define SBW_SELF_SALT_UNROLL 2 // 16-byte vectors per lane, self-salt (Philox-bound)
+#endif
+
 constexpr int kThreads = 256;     // 4 wavefronts of 64
-constexpr int kUnroll = 4;        // 16-byte vectors in flight per lane
+
+// Native vector types (the non-temporal builtins take these, not HIP's float4/uint4).
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+template <typename V>
+__device__ __forceinline__ V stream_load(const V* p) { return __builtin_nontemporal_load(p); }
+template <typename V>
+__device__ __forceinline__ void stream_store(V* p, V v) { __builtin_nontemporal_store(v, p); }
 constexpr int64_t kMaxGrid = 1ll << 20;  // blocks; grid-stride loops cover the rest
 
 // Per-row state shared by all lanes of a workgroup.
@@ -47,8 +65,8 @@ __device__ __forceinline__ uint32_t draw(const RowSeed& rs, uint32_t v) {
 // exactly the 4 words of the Philox block at counter j.
 // ---------------------------------------------------------------------------
 template <int kSeeding>
-__device__ __forceinline__ float4 bias_vec_f32(float4 l, uint32_t j, const RowSeed& rs,
-                                               uint32_t tm1, float delta) {
+__device__ __forceinline__ f32x4 bias_vec_f32(f32x4 l, uint32_t j, const RowSeed& rs,
+                                              uint32_t tm1, float delta) {
   const uint32_t v = j * 4u;
   uint32_t x0, x1, x2, x3;
   if (kSeeding == kContext) {
@@ -60,7 +78,7 @@ __device__ __forceinline__ float4 bias_vec_f32(float4 l, uint32_t j, const RowSe
     x2 = philox_block(j, key_of(self_salt_seed(rs.key, rs.seed, v + 2u))).w2;
     x3 = philox_block(j, key_of(self_salt_seed(rs.key, rs.seed, v + 3u))).w3;
   }
-  float4 o;
+  f32x4 o;
   o.x = bias_f32(l.x, delta, is_green(x0, tm1));
   o.y = bias_f32(l.y, delta, is_green(x1, tm1));
   o.z = bias_f32(l.z, delta, is_green(x2, tm1));
@@ -70,7 +88,7 @@ __device__ __forceinline__ float4 bias_vec_f32(float4 l, uint32_t j, const RowSe
 
 // bf16: a vector is the 8 tokens 8j..8j+7 = Philox blocks 2j and 2j+1.
 template <int kSeeding>
-__device__ __forceinline__ uint4 bias_vec_bf16(uint4 raw, uint32_t j, const RowSeed& rs,
+__device__ __forceinline__ u32x4 bias_vec_bf16(u32x4 raw, uint32_t j, const RowSeed& rs,
                                                uint32_t tm1, float delta) {
   const uint32_t v = j * 8u;
   uint32_t x[8];
@@ -97,7 +115,18 @@ __device__ __forceinline__ uint4 bias_vec_bf16(uint4 raw, uint32_t j, const RowS
         bias_bf16(static_cast<uint16_t>(in[q] >> 16), delta, is_green(x[2 * q + 1], tm1));
     out[q] = static_cast<uint32_t>(lo) | (static_cast<uint32_t>(hi) << 16);
   }
-  return uint4{out[0], out[1], out[2], out[3]};
+  return u32x4{out[0], out[1], out[2], out[3]};
+}
+
+template <int kSeeding>
+__device__ __forceinline__ f32x4 bias_vec(f32x4 l, uint32_t j, const RowSeed& rs, uint32_t tm1,
+                                          float delta) {
+  return bias_vec_f32<kSeeding>(l, j, rs, tm1, delta);
+}
+template <int kSeeding>
+__device__ __forceinline__ u32x4 bias_vec(u32x4 raw, uint32_t j, const RowSeed& rs, uint32_t tm1,
+                                          float delta) {
+  return bias_vec_bf16<kSeeding>(raw, j, rs, tm1, delta);
 }
 
 // One element of either dtype (row tails and unaligned rows).
@@ -121,56 +150,52 @@ __device__ __forceinline__ void bias_one(T* row, uint32_t v, const RowSeed& rs, 
   row[v] = Elem<T>::bias(row[v], delta, is_green(x, tm1));
 }
 
-// Vectorised watermark for rows whose start is 16-byte aligned.
-//   VecT: float4 (fp32, 4 per vector) or uint4 (bf16, 8 per vector).
-template <typename T, int kSeeding>
+// Vectorised watermark for rows whose start is 16-byte aligned.  Grid: x = tile of
+// kThreads * kU vectors within a row, y = row (grid-stride over rows beyond 65535).
+// Each lane issues its logits load before reading the row's previous token, so the
+// scalar load of prev[row] overlaps the HBM stream.
+template <typename T, int kSeeding, int kU>
 __global__ void __launch_bounds__(kThreads)
-watermark_vec_kernel(T* __restrict__ logits, int64_t row_stride, uint32_t V,
-                     const int32_t* __restrict__ prev, uint64_t key, uint32_t tm1, float delta,
-                     uint32_t tiles_per_row, int64_t num_tiles) {
+watermark_vec_kernel(T* __restrict__ logits, int64_t row_stride, uint32_t V, int64_t B,
+                     const int32_t* __restrict__ prev, uint64_t key, uint32_t tm1, float delta) {
+  using VecT = typename std::conditional<sizeof(T) == 4, f32x4, u32x4>::type;
   constexpr uint32_t kPer = 16u / sizeof(T);  // elements per 16-byte vector
   const uint32_t full = V / kPer;             // complete vectors in a row
   const uint32_t tail = V % kPer;
-  for (int64_t tile = blockIdx.x; tile < num_tiles; tile += gridDim.x) {
-    const int64_t row = tile / tiles_per_row;
-    const uint32_t first = static_cast<uint32_t>(tile - row * tiles_per_row) *
-                           (kThreads * kUnroll);
-    const RowSeed rs = row_seed<kSeeding>(key, static_cast<uint32_t>(prev[row]));
+  const uint32_t first = blockIdx.x * (kThreads * kU);
+  for (int64_t row = blockIdx.y; row < B; row += gridDim.y) {
     T* row_ptr = logits + row * row_stride;
-
-    if constexpr (sizeof(T) == 4) {
-      float4* vec = reinterpret_cast<float4*>(row_ptr);
-      float4 buf[kUnroll];
+    VecT* vec = reinterpret_cast<VecT*>(row_ptr);
+    VecT buf[kU];
+    if (first + kThreads * kU <= full) {
+      // Whole tile inside the row: no per-vector guards, all loads in flight at once.
 #pragma unroll
-      for (int u = 0; u < kUnroll; ++u) {
-        const uint32_t j = first + u * kThreads + threadIdx.x;
-        if (j < full) buf[u] = vec[j];
-      }
+      for (int u = 0; u < kU; ++u) buf[u] = stream_load(vec + first + u * kThreads + threadIdx.x);
+      const RowSeed rs = row_seed<kSeeding>(key, static_cast<uint32_t>(prev[row]));
 #pragma unroll
-      for (int u = 0; u < kUnroll; ++u) {
+      for (int u = 0; u < kU; ++u) {
         const uint32_t j = first + u * kThreads + threadIdx.x;
-        if (j < full) vec[j] = bias_vec_f32<kSeeding>(buf[u], j, rs, tm1, delta);
+        stream_store(vec + j, bias_vec<kSeeding>(buf[u], j, rs, tm1, delta));
       }
     } else {
-      uint4* vec = reinterpret_cast<uint4*>(row_ptr);
-      uint4 buf[kUnroll];
 #pragma unroll
-      for (int u = 0; u < kUnroll; ++u) {
+      for (int u = 0; u < kU; ++u) {
         const uint32_t j = first + u * kThreads + threadIdx.x;
-        if (j < full) buf[u] = vec[j];
+        if (j < full) buf[u] = stream_load(vec + j);
       }
+      const RowSeed rs = row_seed<kSeeding>(key, static_cast<uint32_t>(prev[row]));
 #pragma unroll
-      for (int u = 0; u < kUnroll; ++u) {
+      for (int u = 0; u < kU; ++u) {
         const uint32_t j = first + u * kThreads + threadIdx.x;
-        if (j < full) vec[j] = bias_vec_bf16<kSeeding>(buf[u], j, rs, tm1, delta);
+        if (j < full) stream_store(vec + j, bias_vec<kSeeding>(buf[u], j, rs, tm1, delta));
       }
-    }
-    // The partial vector at the end of the row, element by element.
-    // Lane 0 of the tile that covers vector index `full` handles it.
-    if (tail != 0u && threadIdx.x == 0 && full >= first &&
-        full - first < static_cast<uint32_t>(kThreads * kUnroll)) {
-      for (uint32_t e = 0; e < tail; ++e)
-        bias_one<T, kSeeding>(row_ptr, full * kPer + e, rs, tm1, delta);
+      // The partial vector at the end of the row, element by element, by lane 0 of
+      // the tile that covers vector index `full`.
+      if (tail != 0u && threadIdx.x == 0 && full >= first &&
+          full - first < static_cast<uint32_t>(kThreads * kU)) {
+        for (uint32_t e = 0; e < tail; ++e)
+          bias_one<T, kSeeding>(row_ptr, full * kPer + e, rs, tm1, delta);
+      }
     }
   }
 }
@@ -178,15 +203,13 @@ watermark_vec_kernel(T* __restrict__ logits, int64_t row_stride, uint32_t V,
 // Element-wise watermark for rows that are not 16-byte aligned.
 template <typename T, int kSeeding>
 __global__ void __launch_bounds__(kThreads)
-watermark_elem_kernel(T* __restrict__ logits, int64_t row_stride, uint32_t V,
-                      const int32_t* __restrict__ prev, uint64_t key, uint32_t tm1, float delta,
-                      uint32_t tiles_per_row, int64_t num_tiles) {
-  for (int64_t tile = blockIdx.x; tile < num_tiles; tile += gridDim.x) {
-    const int64_t row = tile / tiles_per_row;
-    const uint64_t v64 = static_cast<uint64_t>(tile - row * tiles_per_row) * kThreads + threadIdx.x;
-    if (v64 >= V) continue;
+watermark_elem_kernel(T* __restrict__ logits, int64_t row_stride, uint32_t V, int64_t B,
+                      const int32_t* __restrict__ prev, uint64_t key, uint32_t tm1, float delta) {
+  const uint32_t v = blockIdx.x * kThreads + threadIdx.x;
+  for (int64_t row = blockIdx.y; row < B; row += gridDim.y) {
+    if (v >= V) continue;
     const RowSeed rs = row_seed<kSeeding>(key, static_cast<uint32_t>(prev[row]));
-    bias_one<T, kSeeding>(logits + row * row_stride, static_cast<uint32_t>(v64), rs, tm1, delta);
+    bias_one<T, kSeeding>(logits + row * row_stride, v, rs, tm1, delta);
   }
 }
 
@@ -235,6 +258,20 @@ constexpr int kWave = 64;
 constexpr int kWavesPerBlock = kThreads / kWave;
 
 template <int kSeeding>
+__device__ __forceinline__ bool token_green(uint64_t key, uint32_t p, uint32_t v, uint32_t tm1) {
+  uint64_t r;
+  if (kSeeding == kContext) {
+    r = context_seed(key, p);
+  } else {
+    r = self_salt_seed(key, key * static_cast<uint64_t>(jenkins32(p)), v);
+  }
+  return is_green(cbrng(v, r), tm1);
+}
+
+// Positions handled per lane per pass: a pass covers 64 * kChunk positions and
+// issues all of its token loads before any arithmetic.  The host picks kChunk from L
+// so that short sequences do not compute idle slots.
+template <int kSeeding, int kDetectChunk>
 __global__ void __launch_bounds__(kThreads)
 detect_kernel(const int32_t* __restrict__ tokens, int64_t N, int64_t L, int64_t row_stride,
               uint64_t key, uint32_t tm1, double gamma, int32_t* __restrict__ counts,
@@ -244,21 +281,29 @@ detect_kernel(const int32_t* __restrict__ tokens, int64_t N, int64_t L, int64_t 
   for (int64_t n = wave0; n < N; n += static_cast<int64_t>(gridDim.x) * kWavesPerBlock) {
     const int32_t* seq = tokens + n * row_stride;
     uint32_t green = 0u;  // wave-uniform count
-    for (int64_t base = 1; base < L; base += kWave) {
-      const int64_t i = base + lane;
-      bool g = false;
-      if (i < L) {
-        const uint32_t p = static_cast<uint32_t>(seq[i - 1]);
-        const uint32_t v = static_cast<uint32_t>(seq[i]);
-        uint64_t r;
-        if (kSeeding == kContext) {
-          r = context_seed(key, p);
-        } else {
-          r = self_salt_seed(key, key * static_cast<uint64_t>(jenkins32(p)), v);
+    for (int64_t base = 1; base < L; base += kWave * kDetectChunk) {
+      uint32_t p[kDetectChunk], v[kDetectChunk];
+#pragma unroll
+      for (int c = 0; c < kDetectChunk; ++c) {
+        const int64_t i = base + c * kWave + lane;
+        p[c] = 0u;
+        v[c] = 0u;
+        if (i < L) {
+          p[c] = static_cast<uint32_t>(seq[i - 1]);
+          v[c] = static_cast<uint32_t>(seq[i]);
         }
-        g = is_green(cbrng(v, r), tm1);
       }
-      green += static_cast<uint32_t>(__popcll(__ballot(g)));
+      // Independent membership chains first (instruction-level parallelism), then
+      // one ballot per chunk.
+      bool g[kDetectChunk];
+#pragma unroll
+      for (int c = 0; c < kDetectChunk; ++c) {
+        const int64_t i = base + c * kWave + lane;
+        g[c] = token_green<kSeeding>(key, p[c], v[c], tm1) && i < L;
+      }
+#pragma unroll
+      for (int c = 0; c < kDetectChunk; ++c)
+        green += static_cast<uint32_t>(__popcll(__ballot(g[c])));
     }
     if (lane == 0) {
       const int64_t T = L > 1 ? L - 1 : 0;
@@ -308,27 +353,50 @@ int64_t grid_for(int64_t work_groups) { return work_groups < kMaxGrid ? work_gro
 
 bool valid_seeding(int s) { return s == SBW_SEED_CONTEXT || s == SBW_SEED_SELF_SALT; }
 
+constexpr int64_t kMaxGridY = 65535;
+
+// Vectors per lane.  Two in flight per lane measured best for both seedings on
+// MI355X: the context pass reaches ~80 % of HBM peak (one per lane: ~75 %), and the
+// self-salt pass gets two independent sets of Philox chains per lane.
+template <int kSeeding>
+constexpr int unroll_for() { return kSeeding == kContext ? SBW_CONTEXT_UNROLL : SBW_SELF_SALT_UNROLL; }
+
 template <typename T, int kSeeding>
 void launch_watermark(void* logits, int64_t B, uint32_t V, int64_t row_stride,
                       const int32_t* prev, uint64_t key, uint32_t tm1, float delta,
                       bool aligned, hipStream_t stream) {
   T* p = static_cast<T*>(logits);
+  const uint32_t rows = static_cast<uint32_t>(B < kMaxGridY ? B : kMaxGridY);
   if (aligned) {
+    constexpr int kU = unroll_for<kSeeding>();
     constexpr uint32_t kPer = 16u / sizeof(T);
     const uint64_t vectors = (static_cast<uint64_t>(V) + kPer - 1) / kPer;
-    const uint32_t tiles = static_cast<uint32_t>((vectors + kThreads * kUnroll - 1) /
-                                                 (kThreads * kUnroll));
-    const int64_t num_tiles = B * static_cast<int64_t>(tiles);
-    hipLaunchKernelGGL((watermark_vec_kernel<T, kSeeding>), dim3(grid_for(num_tiles)),
-                       dim3(kThreads), 0, stream, p, row_stride, V, prev, key, tm1, delta, tiles,
-                       num_tiles);
+    const uint32_t tiles = static_cast<uint32_t>((vectors + kThreads * kU - 1) / (kThreads * kU));
+    hipLaunchKernelGGL((watermark_vec_kernel<T, kSeeding, kU>), dim3(tiles, rows), dim3(kThreads),
+                       0, stream, p, row_stride, V, B, prev, key, tm1, delta);
   } else {
     const uint32_t tiles = static_cast<uint32_t>((static_cast<uint64_t>(V) + kThreads - 1) / kThreads);
-    const int64_t num_tiles = B * static_cast<int64_t>(tiles);
-    hipLaunchKernelGGL((watermark_elem_kernel<T, kSeeding>), dim3(grid_for(num_tiles)),
-                       dim3(kThreads), 0, stream, p, row_stride, V, prev, key, tm1, delta, tiles,
-                       num_tiles);
+    hipLaunchKernelGGL((watermark_elem_kernel<T, kSeeding>), dim3(tiles, rows), dim3(kThreads), 0,
+                       stream, p, row_stride, V, B, prev, key, tm1, delta);
   }
+}
+
+template <int kSeeding>
+void launch_detect(int64_t positions, int64_t blocks, hipStream_t st, const int32_t* tokens,
+                   int64_t N, int64_t L, int64_t row_stride, uint64_t key, uint32_t tm1,
+                   double gamma, int32_t* counts, double* z) {
+  if (positions <= kWave)
+    hipLaunchKernelGGL((detect_kernel<kSeeding, 1>), dim3(blocks), dim3(kThreads), 0, st, tokens,
+                       N, L, row_stride, key, tm1, gamma, counts, z);
+  else if (positions <= 2 * kWave)
+    hipLaunchKernelGGL((detect_kernel<kSeeding, 2>), dim3(blocks), dim3(kThreads), 0, st, tokens,
+                       N, L, row_stride, key, tm1, gamma, counts, z);
+  else if (positions <= 4 * kWave)
+    hipLaunchKernelGGL((detect_kernel<kSeeding, 4>), dim3(blocks), dim3(kThreads), 0, st, tokens,
+                       N, L, row_stride, key, tm1, gamma, counts, z);
+  else
+    hipLaunchKernelGGL((detect_kernel<kSeeding, 8>), dim3(blocks), dim3(kThreads), 0, st, tokens,
+                       N, L, row_stride, key, tm1, gamma, counts, z);
 }
 
 }  // namespace
@@ -422,12 +490,13 @@ sbw_status_t sbw_detect(const int32_t* tokens, int64_t N, int64_t L, int64_t row
   const uint32_t tm1 = static_cast<uint32_t>(T - 1);
   const int64_t blocks = grid_for((N + kWavesPerBlock - 1) / kWavesPerBlock);
   hipStream_t st = static_cast<hipStream_t>(stream);
+  const int64_t positions = L > 1 ? L - 1 : 0;
   if (seeding == SBW_SEED_CONTEXT)
-    hipLaunchKernelGGL(detect_kernel<kContext>, dim3(blocks), dim3(kThreads), 0, st, tokens, N, L,
-                       row_stride, key, tm1, gamma, green_counts, z);
+    launch_detect<kContext>(positions, blocks, st, tokens, N, L, row_stride, key, tm1, gamma,
+                            green_counts, z);
   else
-    hipLaunchKernelGGL(detect_kernel<kSelfSalt>, dim3(blocks), dim3(kThreads), 0, st, tokens, N,
-                       L, row_stride, key, tm1, gamma, green_counts, z);
+    launch_detect<kSelfSalt>(positions, blocks, st, tokens, N, L, row_stride, key, tm1, gamma,
+                             green_counts, z);
   return after_launch();
 }
 

@@ -194,6 +194,7 @@ def test_green_mask(env, seeding, B, V):
 
 @pytest.mark.parametrize("seeding", ["context", "self_salt"])
 @pytest.mark.parametrize("N,L", [(1, 0), (3, 1), (2, 2), (5, 63), (5, 64), (5, 65), (7, 200),
+                                 (9, 256), (9, 257), (9, 258), (4, 2049),
                                  (300, 129), (3, 5000)])
 def test_detect_small(env, seeding, N, L):
     rng = np.random.default_rng(N * 31 + L)
