@@ -7,9 +7,10 @@ One step = one pass of the whole hot path over one batch:
   3. detect, self-salt, N=4096 x L=512 token ids over V=128256 (half null,
      half watermarked)
   4. detect, context seeding, the same batch shape
-The timed region runs exactly `--steps` steps, issuing their launches grouped by
-kernel with a HIP event (on the launching stream) at each group boundary; a
-kernel's mean launch duration is its group time / steps.  Logits rotate over six
+The timed region runs exactly `--steps` steps: each kernel's `steps` launches are
+captured in one HIP graph and the four graphs are replayed back to back, with a
+HIP event (on the launching stream) at each group boundary; a kernel's mean launch
+duration is its group time / steps.  Logits rotate over six
 156 MB buffers, so no watermark launch is served from the 256 MB Infinity Cache
 left by the previous one: every launch reads HBM.  A separate pass after the timed
 region brackets single launches with events for p50/p95/p99 latencies.
@@ -71,6 +72,7 @@ def parse():
     ap.add_argument("--buffers", type=int, default=6)
     ap.add_argument("--latency-samples", type=int, default=50)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-configs", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     return ap.parse_args()
 
@@ -123,6 +125,96 @@ def cpu_baseline(x, prev, tok_ss, seconds):
         "cpu": _cpu_model(),
         "nproc": os.cpu_count(),
     }
+
+
+def _mean_us(torch, launch, n_launch, warmup=10):
+    """Mean GPU duration of one launch: n_launch launches captured in a HIP graph,
+    replayed once between two events (no host overhead inside the interval)."""
+    for i in range(warmup):
+        launch(i)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        for i in range(n_launch):
+            launch(i)
+    g.replay()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    a.record()
+    g.replay()
+    b.record()
+    torch.cuda.synchronize()
+    return a.elapsed_time(b) / n_launch * 1e3
+
+
+def other_configs(torch, sbw, dev, steps):
+    """The remaining workload configurations, each timed back to back with enough
+    rotating buffers (> 256 MB in total) that no launch is served from the Infinity
+    Cache left by the previous one."""
+    key = workloads.PAPER_KEY
+    res = {}
+
+    def rotating(x, min_total_bytes=400 << 20):
+        t = torch.from_numpy(x.view(np.int16) if x.dtype == np.uint16 else x).to(dev)
+        if x.dtype == np.uint16:
+            t = t.view(torch.bfloat16)
+        n = max(2, -(-min_total_bytes // (t.numel() * t.element_size())))
+        return [t.clone() for _ in range(n)]
+
+    # c1: B=1 x V=32000 fp32, context; launch-latency bound, so report microseconds
+    c = workloads.C1
+    x, prev = workloads.watermark_inputs("c1")
+    bufs, p = rotating(x), torch.from_numpy(prev).to(dev)
+    us = _mean_us(torch, lambda i: sbw.watermark(bufs[i % len(bufs)], p, key, c["gamma"],
+                                                 c["delta"], "context"), steps)
+    tok = torch.from_numpy(workloads.uniform_tokens(c["detect_N"], c["detect_L"], c["V"],
+                                                    workloads.rng_for("c1", 1))).to(dev)
+    det = {s: _mean_us(torch, lambda i, s=s: sbw.detect(tok, key, c["gamma"], s), steps)
+           for s in ("context", "self_salt")}
+    res["c1"] = {"watermark_us": us, "gelem_per_s": c["B"] * c["V"] / us / 1e3,
+                 "detect_8x200_us": det}
+    del bufs
+
+    # c2: B=64 x V=128256 bf16, context, 8 (gamma, delta) pairs
+    c = workloads.C2
+    x, prev = workloads.watermark_inputs("c2")
+    bufs, p = rotating(x), torch.from_numpy(prev).to(dev)
+    sweep = {}
+    for g, d in c["sweep"]:
+        us = _mean_us(torch, lambda i, g=g, d=d: sbw.watermark(bufs[i % len(bufs)], p, key, g, d,
+                                                               "context"), steps)
+        sweep[f"gamma={g},delta={d}"] = {"us": us, "gelem_per_s": c["B"] * c["V"] / us / 1e3,
+                                         "hbm_gbps": 4 * c["B"] * c["V"] / us / 1e3}
+    res["c2"] = sweep
+    del bufs
+
+    # c3: B=64 x V=128256 fp32, self-salt, gamma=0.25, delta=4
+    c = workloads.C3
+    x, prev = workloads.watermark_inputs("c3")
+    bufs, p = rotating(x), torch.from_numpy(prev).to(dev)
+    us = _mean_us(torch, lambda i: sbw.watermark(bufs[i % len(bufs)], p, key, c["gamma"],
+                                                 c["delta"], "self_salt"), steps)
+    res["c3"] = {"us": us, "gelem_per_s": c["B"] * c["V"] / us / 1e3,
+                 "philox_gblocks_per_s": c["B"] * c["V"] / us / 1e3}
+    del bufs
+
+    # c4 at B=1024 (623 MB per buffer), both seedings
+    c = workloads.C4
+    x, prev = workloads.watermark_inputs("c4", B=c["B_large"])
+    bufs, p = rotating(x, 1 << 30), torch.from_numpy(prev).to(dev)
+    del x
+    big = {}
+    n = c["B_large"] * c["V"]
+    for seeding in ("self_salt", "context"):
+        us = _mean_us(torch, lambda i, s=seeding: sbw.watermark(bufs[i % len(bufs)], p, key,
+                                                                c["gamma"], c["delta"], s),
+                      max(20, steps // 4))
+        big[seeding] = {"us": us, "gelem_per_s": n / us / 1e3,
+                        "hbm_gbps": 8 * n / us / 1e3, "hbm_frac": 8 * n / us / 1e3 / HBM_PEAK_GBPS}
+    res["c4_B1024"] = big
+    del bufs
+    torch.cuda.empty_cache()
+    return res
 
 
 def _cpu_model():
@@ -182,23 +274,36 @@ def main():
             launch(name, seeding, i)
     torch.cuda.synchronize()
 
-    # Timed region: exactly `steps` steps.  The steps' launches are issued grouped by
-    # kernel (all watermark self-salt launches, then all context ones, ...), with a
-    # HIP event on the launching stream at each group boundary, so each kernel's mean
-    # launch duration is its group time / steps without per-launch marker overhead.
+    # Each kernel's `steps` launches are captured once in a HIP graph (the library's
+    # launches go to the capturing stream), so the timed region measures GPU time and
+    # not the Python call overhead of a host loop.
+    graphs = []
+    for name, seeding in launches:
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for i in range(args.steps):
+                launch(name, seeding, i)
+        graphs.append(g)
+    for g in graphs:        # one untimed replay each
+        g.replay()
+    torch.cuda.synchronize()
+
+    # Timed region: exactly `steps` steps, their launches grouped by kernel (one graph
+    # replay per kernel), with a HIP event on the launching stream at each group
+    # boundary: a kernel's mean launch duration is its group time / steps.
     marks = [torch.cuda.Event(enable_timing=True) for _ in range(len(launches) + 1)]
     torch.cuda.synchronize()
     wall0 = time.perf_counter()
     marks[0].record()
-    for k, (name, seeding) in enumerate(launches):
-        for i in range(args.steps):
-            launch(name, seeding, i)
+    for k, g in enumerate(graphs):
+        g.replay()
         marks[k + 1].record()
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
     total_ms = marks[0].elapsed_time(marks[-1])
     mean_ms = {name: marks[k].elapsed_time(marks[k + 1]) / args.steps
                for k, (name, _) in enumerate(launches)}
+    del graphs
 
     # Latency pass (outside the timed region): per-launch events for percentiles; each
     # sample includes the event markers around one launch.
@@ -238,7 +343,10 @@ def main():
     ctx = wm_stats("wm_context")
     ss_blocks = elems / (mean_ms["wm_self_salt"] * 1e-3) / 1e9   # one Philox block per logit
     traffic = measured_traffic()
-    wm_tiles = B * math.ceil(math.ceil(V / 4) / 1024)          # workgroups per launch
+
+    def traffic_of(prefix):
+        hits = [v for k, v in traffic.items() if k.startswith(prefix)]
+        return hits[0] if len(hits) == 1 else None
 
     out = {
         "metric": "watermarked logits Gelem/s + achieved HBM GB/s (B=256,V=152064); detect seq/s",
@@ -267,16 +375,20 @@ def main():
         "roofline": {"bound": "alu", "kernel": "watermark_vec_kernel<float, self-salt>",
                      "achieved": ss_blocks, "peak": PHILOX_PEAK_GBLOCKS,
                      "unit": "G Philox4x32-10 blocks/s", "frac": ss_blocks / PHILOX_PEAK_GBLOCKS,
-                     "traffic": traffic.get(f"sbw::watermark_vec_kernel<float, 1>@{wm_tiles}"),
+                     "traffic": traffic_of("sbw::watermark_vec_kernel<float, 1,"),
                      "algorithmic_per_launch": f"{elems} Philox blocks (one per logit), "
                                                f"{bytes_wm} HBM bytes"},
         "roofline_context": {"bound": "hbm", "kernel": "watermark_vec_kernel<float, context>",
                              "achieved": ctx["hbm_gbps"], "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                              "frac": ctx["hbm_frac"],
-                             "traffic": traffic.get(f"sbw::watermark_vec_kernel<float, 0>@{wm_tiles}"),
+                             "traffic": traffic_of("sbw::watermark_vec_kernel<float, 0,"),
                              "algorithmic_per_launch": f"{bytes_wm} bytes"},
         "wall_s_timed": wall,
     }
+    if not args.no_configs:
+        del bufs
+        torch.cuda.empty_cache()
+        out["configs"] = other_configs(torch, sbw, dev, args.steps)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(x, prev, toks["self_salt"], args.cpu_seconds)
     print(json.dumps(out))
