@@ -130,13 +130,28 @@ __device__ __forceinline__ float bias_f32(float l, float delta, bool green) {
   return green ? l + delta : l;
 }
 
-// bf16 bias: exact widening, one fp32 add, round to nearest even; NaN stays NaN.
+// fp32 -> bf16 pair, round to nearest even (gfx950's v_cvt_pk_bf16_f32; NaN in,
+// NaN out).  Element a lands in the low half.
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint32_t to_bf16x2(float a, float b) {
+  const bf16x2_t r = __builtin_convertvector((f32x2_t){a, b}, bf16x2_t);
+  return __builtin_bit_cast(uint32_t, r);
+}
+
+// bf16 bias of a packed pair: exact widening, one fp32 add each, one rounding to
+// bf16; halves whose token is not green keep their bits.
+__device__ __forceinline__ uint32_t bias_bf16x2(uint32_t pair, float delta, bool green_lo,
+                                                bool green_hi) {
+  const float lo = __uint_as_float(pair << 16) + delta;
+  const float hi = __uint_as_float(pair & 0xFFFF0000u) + delta;
+  const uint32_t biased = to_bf16x2(lo, hi);
+  const uint32_t take = (green_lo ? 0x0000FFFFu : 0u) | (green_hi ? 0xFFFF0000u : 0u);
+  return (biased & take) | (pair & ~take);
+}
+
 __device__ __forceinline__ uint16_t bias_bf16(uint16_t l, float delta, bool green) {
-  const float s = __uint_as_float(static_cast<uint32_t>(l) << 16) + delta;
-  const uint32_t u = __float_as_uint(s);
-  const uint32_t rounded = (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
-  const uint32_t out = (s != s) ? ((u >> 16) | 0x40u) : rounded;
-  return green ? static_cast<uint16_t>(out) : l;
+  return static_cast<uint16_t>(bias_bf16x2(l, delta, green, false));
 }
 
 }  // namespace sbw

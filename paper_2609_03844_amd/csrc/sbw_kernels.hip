@@ -109,12 +109,8 @@ __device__ __forceinline__ u32x4 bias_vec_bf16(u32x4 raw, uint32_t j, const RowS
   const uint32_t in[4] = {raw.x, raw.y, raw.z, raw.w};
   uint32_t out[4];
 #pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    const uint16_t lo = bias_bf16(static_cast<uint16_t>(in[q]), delta, is_green(x[2 * q], tm1));
-    const uint16_t hi =
-        bias_bf16(static_cast<uint16_t>(in[q] >> 16), delta, is_green(x[2 * q + 1], tm1));
-    out[q] = static_cast<uint32_t>(lo) | (static_cast<uint32_t>(hi) << 16);
-  }
+  for (int q = 0; q < 4; ++q)
+    out[q] = bias_bf16x2(in[q], delta, is_green(x[2 * q], tm1), is_green(x[2 * q + 1], tm1));
   return u32x4{out[0], out[1], out[2], out[3]};
 }
 

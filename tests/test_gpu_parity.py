@@ -307,3 +307,26 @@ def test_config_c5(env, seeding):
     # the watermarked half is detected, the null half is not
     z = expect[1]
     assert np.median(z[c["N"] // 2:]) > 15 and abs(np.median(z[: c["N"] // 2])) < 1
+
+
+BF16_DELTAS = [2.0 ** -149, -(2.0 ** -149), 1e-40, -3e-39, 1e-38, 1e-30, -1e-20, 1e-10, 3e-5,
+               -1e-3, 0.0078125, 0.1, -0.3, 0.5, 1.0, -1.0, 1.5, 2.0, 3.0, -7.0, 8.0, 10.0,
+               100.0, -1e3, 12345.678, 1e6, -3e7, 1e10, 1e20, -1e30, 3e38, -3e38, 0.0, -0.0,
+               1 / 3, 2 / 3, math.pi, -math.e, math.sqrt(2)]
+
+
+@pytest.mark.parametrize("layout", ["vector", "unaligned"])
+def test_bf16_rounding_every_pattern(env, layout):
+    # Every bf16 bit pattern, all green (gamma = 1), one fp32 add and one rounding to
+    # bf16 per element, for deltas from the smallest subnormal to 3e38: covers ties,
+    # carries into the exponent, overflow to infinity, subnormal sums and NaN inputs.
+    x = np.arange(1 << 16, dtype=np.uint32).astype(np.uint16).reshape(1, -1)
+    prev = np.array([7], dtype=np.int32)
+    for delta in BF16_DELTAS:
+        say(f"bf16 rounding {layout} delta={delta!r}")
+        if layout == "vector":
+            got = run_watermark(env, x, prev, KEY, 1.0, delta, "context")
+        else:
+            got = run_watermark(env, x, prev, KEY, 1.0, delta, "context", offset=1)
+        assert_logits_equal(got, oracle.watermark(x, prev, KEY, 1.0, delta, "context"),
+                            f"bf16 delta={delta!r}")
