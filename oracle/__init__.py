@@ -73,6 +73,14 @@ def _declare(l: ctypes.CDLL) -> ctypes.CDLL:
         "oracle_bias_f32_many": (None, [P, i64, f32, P]),
         "oracle_bias_bf16_many": (None, [P, i64, f32, P]),
         "oracle_f32_to_bf16_many": (None, [P, i64, P]),
+        "oracle_seed_context_w": (u64, [u64, P, i64]),
+        "oracle_seed_self_salt_w": (u64, [u64, P, i64, u32]),
+        "oracle_watermark_f32_w": (None, [P, i64, i64, i64, P, i64, u64, f64, f32, i32]),
+        "oracle_watermark_bf16_w": (None, [P, i64, i64, i64, P, i64, u64, f64, f32, i32]),
+        "oracle_green_mask_w": (None, [P, i64, i64, P, i64, u64, f64, i32]),
+        "oracle_detect_w": (None, [P, i64, i64, i64, i64, u64, f64, i32, P, P]),
+        "oracle_seed_w_many": (None, [u64, P, i64, P, i64, i32, P]),
+        "oracle_is_green_w_many": (None, [u64, P, i64, P, i64, f64, i32, P]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(l, name)
@@ -221,4 +229,66 @@ def detect(tokens: np.ndarray, key: int, gamma: float, seeding="context"):
     z = np.empty(N, dtype=np.float64)
     lib().oracle_detect(_ptr(tok), N, L, L, key, float(gamma), _seeding(seeding),
                         _ptr(counts), _ptr(z))
+    return counts, z
+
+
+# --- context width h (window of the h tokens before each position) ----------------
+
+def _context(context, rows: int | None = None) -> np.ndarray:
+    c = np.ascontiguousarray(context, dtype=np.int32)
+    if c.ndim == 1:
+        c = c.reshape(-1, 1)
+    if c.ndim != 2 or (rows is not None and c.shape[0] != rows):
+        raise ValueError("context must be [rows, width]")
+    return c
+
+
+def seed_w_many(key: int, context, cand, seeding) -> np.ndarray:
+    c = _context(context)
+    cand = np.ascontiguousarray(np.broadcast_to(np.asarray(cand, dtype=np.int32), (c.shape[0],)))
+    out = np.empty(c.shape[0], dtype=np.uint64)
+    lib().oracle_seed_w_many(key, _ptr(c), c.shape[1], _ptr(cand), c.shape[0], _seeding(seeding),
+                             _ptr(out))
+    return out
+
+
+def is_green_w_many(key: int, context, cand, gamma: float, seeding) -> np.ndarray:
+    c = _context(context)
+    cand = np.ascontiguousarray(cand, dtype=np.int32)
+    assert cand.shape == (c.shape[0],)
+    out = np.empty(c.shape[0], dtype=np.uint8)
+    lib().oracle_is_green_w_many(key, _ptr(c), c.shape[1], _ptr(cand), c.shape[0], float(gamma),
+                                 _seeding(seeding), _ptr(out))
+    return out.astype(bool)
+
+
+def watermark_w(logits: np.ndarray, context, key: int, gamma: float, delta: float,
+                seeding="context") -> np.ndarray:
+    """Width-h watermark: context [B, h] holds the h tokens before this step per row."""
+    out = np.array(logits, copy=True, order="C")
+    B, V = out.shape
+    c = _context(context, B)
+    fn = lib().oracle_watermark_f32_w if out.dtype == np.float32 else lib().oracle_watermark_bf16_w
+    if out.dtype not in (np.float32, np.uint16):
+        raise TypeError("logits must be float32 or uint16 (bf16 bits)")
+    fn(_ptr(out), B, V, V, _ptr(c), c.shape[1], key, float(gamma), float(delta), _seeding(seeding))
+    return out
+
+
+def green_mask_w(B: int, V: int, context, key: int, gamma: float, seeding="context") -> np.ndarray:
+    c = _context(context, B)
+    out = np.empty((B, (V + 31) // 32), dtype=np.uint32)
+    lib().oracle_green_mask_w(_ptr(out), B, V, _ptr(c), c.shape[1], key, float(gamma),
+                              _seeding(seeding))
+    return out
+
+
+def detect_w(tokens: np.ndarray, width: int, key: int, gamma: float, seeding="context"):
+    """Width-h detect: positions h..L-1, each under the h tokens before it (T = L - h)."""
+    tok = np.ascontiguousarray(tokens, dtype=np.int32)
+    N, L = tok.shape
+    counts = np.empty(N, dtype=np.int32)
+    z = np.empty(N, dtype=np.float64)
+    lib().oracle_detect_w(_ptr(tok), N, L, L, int(width), key, float(gamma), _seeding(seeding),
+                          _ptr(counts), _ptr(z))
     return counts, z

@@ -300,3 +300,122 @@ void oracle_f32_to_bf16_many(const float *in, int64_t n, uint16_t *out)
 {
     for (int64_t i = 0; i < n; ++i) out[i] = oracle_f32_to_bf16(in[i]);
 }
+
+/* ------------------------------------------------------------------------- */
+/* Context width h (SBW-4 and SBW-ss-V in the scheme table of App. D; the      */
+/* isolated benchmark of App. E).  The window is the h tokens before position   */
+/* t, context[0..h-1]; both PRFs are symmetric in the window, so its order does */
+/* not matter.                                                                   */
+/*   R3h  additive PRF:   r = K * (p_1 + ... + p_h) mod 2^64, p_i as uint32      */
+/*   R5h  anchored minhash with self-salt over {p_1..p_h, v}, anchored on v:     */
+/*        r = min_u64( min_i K*J(p_i)*J(v), K*J(v)*J(v) )                        */
+/*   R6h  detection scores positions h..L-1 (T = L - h) under the h tokens       */
+/*        before each position.                                                 */
+/* Width 1 is exactly the definitions above.                                     */
+/* ------------------------------------------------------------------------- */
+
+uint64_t oracle_seed_context_w(uint64_t key, const int32_t *context, int64_t width)
+{
+    uint64_t sum = 0;
+    for (int64_t i = 0; i < width; ++i) sum += (uint64_t)(uint32_t)context[i];
+    return key * sum;
+}
+
+uint64_t oracle_seed_self_salt_w(uint64_t key, const int32_t *context, int64_t width,
+                                 uint32_t cand)
+{
+    uint64_t hv = (uint64_t)oracle_jenkins32(cand);
+    uint64_t best = key * hv * hv;                       /* the candidate itself */
+    for (int64_t i = 0; i < width; ++i) {
+        uint64_t term = key * (uint64_t)oracle_jenkins32((uint32_t)context[i]) * hv;
+        if (term < best) best = term;
+    }
+    return best;
+}
+
+uint64_t oracle_seed_w(uint64_t key, const int32_t *context, int64_t width, uint32_t cand,
+                       int seeding)
+{
+    if (seeding == ORACLE_SEED_SELF_SALT)
+        return oracle_seed_self_salt_w(key, context, width, cand);
+    return oracle_seed_context_w(key, context, width);
+}
+
+int oracle_is_green_w(uint64_t key, const int32_t *context, int64_t width, uint32_t cand,
+                      uint64_t threshold, int seeding)
+{
+    uint64_t r = oracle_seed_w(key, context, width, cand, seeding);
+    return (uint64_t)oracle_cbrng(cand, r) < threshold;
+}
+
+/* context: [B, width] int32, row-major. */
+void oracle_watermark_f32_w(float *logits, int64_t B, int64_t V, int64_t row_stride,
+                            const int32_t *context, int64_t width, uint64_t key, double gamma,
+                            float delta, int seeding)
+{
+    uint64_t threshold = oracle_threshold(gamma);
+    for (int64_t b = 0; b < B; ++b)
+        for (int64_t v = 0; v < V; ++v)
+            if (oracle_is_green_w(key, context + b * width, width, (uint32_t)v, threshold, seeding)) {
+                float *l = &logits[b * row_stride + v];
+                *l = oracle_bias_f32(*l, delta);
+            }
+}
+
+void oracle_watermark_bf16_w(uint16_t *logits, int64_t B, int64_t V, int64_t row_stride,
+                             const int32_t *context, int64_t width, uint64_t key, double gamma,
+                             float delta, int seeding)
+{
+    uint64_t threshold = oracle_threshold(gamma);
+    for (int64_t b = 0; b < B; ++b)
+        for (int64_t v = 0; v < V; ++v)
+            if (oracle_is_green_w(key, context + b * width, width, (uint32_t)v, threshold, seeding)) {
+                uint16_t *l = &logits[b * row_stride + v];
+                *l = oracle_bias_bf16(*l, delta);
+            }
+}
+
+void oracle_green_mask_w(uint32_t *bits, int64_t B, int64_t V, const int32_t *context,
+                         int64_t width, uint64_t key, double gamma, int seeding)
+{
+    uint64_t threshold = oracle_threshold(gamma);
+    int64_t words = (V + 31) / 32;
+    for (int64_t i = 0; i < B * words; ++i) bits[i] = 0u;
+    for (int64_t b = 0; b < B; ++b)
+        for (int64_t v = 0; v < V; ++v)
+            if (oracle_is_green_w(key, context + b * width, width, (uint32_t)v, threshold, seeding))
+                bits[b * words + v / 32] |= 1u << (v % 32);
+}
+
+void oracle_detect_w(const int32_t *tokens, int64_t N, int64_t L, int64_t row_stride,
+                     int64_t width, uint64_t key, double gamma, int seeding,
+                     int32_t *green_counts, double *z)
+{
+    uint64_t threshold = oracle_threshold(gamma);
+    int64_t T = L > width ? L - width : 0;
+    for (int64_t n = 0; n < N; ++n) {
+        const int32_t *row = tokens + n * row_stride;
+        int64_t count = 0;
+        for (int64_t i = width; i < L; ++i)
+            count += oracle_is_green_w(key, row + i - width, width, (uint32_t)row[i], threshold,
+                                       seeding);
+        green_counts[n] = (int32_t)count;
+        z[n] = oracle_z_score(count, T, gamma);
+    }
+}
+
+void oracle_seed_w_many(uint64_t key, const int32_t *context, int64_t width, const int32_t *cand,
+                        int64_t n, int seeding, uint64_t *out)
+{
+    for (int64_t i = 0; i < n; ++i)
+        out[i] = oracle_seed_w(key, context + i * width, width, (uint32_t)cand[i], seeding);
+}
+
+void oracle_is_green_w_many(uint64_t key, const int32_t *context, int64_t width,
+                            const int32_t *cand, int64_t n, double gamma, int seeding, uint8_t *out)
+{
+    uint64_t threshold = oracle_threshold(gamma);
+    for (int64_t i = 0; i < n; ++i)
+        out[i] = (uint8_t)oracle_is_green_w(key, context + i * width, width, (uint32_t)cand[i],
+                                            threshold, seeding);
+}

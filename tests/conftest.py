@@ -4,8 +4,10 @@ import sys
 import pytest
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
-if ROOT not in sys.path:
-    sys.path.insert(0, ROOT)
+HERE = os.path.dirname(os.path.abspath(__file__))
+for path in (ROOT, HERE):
+    if path not in sys.path:
+        sys.path.insert(0, path)
 
 
 def pytest_configure(config):
@@ -23,3 +25,10 @@ def pytest_collection_modifyitems(config, items):
                 have_gpu = torch.cuda.is_available()
             if not have_gpu:
                 item.add_marker(pytest.mark.skip(reason="no GPU visible"))
+
+
+@pytest.fixture(scope="session")
+def xcheck_libs(tmp_path_factory):
+    """Independent open-source Philox engines built for the host (test-only)."""
+    import engines
+    return engines.build(tmp_path_factory.mktemp("xcheck"))

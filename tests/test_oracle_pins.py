@@ -17,6 +17,7 @@ import numpy as np
 import pytest
 
 import oracle
+from engines import engine_words as _engine_words
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 GOLDEN = os.path.join(HERE, "golden")
@@ -38,37 +39,6 @@ def _kat():
 @pytest.mark.parametrize("ctr,key,expect", _kat())
 def test_philox_known_answers(ctr, key, expect):
     assert list(oracle.philox4x32_10(ctr, key)) == expect
-
-
-@pytest.fixture(scope="module")
-def xcheck_libs(tmp_path_factory):
-    """Independent Philox engines from open-source headers, built for the host."""
-    out = tmp_path_factory.mktemp("xcheck")
-    libs = {}
-    import torch
-    tinc = os.path.join(os.path.dirname(torch.__file__), "include")
-    aten = out / "libaten_x.so"
-    subprocess.run(["g++", "-O2", "-std=c++17", "-fPIC", "-shared", "-I", tinc, "-o", str(aten),
-                    os.path.join(HERE, "xcheck", "aten_philox.cpp")], check=True)
-    libs["aten"] = (ctypes.CDLL(str(aten)), "aten_stream_word")
-    hipcc = shutil.which("hipcc") or "/opt/rocm/bin/hipcc"
-    if os.path.exists(hipcc):
-        roc = out / "librocrand_x.so"
-        subprocess.run([hipcc, "-x", "hip", "--offload-host-only", "-O2", "-std=c++17", "-fPIC",
-                        "-shared", "-o", str(roc),
-                        os.path.join(HERE, "xcheck", "rocrand_philox.cpp")], check=True)
-        libs["rocrand"] = (ctypes.CDLL(str(roc)), "rocrand_stream_word")
-    return libs
-
-
-def _engine_words(libs, name, v, r):
-    lib, fn = libs[name]
-    v = np.ascontiguousarray(v, dtype=np.uint32)
-    r = np.ascontiguousarray(r, dtype=np.uint64)
-    out = np.empty(v.shape, np.uint32)
-    getattr(lib, fn)(ctypes.c_void_p(v.ctypes.data), ctypes.c_void_p(r.ctypes.data),
-                     ctypes.c_int64(v.size), ctypes.c_void_p(out.ctypes.data))
-    return out
 
 
 @pytest.mark.parametrize("engine", ["aten", "rocrand"])
