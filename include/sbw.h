@@ -132,6 +132,40 @@ sbw_status_t sbw_detect(const int32_t *tokens, int64_t N, int64_t L, int64_t row
                         uint64_t key, double gamma, sbw_seeding_t seeding,
                         int32_t *green_counts, double *z, void *stream);
 
+/*
+ * Context windows of width h (the full-vocabulary schemes SBW-4 and SBW-ss-V of
+ * the paper's scheme table and isolated benchmark, App. D and E).  The seed of a
+ * step is derived from the h tokens before it:
+ *   context seeding  r = key * (p_1 + ... + p_h) mod 2^64   ("additive" PRF)
+ *   self-salt        r = min_u64( min_i key*J(p_i)*J(v), key*J(v)*J(v) )
+ *                    ("anchored minhash" over the window and the candidate v)
+ * Both are symmetric in the window.  Width 1 gives exactly sbw_watermark,
+ * sbw_green_mask and sbw_detect, which are these calls with width = 1.
+ *
+ *   context      device, [B, width] int32 row-major: row b's window is
+ *                context[b*width .. b*width + width-1] (any order).
+ *   width        1 <= width <= 8; width < 1 is SBW_ERR_INVALID_ARG, width > 8
+ *                SBW_ERR_UNSUPPORTED.
+ * Other arguments, layouts and errors as for the width-1 calls.
+ */
+sbw_status_t sbw_watermark_window(void *logits, sbw_dtype_t dtype, int64_t B, int64_t V,
+                                  int64_t row_stride, const int32_t *context, int64_t width,
+                                  uint64_t key, double gamma, float delta, sbw_seeding_t seeding,
+                                  void *stream);
+
+sbw_status_t sbw_green_mask_window(uint32_t *bits, int64_t B, int64_t V, const int32_t *context,
+                                   int64_t width, uint64_t key, double gamma,
+                                   sbw_seeding_t seeding, void *stream);
+
+/*
+ * Windowed detection: position i (width <= i < L) is scored under the window
+ * tokens[n*row_stride + i-width .. i-1], so T = L - width; for L <= width the
+ * count is 0 and z is NaN.
+ */
+sbw_status_t sbw_detect_window(const int32_t *tokens, int64_t N, int64_t L, int64_t row_stride,
+                               int64_t width, uint64_t key, double gamma, sbw_seeding_t seeding,
+                               int32_t *green_counts, double *z, void *stream);
+
 /* Static description of a status code (never NULL). */
 const char *sbw_strerror(sbw_status_t status);
 

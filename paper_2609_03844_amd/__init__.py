@@ -39,8 +39,10 @@ _STATUS = {
     6: "SBW_ERR_HIP",
 }
 
-EXPORTED = ("sbw_watermark", "sbw_green_mask", "sbw_detect", "sbw_strerror",
-            "sbw_last_hip_error", "sbw_version")
+EXPORTED = ("sbw_watermark", "sbw_green_mask", "sbw_detect", "sbw_watermark_window",
+            "sbw_green_mask_window", "sbw_detect_window", "sbw_strerror", "sbw_last_hip_error",
+            "sbw_version")
+MAX_WIDTH = 8
 
 
 class SbwError(RuntimeError):
@@ -67,6 +69,12 @@ def _load() -> ctypes.CDLL:
     lib.sbw_green_mask.argtypes = [P, i64, i64, P, u64, f64, i32, P]
     lib.sbw_detect.restype = i32
     lib.sbw_detect.argtypes = [P, i64, i64, i64, u64, f64, i32, P, P, P]
+    lib.sbw_watermark_window.restype = i32
+    lib.sbw_watermark_window.argtypes = [P, i32, i64, i64, i64, P, i64, u64, f64, f32, i32, P]
+    lib.sbw_green_mask_window.restype = i32
+    lib.sbw_green_mask_window.argtypes = [P, i64, i64, P, i64, u64, f64, i32, P]
+    lib.sbw_detect_window.restype = i32
+    lib.sbw_detect_window.argtypes = [P, i64, i64, i64, i64, u64, f64, i32, P, P, P]
     lib.sbw_strerror.restype = ctypes.c_char_p
     lib.sbw_strerror.argtypes = [i32]
     lib.sbw_last_hip_error.restype = ctypes.c_char_p
@@ -114,12 +122,30 @@ def _key(key: int) -> int:
     return int(key) & 0xFFFFFFFFFFFFFFFF
 
 
+def _window(context: torch.Tensor, B: int):
+    """[B] (the previous token) or [B, h] (the h tokens before the step) -> (tensor, h)."""
+    if context.dtype != torch.int32:
+        raise ValueError("the context tokens must be int32")
+    if context.dim() == 1:
+        if context.shape[0] != B:
+            raise ValueError("prev_tokens must be int32 [B]")
+        width = 1
+    elif context.dim() == 2 and context.shape[0] == B:
+        width = context.shape[1]
+    else:
+        raise ValueError("context must be int32 [B] or [B, width]")
+    if B > 0 and not context.is_contiguous():
+        raise ValueError("the context tokens must be contiguous")
+    return context, width
+
+
 def watermark(logits: torch.Tensor, prev_tokens: torch.Tensor, key: int, gamma: float,
               delta: float, seeding="context", stream=None) -> torch.Tensor:
     """Adds delta to the green logits of every row, in place; returns ``logits``.
 
     logits: [B, V] float32 or bfloat16 on the GPU, unit stride along V (rows may be
-    padded: stride(0) >= V).  prev_tokens: [B] int32 on the same device.
+    padded: stride(0) >= V).  prev_tokens: int32 [B] (the previous token of each row)
+    or int32 [B, h] (the h tokens before the step, context width h <= 8).
     """
     if logits.dim() != 2:
         raise ValueError("logits must be [B, V]")
@@ -132,36 +158,38 @@ def watermark(logits: torch.Tensor, prev_tokens: torch.Tensor, key: int, gamma: 
     B, V = logits.shape
     if B > 0 and V > 0 and logits.stride(1) != 1:
         raise ValueError("logits must have unit stride along the vocabulary")
-    if prev_tokens.dtype != torch.int32 or prev_tokens.dim() != 1 or prev_tokens.shape[0] != B:
-        raise ValueError("prev_tokens must be int32 [B]")
-    if B > 0 and not prev_tokens.is_contiguous():
-        raise ValueError("prev_tokens must be contiguous")
+    context, width = _window(prev_tokens, B)
     row_stride = logits.stride(0) if B > 1 else max(V, logits.stride(0))
-    _check(_lib.sbw_watermark(logits.data_ptr(), dtype, B, V, row_stride,
-                              prev_tokens.data_ptr(), _key(key), float(gamma), float(delta),
-                              _seeding(seeding), _stream(stream)))
+    _check(_lib.sbw_watermark_window(logits.data_ptr(), dtype, B, V, row_stride,
+                                     context.data_ptr(), width, _key(key), float(gamma),
+                                     float(delta), _seeding(seeding), _stream(stream)))
     return logits
 
 
 def green_mask(prev_tokens: torch.Tensor, V: int, key: int, gamma: float, seeding="context",
                out: torch.Tensor | None = None, stream=None) -> torch.Tensor:
-    """Green lists as bit sets: int32 [B, ceil(V/32)], bit v%32 of word v//32."""
-    if prev_tokens.dtype != torch.int32 or prev_tokens.dim() != 1:
-        raise ValueError("prev_tokens must be int32 [B]")
+    """Green lists as bit sets: int32 [B, ceil(V/32)], bit v%32 of word v//32.
+    prev_tokens: int32 [B] or [B, h] as for watermark()."""
+    if prev_tokens.dim() not in (1, 2):
+        raise ValueError("prev_tokens must be int32 [B] or [B, width]")
     B = prev_tokens.shape[0]
+    context, width = _window(prev_tokens, B)
     words = (int(V) + 31) // 32
     if out is None:
         out = torch.empty((B, words), dtype=torch.int32, device=prev_tokens.device)
     elif out.shape != (B, words) or out.dtype != torch.int32 or not out.is_contiguous():
         raise ValueError("out must be contiguous int32 [B, ceil(V/32)]")
-    _check(_lib.sbw_green_mask(out.data_ptr(), B, int(V), prev_tokens.data_ptr(), _key(key),
-                               float(gamma), _seeding(seeding), _stream(stream)))
+    _check(_lib.sbw_green_mask_window(out.data_ptr(), B, int(V), context.data_ptr(), width,
+                                      _key(key), float(gamma), _seeding(seeding),
+                                      _stream(stream)))
     return out
 
 
 def detect(tokens: torch.Tensor, key: int, gamma: float, seeding="context",
-           counts: torch.Tensor | None = None, z: torch.Tensor | None = None, stream=None):
-    """Green count and z-score per sequence of tokens [N, L] int32 (unit stride along L)."""
+           counts: torch.Tensor | None = None, z: torch.Tensor | None = None, stream=None,
+           width: int = 1):
+    """Green count and z-score per sequence of tokens [N, L] int32 (unit stride along L).
+    Positions width..L-1 are scored under the `width` tokens before each (T = L - width)."""
     if tokens.dtype != torch.int32 or tokens.dim() != 2:
         raise ValueError("tokens must be int32 [N, L]")
     N, L = tokens.shape
@@ -177,7 +205,7 @@ def detect(tokens: torch.Tensor, key: int, gamma: float, seeding="context",
     if z.shape != (N,) or z.dtype != torch.float64 or not z.is_contiguous():
         raise ValueError("z must be contiguous float64 [N]")
     row_stride = tokens.stride(0) if N > 1 else max(L, tokens.stride(0))
-    _check(_lib.sbw_detect(tokens.data_ptr() if L > 0 else None, N, L, row_stride, _key(key),
-                           float(gamma), _seeding(seeding), counts.data_ptr(), z.data_ptr(),
-                           _stream(stream)))
+    _check(_lib.sbw_detect_window(tokens.data_ptr() if L > 0 else None, N, L, row_stride,
+                                  int(width), _key(key), float(gamma), _seeding(seeding),
+                                  counts.data_ptr(), z.data_ptr(), _stream(stream)))
     return counts, z

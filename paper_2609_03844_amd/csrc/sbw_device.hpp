@@ -108,16 +108,6 @@ __device__ __forceinline__ uint64_t mul_64x64(uint64_t a, uint64_t s) {
   return (static_cast<uint64_t>(hi) << 32) | static_cast<uint32_t>(lo);
 }
 
-// Self-salt seed with the row part precomputed: key_jp = key * J(p) mod 2^64.
-// r = min_u64(key*J(p)*J(v), key*J(v)*J(v)); the second product is key * (J(v)^2).
-__device__ __forceinline__ uint64_t self_salt_seed(uint64_t key, uint64_t key_jp,
-                                                   uint32_t v) {
-  const uint32_t jv = jenkins32(v);
-  const uint64_t with_prev = mul_64x32(key_jp, jv);
-  const uint64_t with_self = mul_64x64(key, wide_mul(jv, jv));
-  return with_prev < with_self ? with_prev : with_self;
-}
-
 // Membership: x < T with T = threshold_minus_1 + 1 in [1, 2^32].  T == 0 (gamma
 // == 0) never reaches a kernel that calls this.
 __device__ __forceinline__ bool is_green(uint32_t x, uint32_t threshold_minus_1) {

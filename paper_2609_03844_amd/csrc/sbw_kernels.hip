@@ -3,13 +3,18 @@
 // watermark   one streaming pass over the logits: each lane owns 16-byte vectors
 //             of one row (4 fp32 or 8 bf16 logits), loads them, derives the green
 //             decision in registers (seed, Philox4x32-10 draw, threshold compare)
-//             and stores them back.  Row-uniform values (previous token, context
-//             seed, key * J(p)) are computed once per workgroup in scalar
-//             registers.  Context seeding shares one Philox block between the 4
-//             tokens of a counter; self-salt needs one block per token.
+//             and stores them back.  Row-uniform values (the window of previous
+//             tokens, the context seed, key * J(p_i)) are computed once per
+//             workgroup in scalar registers.  Context seeding shares one Philox
+//             block between the 4 tokens of a counter; self-salt needs one block
+//             per token.
 // green_mask  one lane per 32-token word of the bit set.
 // detect      one wavefront per sequence; each lane scores positions i, i+64, ...
 //             and the wave counts green positions with a ballot + popcount.
+//
+// The context window: row b of a watermark call sees the `width` tokens
+// context[b*width .. b*width+width-1] (the tokens before the step); position i of a
+// detected sequence sees tokens i-width .. i-1.  Width 1 is the previous token.
 #include <hip/hip_runtime.h>
 #include <math.h>
 #include <stdint.h>
@@ -30,7 +35,10 @@ namespace {
 #define SBW_SELF_SALT_UNROLL 2 // 16-byte vectors per lane, self-salt (Philox-bound)
 #endif
 
-constexpr int kThreads = 256;     // 4 wavefronts of 64
+constexpr int kThreads = 256;            // 4 wavefronts of 64
+constexpr int kMaxWidth = 8;             // longest context window
+constexpr int64_t kMaxGrid = 1ll << 20;  // blocks; grid-stride loops cover the rest
+constexpr int64_t kMaxGridY = 65535;
 
 // Native vector types (the non-temporal builtins take these, not HIP's float4/uint4).
 typedef float f32x4 __attribute__((ext_vector_type(4)));
@@ -40,43 +48,78 @@ template <typename V>
 __device__ __forceinline__ V stream_load(const V* p) { return __builtin_nontemporal_load(p); }
 template <typename V>
 __device__ __forceinline__ void stream_store(V* p, V v) { __builtin_nontemporal_store(v, p); }
-constexpr int64_t kMaxGrid = 1ll << 20;  // blocks; grid-stride loops cover the rest
 
-// Per-row state shared by all lanes of a workgroup.
+// ---------------------------------------------------------------------------
+// Seeds.  kW is the compile-time bound on the window width: 1 for the
+// previous-token path, kMaxWidth for wider windows (runtime width <= kW).
+// ---------------------------------------------------------------------------
+template <int kW>
 struct RowSeed {
-  uint64_t key;      // the watermark key
-  uint64_t seed;     // context: key * p;  self-salt: key * J(p)
+  uint64_t key;        // the watermark key
+  uint64_t seed;       // context seeding: key * (sum of the window)
+  uint64_t kjp[kW];    // self-salt: key * J(p_i) for the window tokens
+  int width;
 };
 
-template <int kSeeding>
-__device__ __forceinline__ RowSeed row_seed(uint64_t key, uint32_t prev) {
-  if (kSeeding == kContext) return RowSeed{key, context_seed(key, prev)};
-  return RowSeed{key, key * static_cast<uint64_t>(jenkins32(prev))};
+template <int kSeeding, int kW>
+__device__ __forceinline__ RowSeed<kW> row_seed(uint64_t key, const int32_t* window, int width) {
+  RowSeed<kW> rs;
+  rs.key = key;
+  rs.width = width;
+  rs.seed = 0u;
+  if (kSeeding == kContext) {
+    uint64_t sum = 0u;
+    for (int i = 0; i < (kW == 1 ? 1 : width); ++i) sum += static_cast<uint32_t>(window[i]);
+    rs.seed = key * sum;
+  } else {
+#pragma unroll
+    for (int i = 0; i < kW; ++i)
+      rs.kjp[i] = (kW == 1 || i < width)
+                      ? key * static_cast<uint64_t>(jenkins32(static_cast<uint32_t>(window[i])))
+                      : 0u;
+  }
+  return rs;
 }
 
-template <int kSeeding>
-__device__ __forceinline__ uint32_t draw(const RowSeed& rs, uint32_t v) {
+// Self-salt seed of candidate v: min over the window and v itself of key*J(w)*J(v).
+template <int kW>
+__device__ __forceinline__ uint64_t self_salt_seed_w(const RowSeed<kW>& rs, uint32_t v) {
+  const uint32_t jv = jenkins32(v);
+  uint64_t best = mul_64x64(rs.key, wide_mul(jv, jv));
+#pragma unroll
+  for (int i = 0; i < kW; ++i) {
+    if (kW == 1 || i < rs.width) {
+      const uint64_t t = mul_64x32(rs.kjp[i], jv);
+      best = t < best ? t : best;
+    }
+  }
+  return best;
+}
+
+template <int kSeeding, int kW>
+__device__ __forceinline__ uint32_t draw(const RowSeed<kW>& rs, uint32_t v) {
   if (kSeeding == kContext) return cbrng(v, rs.seed);
-  return cbrng(v, self_salt_seed(rs.key, rs.seed, v));
+  return cbrng(v, self_salt_seed_w(rs, v));
 }
 
 // ---------------------------------------------------------------------------
-// Watermark, fp32, rows 16-byte aligned: a vector is the 4 tokens 4j..4j+3,
-// exactly the 4 words of the Philox block at counter j.
+// Watermark vectors.
+// fp32: a vector is the 4 tokens 4j..4j+3, exactly the 4 words of the Philox
+// block at counter j.  bf16: the 8 tokens 8j..8j+7 = blocks 2j and 2j+1.
 // ---------------------------------------------------------------------------
-template <int kSeeding>
-__device__ __forceinline__ f32x4 bias_vec_f32(f32x4 l, uint32_t j, const RowSeed& rs,
-                                              uint32_t tm1, float delta) {
+template <int kSeeding, int kW>
+__device__ __forceinline__ f32x4 bias_vec(f32x4 l, uint32_t j, const RowSeed<kW>& rs, uint32_t tm1,
+                                          float delta) {
   const uint32_t v = j * 4u;
   uint32_t x0, x1, x2, x3;
   if (kSeeding == kContext) {
     const Block blk = philox_block(j, key_of(rs.seed));
     x0 = blk.w0; x1 = blk.w1; x2 = blk.w2; x3 = blk.w3;
   } else {
-    x0 = philox_block(j, key_of(self_salt_seed(rs.key, rs.seed, v + 0u))).w0;
-    x1 = philox_block(j, key_of(self_salt_seed(rs.key, rs.seed, v + 1u))).w1;
-    x2 = philox_block(j, key_of(self_salt_seed(rs.key, rs.seed, v + 2u))).w2;
-    x3 = philox_block(j, key_of(self_salt_seed(rs.key, rs.seed, v + 3u))).w3;
+    x0 = philox_block(j, key_of(self_salt_seed_w(rs, v + 0u))).w0;
+    x1 = philox_block(j, key_of(self_salt_seed_w(rs, v + 1u))).w1;
+    x2 = philox_block(j, key_of(self_salt_seed_w(rs, v + 2u))).w2;
+    x3 = philox_block(j, key_of(self_salt_seed_w(rs, v + 3u))).w3;
   }
   f32x4 o;
   o.x = bias_f32(l.x, delta, is_green(x0, tm1));
@@ -86,10 +129,9 @@ __device__ __forceinline__ f32x4 bias_vec_f32(f32x4 l, uint32_t j, const RowSeed
   return o;
 }
 
-// bf16: a vector is the 8 tokens 8j..8j+7 = Philox blocks 2j and 2j+1.
-template <int kSeeding>
-__device__ __forceinline__ u32x4 bias_vec_bf16(u32x4 raw, uint32_t j, const RowSeed& rs,
-                                               uint32_t tm1, float delta) {
+template <int kSeeding, int kW>
+__device__ __forceinline__ u32x4 bias_vec(u32x4 raw, uint32_t j, const RowSeed<kW>& rs,
+                                          uint32_t tm1, float delta) {
   const uint32_t v = j * 8u;
   uint32_t x[8];
   if (kSeeding == kContext) {
@@ -102,7 +144,7 @@ __device__ __forceinline__ u32x4 bias_vec_bf16(u32x4 raw, uint32_t j, const RowS
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
       const uint32_t t = v + static_cast<uint32_t>(e);
-      x[e] = block_word(philox_block(t >> 2, key_of(self_salt_seed(rs.key, rs.seed, t))),
+      x[e] = block_word(philox_block(t >> 2, key_of(self_salt_seed_w(rs, t))),
                         static_cast<uint32_t>(e & 3));
     }
   }
@@ -114,46 +156,28 @@ __device__ __forceinline__ u32x4 bias_vec_bf16(u32x4 raw, uint32_t j, const RowS
   return u32x4{out[0], out[1], out[2], out[3]};
 }
 
-template <int kSeeding>
-__device__ __forceinline__ f32x4 bias_vec(f32x4 l, uint32_t j, const RowSeed& rs, uint32_t tm1,
-                                          float delta) {
-  return bias_vec_f32<kSeeding>(l, j, rs, tm1, delta);
-}
-template <int kSeeding>
-__device__ __forceinline__ u32x4 bias_vec(u32x4 raw, uint32_t j, const RowSeed& rs, uint32_t tm1,
-                                          float delta) {
-  return bias_vec_bf16<kSeeding>(raw, j, rs, tm1, delta);
-}
-
 // One element of either dtype (row tails and unaligned rows).
-template <typename T>
-struct Elem;
-template <>
-struct Elem<float> {
-  static __device__ __forceinline__ float bias(float l, float d, bool g) { return bias_f32(l, d, g); }
-};
-template <>
-struct Elem<uint16_t> {
-  static __device__ __forceinline__ uint16_t bias(uint16_t l, float d, bool g) {
-    return bias_bf16(l, d, g);
-  }
-};
+__device__ __forceinline__ float bias_elem(float l, float d, bool g) { return bias_f32(l, d, g); }
+__device__ __forceinline__ uint16_t bias_elem(uint16_t l, float d, bool g) {
+  return bias_bf16(l, d, g);
+}
 
-template <typename T, int kSeeding>
-__device__ __forceinline__ void bias_one(T* row, uint32_t v, const RowSeed& rs, uint32_t tm1,
+template <typename T, int kSeeding, int kW>
+__device__ __forceinline__ void bias_one(T* row, uint32_t v, const RowSeed<kW>& rs, uint32_t tm1,
                                          float delta) {
   const uint32_t x = draw<kSeeding>(rs, v);
-  row[v] = Elem<T>::bias(row[v], delta, is_green(x, tm1));
+  row[v] = bias_elem(row[v], delta, is_green(x, tm1));
 }
 
 // Vectorised watermark for rows whose start is 16-byte aligned.  Grid: x = tile of
 // kThreads * kU vectors within a row, y = row (grid-stride over rows beyond 65535).
-// Each lane issues its logits load before reading the row's previous token, so the
-// scalar load of prev[row] overlaps the HBM stream.
-template <typename T, int kSeeding, int kU>
+// Each lane issues its logits load before reading the row's window, so the scalar
+// loads of the window overlap the HBM stream.
+template <typename T, int kSeeding, int kU, int kW>
 __global__ void __launch_bounds__(kThreads)
 watermark_vec_kernel(T* __restrict__ logits, int64_t row_stride, uint32_t V, int64_t B,
-                     const int32_t* __restrict__ prev, uint64_t key, uint32_t tm1, float delta) {
+                     const int32_t* __restrict__ context, int width, uint64_t key, uint32_t tm1,
+                     float delta) {
   using VecT = typename std::conditional<sizeof(T) == 4, f32x4, u32x4>::type;
   constexpr uint32_t kPer = 16u / sizeof(T);  // elements per 16-byte vector
   const uint32_t full = V / kPer;             // complete vectors in a row
@@ -162,12 +186,13 @@ watermark_vec_kernel(T* __restrict__ logits, int64_t row_stride, uint32_t V, int
   for (int64_t row = blockIdx.y; row < B; row += gridDim.y) {
     T* row_ptr = logits + row * row_stride;
     VecT* vec = reinterpret_cast<VecT*>(row_ptr);
+    const int32_t* window = context + row * width;
     VecT buf[kU];
     if (first + kThreads * kU <= full) {
       // Whole tile inside the row: no per-vector guards, all loads in flight at once.
 #pragma unroll
       for (int u = 0; u < kU; ++u) buf[u] = stream_load(vec + first + u * kThreads + threadIdx.x);
-      const RowSeed rs = row_seed<kSeeding>(key, static_cast<uint32_t>(prev[row]));
+      const RowSeed<kW> rs = row_seed<kSeeding, kW>(key, window, width);
 #pragma unroll
       for (int u = 0; u < kU; ++u) {
         const uint32_t j = first + u * kThreads + threadIdx.x;
@@ -179,7 +204,7 @@ watermark_vec_kernel(T* __restrict__ logits, int64_t row_stride, uint32_t V, int
         const uint32_t j = first + u * kThreads + threadIdx.x;
         if (j < full) buf[u] = stream_load(vec + j);
       }
-      const RowSeed rs = row_seed<kSeeding>(key, static_cast<uint32_t>(prev[row]));
+      const RowSeed<kW> rs = row_seed<kSeeding, kW>(key, window, width);
 #pragma unroll
       for (int u = 0; u < kU; ++u) {
         const uint32_t j = first + u * kThreads + threadIdx.x;
@@ -197,14 +222,15 @@ watermark_vec_kernel(T* __restrict__ logits, int64_t row_stride, uint32_t V, int
 }
 
 // Element-wise watermark for rows that are not 16-byte aligned.
-template <typename T, int kSeeding>
+template <typename T, int kSeeding, int kW>
 __global__ void __launch_bounds__(kThreads)
 watermark_elem_kernel(T* __restrict__ logits, int64_t row_stride, uint32_t V, int64_t B,
-                      const int32_t* __restrict__ prev, uint64_t key, uint32_t tm1, float delta) {
+                      const int32_t* __restrict__ context, int width, uint64_t key, uint32_t tm1,
+                      float delta) {
   const uint32_t v = blockIdx.x * kThreads + threadIdx.x;
   for (int64_t row = blockIdx.y; row < B; row += gridDim.y) {
     if (v >= V) continue;
-    const RowSeed rs = row_seed<kSeeding>(key, static_cast<uint32_t>(prev[row]));
+    const RowSeed<kW> rs = row_seed<kSeeding, kW>(key, context + row * width, width);
     bias_one<T, kSeeding>(logits + row * row_stride, v, rs, tm1, delta);
   }
 }
@@ -212,18 +238,18 @@ watermark_elem_kernel(T* __restrict__ logits, int64_t row_stride, uint32_t V, in
 // ---------------------------------------------------------------------------
 // Green mask: one lane per 32-bit word (tokens 32w .. 32w+31).
 // ---------------------------------------------------------------------------
-template <int kSeeding>
+template <int kSeeding, int kW>
 __global__ void __launch_bounds__(kThreads)
 green_mask_kernel(uint32_t* __restrict__ bits, uint32_t V, uint32_t words_per_row,
-                  const int32_t* __restrict__ prev, uint64_t key, uint32_t tm1, int none_green,
-                  int64_t num_words) {
+                  const int32_t* __restrict__ context, int width, uint64_t key, uint32_t tm1,
+                  int none_green, int64_t num_words) {
   for (int64_t w = static_cast<int64_t>(blockIdx.x) * kThreads + threadIdx.x; w < num_words;
        w += static_cast<int64_t>(gridDim.x) * kThreads) {
     const int64_t row = w / words_per_row;
     const uint32_t word = static_cast<uint32_t>(w - row * words_per_row);
     uint32_t out = 0u;
     if (!none_green) {
-      const RowSeed rs = row_seed<kSeeding>(key, static_cast<uint32_t>(prev[row]));
+      const RowSeed<kW> rs = row_seed<kSeeding, kW>(key, context + row * width, width);
       const uint32_t v0 = word * 32u;
       if (kSeeding == kContext) {
         const Key k = key_of(rs.seed);
@@ -253,56 +279,72 @@ green_mask_kernel(uint32_t* __restrict__ bits, uint32_t V, uint32_t words_per_ro
 constexpr int kWave = 64;
 constexpr int kWavesPerBlock = kThreads / kWave;
 
-template <int kSeeding>
-__device__ __forceinline__ bool token_green(uint64_t key, uint32_t p, uint32_t v, uint32_t tm1) {
+// Membership of token v at a position whose window is w[0..width-1].
+template <int kSeeding, int kW>
+__device__ __forceinline__ bool window_green(uint64_t key, const uint32_t (&w)[kW], int width,
+                                             uint32_t v, uint32_t tm1) {
   uint64_t r;
   if (kSeeding == kContext) {
-    r = context_seed(key, p);
+    uint64_t sum = 0u;
+#pragma unroll
+    for (int i = 0; i < kW; ++i)
+      if (kW == 1 || i < width) sum += w[i];
+    r = key * sum;
   } else {
-    r = self_salt_seed(key, key * static_cast<uint64_t>(jenkins32(p)), v);
+    const uint32_t jv = jenkins32(v);
+    r = mul_64x64(key, wide_mul(jv, jv));
+#pragma unroll
+    for (int i = 0; i < kW; ++i) {
+      if (kW == 1 || i < width) {
+        const uint64_t t = mul_64x32(key * static_cast<uint64_t>(jenkins32(w[i])), jv);
+        r = t < r ? t : r;
+      }
+    }
   }
   return is_green(cbrng(v, r), tm1);
 }
 
 // Positions handled per lane per pass: a pass covers 64 * kChunk positions and
-// issues all of its token loads before any arithmetic.  The host picks kChunk from L
-// so that short sequences do not compute idle slots.
-template <int kSeeding, int kDetectChunk>
+// issues all of its token loads before any arithmetic.  The host picks kChunk from
+// the number of scored positions so that short sequences do not compute idle slots.
+template <int kSeeding, int kChunk, int kW>
 __global__ void __launch_bounds__(kThreads)
 detect_kernel(const int32_t* __restrict__ tokens, int64_t N, int64_t L, int64_t row_stride,
-              uint64_t key, uint32_t tm1, double gamma, int32_t* __restrict__ counts,
+              int width, uint64_t key, uint32_t tm1, double gamma, int32_t* __restrict__ counts,
               double* __restrict__ z) {
   const int lane = threadIdx.x % kWave;
   const int64_t wave0 = static_cast<int64_t>(blockIdx.x) * kWavesPerBlock + threadIdx.x / kWave;
   for (int64_t n = wave0; n < N; n += static_cast<int64_t>(gridDim.x) * kWavesPerBlock) {
     const int32_t* seq = tokens + n * row_stride;
     uint32_t green = 0u;  // wave-uniform count
-    for (int64_t base = 1; base < L; base += kWave * kDetectChunk) {
-      uint32_t p[kDetectChunk], v[kDetectChunk];
+    for (int64_t base = width; base < L; base += kWave * kChunk) {
+      uint32_t w[kChunk][kW], v[kChunk];
 #pragma unroll
-      for (int c = 0; c < kDetectChunk; ++c) {
+      for (int c = 0; c < kChunk; ++c) {
         const int64_t i = base + c * kWave + lane;
-        p[c] = 0u;
         v[c] = 0u;
+#pragma unroll
+        for (int k = 0; k < kW; ++k) w[c][k] = 0u;
         if (i < L) {
-          p[c] = static_cast<uint32_t>(seq[i - 1]);
           v[c] = static_cast<uint32_t>(seq[i]);
+#pragma unroll
+          for (int k = 0; k < kW; ++k)
+            if (kW == 1 || k < width) w[c][k] = static_cast<uint32_t>(seq[i - width + k]);
         }
       }
       // Independent membership chains first (instruction-level parallelism), then
       // one ballot per chunk.
-      bool g[kDetectChunk];
+      bool g[kChunk];
 #pragma unroll
-      for (int c = 0; c < kDetectChunk; ++c) {
+      for (int c = 0; c < kChunk; ++c) {
         const int64_t i = base + c * kWave + lane;
-        g[c] = token_green<kSeeding>(key, p[c], v[c], tm1) && i < L;
+        g[c] = window_green<kSeeding, kW>(key, w[c], width, v[c], tm1) && i < L;
       }
 #pragma unroll
-      for (int c = 0; c < kDetectChunk; ++c)
-        green += static_cast<uint32_t>(__popcll(__ballot(g[c])));
+      for (int c = 0; c < kChunk; ++c) green += static_cast<uint32_t>(__popcll(__ballot(g[c])));
     }
     if (lane == 0) {
-      const int64_t T = L > 1 ? L - 1 : 0;
+      const int64_t T = L > width ? L - width : 0;
       const double t = static_cast<double>(T);
       const double numerator = static_cast<double>(green) - t * gamma;
       const double denominator = sqrt(t * gamma * (1.0 - gamma));
@@ -349,7 +391,11 @@ int64_t grid_for(int64_t work_groups) { return work_groups < kMaxGrid ? work_gro
 
 bool valid_seeding(int s) { return s == SBW_SEED_CONTEXT || s == SBW_SEED_SELF_SALT; }
 
-constexpr int64_t kMaxGridY = 65535;
+sbw_status_t check_width(int64_t width) {
+  if (width < 1) return SBW_ERR_INVALID_ARG;
+  if (width > kMaxWidth) return SBW_ERR_UNSUPPORTED;
+  return SBW_OK;
+}
 
 // Vectors per lane.  Two in flight per lane measured best for both seedings on
 // MI355X: the context pass reaches ~80 % of HBM peak (one per lane: ~75 %), and the
@@ -357,9 +403,9 @@ constexpr int64_t kMaxGridY = 65535;
 template <int kSeeding>
 constexpr int unroll_for() { return kSeeding == kContext ? SBW_CONTEXT_UNROLL : SBW_SELF_SALT_UNROLL; }
 
-template <typename T, int kSeeding>
+template <typename T, int kSeeding, int kW>
 void launch_watermark(void* logits, int64_t B, uint32_t V, int64_t row_stride,
-                      const int32_t* prev, uint64_t key, uint32_t tm1, float delta,
+                      const int32_t* context, int width, uint64_t key, uint32_t tm1, float delta,
                       bool aligned, hipStream_t stream) {
   T* p = static_cast<T*>(logits);
   const uint32_t rows = static_cast<uint32_t>(B < kMaxGridY ? B : kMaxGridY);
@@ -368,31 +414,49 @@ void launch_watermark(void* logits, int64_t B, uint32_t V, int64_t row_stride,
     constexpr uint32_t kPer = 16u / sizeof(T);
     const uint64_t vectors = (static_cast<uint64_t>(V) + kPer - 1) / kPer;
     const uint32_t tiles = static_cast<uint32_t>((vectors + kThreads * kU - 1) / (kThreads * kU));
-    hipLaunchKernelGGL((watermark_vec_kernel<T, kSeeding, kU>), dim3(tiles, rows), dim3(kThreads),
-                       0, stream, p, row_stride, V, B, prev, key, tm1, delta);
+    hipLaunchKernelGGL((watermark_vec_kernel<T, kSeeding, kU, kW>), dim3(tiles, rows),
+                       dim3(kThreads), 0, stream, p, row_stride, V, B, context, width, key, tm1,
+                       delta);
   } else {
     const uint32_t tiles = static_cast<uint32_t>((static_cast<uint64_t>(V) + kThreads - 1) / kThreads);
-    hipLaunchKernelGGL((watermark_elem_kernel<T, kSeeding>), dim3(tiles, rows), dim3(kThreads), 0,
-                       stream, p, row_stride, V, B, prev, key, tm1, delta);
+    hipLaunchKernelGGL((watermark_elem_kernel<T, kSeeding, kW>), dim3(tiles, rows), dim3(kThreads),
+                       0, stream, p, row_stride, V, B, context, width, key, tm1, delta);
   }
 }
 
-template <int kSeeding>
+template <typename T>
+void dispatch_watermark(void* logits, int64_t B, uint32_t V, int64_t row_stride,
+                        const int32_t* context, int width, uint64_t key, uint32_t tm1, float delta,
+                        sbw_seeding_t seeding, bool aligned, hipStream_t st) {
+  // Context seeding folds any window into one row seed; self-salt needs the window
+  // per candidate, so wider windows take the kMaxWidth instantiation.
+  if (seeding == SBW_SEED_CONTEXT)
+    launch_watermark<T, kContext, kMaxWidth>(logits, B, V, row_stride, context, width, key, tm1,
+                                             delta, aligned, st);
+  else if (width == 1)
+    launch_watermark<T, kSelfSalt, 1>(logits, B, V, row_stride, context, width, key, tm1, delta,
+                                      aligned, st);
+  else
+    launch_watermark<T, kSelfSalt, kMaxWidth>(logits, B, V, row_stride, context, width, key, tm1,
+                                              delta, aligned, st);
+}
+
+template <int kSeeding, int kW>
 void launch_detect(int64_t positions, int64_t blocks, hipStream_t st, const int32_t* tokens,
-                   int64_t N, int64_t L, int64_t row_stride, uint64_t key, uint32_t tm1,
+                   int64_t N, int64_t L, int64_t row_stride, int width, uint64_t key, uint32_t tm1,
                    double gamma, int32_t* counts, double* z) {
   if (positions <= kWave)
-    hipLaunchKernelGGL((detect_kernel<kSeeding, 1>), dim3(blocks), dim3(kThreads), 0, st, tokens,
-                       N, L, row_stride, key, tm1, gamma, counts, z);
+    hipLaunchKernelGGL((detect_kernel<kSeeding, 1, kW>), dim3(blocks), dim3(kThreads), 0, st,
+                       tokens, N, L, row_stride, width, key, tm1, gamma, counts, z);
   else if (positions <= 2 * kWave)
-    hipLaunchKernelGGL((detect_kernel<kSeeding, 2>), dim3(blocks), dim3(kThreads), 0, st, tokens,
-                       N, L, row_stride, key, tm1, gamma, counts, z);
-  else if (positions <= 4 * kWave)
-    hipLaunchKernelGGL((detect_kernel<kSeeding, 4>), dim3(blocks), dim3(kThreads), 0, st, tokens,
-                       N, L, row_stride, key, tm1, gamma, counts, z);
+    hipLaunchKernelGGL((detect_kernel<kSeeding, 2, kW>), dim3(blocks), dim3(kThreads), 0, st,
+                       tokens, N, L, row_stride, width, key, tm1, gamma, counts, z);
+  else if (positions <= 4 * kWave || kW > 1)
+    hipLaunchKernelGGL((detect_kernel<kSeeding, 4, kW>), dim3(blocks), dim3(kThreads), 0, st,
+                       tokens, N, L, row_stride, width, key, tm1, gamma, counts, z);
   else
-    hipLaunchKernelGGL((detect_kernel<kSeeding, 8>), dim3(blocks), dim3(kThreads), 0, st, tokens,
-                       N, L, row_stride, key, tm1, gamma, counts, z);
+    hipLaunchKernelGGL((detect_kernel<kSeeding, 8, kW>), dim3(blocks), dim3(kThreads), 0, st,
+                       tokens, N, L, row_stride, width, key, tm1, gamma, counts, z);
 }
 
 }  // namespace
@@ -402,21 +466,24 @@ using namespace sbw;
 
 extern "C" {
 
-sbw_status_t sbw_watermark(void* logits, sbw_dtype_t dtype, int64_t B, int64_t V,
-                           int64_t row_stride, const int32_t* prev_tokens, uint64_t key,
-                           double gamma, float delta, sbw_seeding_t seeding, void* stream) {
+sbw_status_t sbw_watermark_window(void* logits, sbw_dtype_t dtype, int64_t B, int64_t V,
+                                  int64_t row_stride, const int32_t* context, int64_t width,
+                                  uint64_t key, double gamma, float delta, sbw_seeding_t seeding,
+                                  void* stream) {
   if (B < 0 || V < 0 || row_stride < V) return SBW_ERR_INVALID_ARG;
+  sbw_status_t s = check_width(width);
+  if (s != SBW_OK) return s;
   if (dtype != SBW_F32 && dtype != SBW_BF16) return SBW_ERR_UNSUPPORTED;
   if (!valid_seeding(seeding)) return SBW_ERR_UNSUPPORTED;
   if (!(gamma >= 0.0 && gamma <= 1.0)) return SBW_ERR_GAMMA;
   if (!isfinite(delta)) return SBW_ERR_DELTA;
   if (V >= (int64_t{1} << 32)) return SBW_ERR_UNSUPPORTED;  // token ids are 32-bit
   if (B == 0 || V == 0) return SBW_OK;
-  if (logits == nullptr || prev_tokens == nullptr) return SBW_ERR_INVALID_ARG;
+  if (logits == nullptr || context == nullptr) return SBW_ERR_INVALID_ARG;
   if (B > INT64_MAX / 4 / row_stride) return SBW_ERR_UNSUPPORTED;
   const uint64_t T = threshold_of(gamma);
   if (T == 0) return SBW_OK;  // nothing is green: the logits stay as they are
-  sbw_status_t s = check_device();
+  s = check_device();
   if (s != SBW_OK) return s;
 
   const size_t esize = dtype == SBW_F32 ? 4 : 2;
@@ -424,54 +491,71 @@ sbw_status_t sbw_watermark(void* logits, sbw_dtype_t dtype, int64_t B, int64_t V
                        ((static_cast<uint64_t>(row_stride) * esize) % 16 == 0);
   const uint32_t tm1 = static_cast<uint32_t>(T - 1);
   const uint32_t v32 = static_cast<uint32_t>(V);
+  const int w = static_cast<int>(width);
   hipStream_t st = static_cast<hipStream_t>(stream);
-  if (dtype == SBW_F32) {
-    if (seeding == SBW_SEED_CONTEXT)
-      launch_watermark<float, kContext>(logits, B, v32, row_stride, prev_tokens, key, tm1, delta, aligned, st);
-    else
-      launch_watermark<float, kSelfSalt>(logits, B, v32, row_stride, prev_tokens, key, tm1, delta, aligned, st);
-  } else {
-    if (seeding == SBW_SEED_CONTEXT)
-      launch_watermark<uint16_t, kContext>(logits, B, v32, row_stride, prev_tokens, key, tm1, delta, aligned, st);
-    else
-      launch_watermark<uint16_t, kSelfSalt>(logits, B, v32, row_stride, prev_tokens, key, tm1, delta, aligned, st);
-  }
+  if (dtype == SBW_F32)
+    dispatch_watermark<float>(logits, B, v32, row_stride, context, w, key, tm1, delta, seeding,
+                              aligned, st);
+  else
+    dispatch_watermark<uint16_t>(logits, B, v32, row_stride, context, w, key, tm1, delta, seeding,
+                                 aligned, st);
   return after_launch();
 }
 
-sbw_status_t sbw_green_mask(uint32_t* bits, int64_t B, int64_t V, const int32_t* prev_tokens,
-                            uint64_t key, double gamma, sbw_seeding_t seeding, void* stream) {
+sbw_status_t sbw_watermark(void* logits, sbw_dtype_t dtype, int64_t B, int64_t V,
+                           int64_t row_stride, const int32_t* prev_tokens, uint64_t key,
+                           double gamma, float delta, sbw_seeding_t seeding, void* stream) {
+  return sbw_watermark_window(logits, dtype, B, V, row_stride, prev_tokens, 1, key, gamma, delta,
+                              seeding, stream);
+}
+
+sbw_status_t sbw_green_mask_window(uint32_t* bits, int64_t B, int64_t V, const int32_t* context,
+                                   int64_t width, uint64_t key, double gamma,
+                                   sbw_seeding_t seeding, void* stream) {
   if (B < 0 || V < 0) return SBW_ERR_INVALID_ARG;
+  sbw_status_t s = check_width(width);
+  if (s != SBW_OK) return s;
   if (!valid_seeding(seeding)) return SBW_ERR_UNSUPPORTED;
   if (!(gamma >= 0.0 && gamma <= 1.0)) return SBW_ERR_GAMMA;
   if (V >= (int64_t{1} << 32)) return SBW_ERR_UNSUPPORTED;
   if (B == 0 || V == 0) return SBW_OK;
-  if (bits == nullptr || prev_tokens == nullptr) return SBW_ERR_INVALID_ARG;
+  if (bits == nullptr || context == nullptr) return SBW_ERR_INVALID_ARG;
   const int64_t words = (V + 31) / 32;
   if (B > INT64_MAX / 4 / words) return SBW_ERR_UNSUPPORTED;
-  sbw_status_t s = check_device();
+  s = check_device();
   if (s != SBW_OK) return s;
 
   const uint64_t T = threshold_of(gamma);
   const uint32_t tm1 = T == 0 ? 0u : static_cast<uint32_t>(T - 1);
   const int64_t num_words = B * words;
   const int64_t blocks = grid_for((num_words + kThreads - 1) / kThreads);
+  const int w = static_cast<int>(width);
+  const int none = T == 0 ? 1 : 0;
   hipStream_t st = static_cast<hipStream_t>(stream);
+  const uint32_t v32 = static_cast<uint32_t>(V), wpr = static_cast<uint32_t>(words);
   if (seeding == SBW_SEED_CONTEXT)
-    hipLaunchKernelGGL(green_mask_kernel<kContext>, dim3(blocks), dim3(kThreads), 0, st, bits,
-                       static_cast<uint32_t>(V), static_cast<uint32_t>(words), prev_tokens, key,
-                       tm1, T == 0 ? 1 : 0, num_words);
+    hipLaunchKernelGGL((green_mask_kernel<kContext, kMaxWidth>), dim3(blocks), dim3(kThreads), 0,
+                       st, bits, v32, wpr, context, w, key, tm1, none, num_words);
+  else if (w == 1)
+    hipLaunchKernelGGL((green_mask_kernel<kSelfSalt, 1>), dim3(blocks), dim3(kThreads), 0, st,
+                       bits, v32, wpr, context, w, key, tm1, none, num_words);
   else
-    hipLaunchKernelGGL(green_mask_kernel<kSelfSalt>, dim3(blocks), dim3(kThreads), 0, st, bits,
-                       static_cast<uint32_t>(V), static_cast<uint32_t>(words), prev_tokens, key,
-                       tm1, T == 0 ? 1 : 0, num_words);
+    hipLaunchKernelGGL((green_mask_kernel<kSelfSalt, kMaxWidth>), dim3(blocks), dim3(kThreads), 0,
+                       st, bits, v32, wpr, context, w, key, tm1, none, num_words);
   return after_launch();
 }
 
-sbw_status_t sbw_detect(const int32_t* tokens, int64_t N, int64_t L, int64_t row_stride,
-                        uint64_t key, double gamma, sbw_seeding_t seeding,
-                        int32_t* green_counts, double* z, void* stream) {
+sbw_status_t sbw_green_mask(uint32_t* bits, int64_t B, int64_t V, const int32_t* prev_tokens,
+                            uint64_t key, double gamma, sbw_seeding_t seeding, void* stream) {
+  return sbw_green_mask_window(bits, B, V, prev_tokens, 1, key, gamma, seeding, stream);
+}
+
+sbw_status_t sbw_detect_window(const int32_t* tokens, int64_t N, int64_t L, int64_t row_stride,
+                               int64_t width, uint64_t key, double gamma, sbw_seeding_t seeding,
+                               int32_t* green_counts, double* z, void* stream) {
   if (N < 0 || L < 0 || row_stride < L) return SBW_ERR_INVALID_ARG;
+  sbw_status_t s = check_width(width);
+  if (s != SBW_OK) return s;
   if (!valid_seeding(seeding)) return SBW_ERR_UNSUPPORTED;
   if (!(gamma > 0.0 && gamma < 1.0)) return SBW_ERR_GAMMA;
   if (L > INT32_MAX) return SBW_ERR_UNSUPPORTED;
@@ -479,21 +563,38 @@ sbw_status_t sbw_detect(const int32_t* tokens, int64_t N, int64_t L, int64_t row
   if (green_counts == nullptr || z == nullptr || (L > 0 && tokens == nullptr))
     return SBW_ERR_INVALID_ARG;
   if (row_stride > 0 && N > INT64_MAX / 4 / row_stride) return SBW_ERR_UNSUPPORTED;
-  sbw_status_t s = check_device();
+  s = check_device();
   if (s != SBW_OK) return s;
 
   const uint64_t T = threshold_of(gamma);  // in [1, 2^32 - 1] for 0 < gamma < 1
   const uint32_t tm1 = static_cast<uint32_t>(T - 1);
   const int64_t blocks = grid_for((N + kWavesPerBlock - 1) / kWavesPerBlock);
+  const int64_t positions = L > width ? L - width : 0;
+  const int w = static_cast<int>(width);
   hipStream_t st = static_cast<hipStream_t>(stream);
-  const int64_t positions = L > 1 ? L - 1 : 0;
-  if (seeding == SBW_SEED_CONTEXT)
-    launch_detect<kContext>(positions, blocks, st, tokens, N, L, row_stride, key, tm1, gamma,
-                            green_counts, z);
-  else
-    launch_detect<kSelfSalt>(positions, blocks, st, tokens, N, L, row_stride, key, tm1, gamma,
-                             green_counts, z);
+  if (w == 1) {
+    if (seeding == SBW_SEED_CONTEXT)
+      launch_detect<kContext, 1>(positions, blocks, st, tokens, N, L, row_stride, w, key, tm1,
+                                 gamma, green_counts, z);
+    else
+      launch_detect<kSelfSalt, 1>(positions, blocks, st, tokens, N, L, row_stride, w, key, tm1,
+                                  gamma, green_counts, z);
+  } else {
+    if (seeding == SBW_SEED_CONTEXT)
+      launch_detect<kContext, kMaxWidth>(positions, blocks, st, tokens, N, L, row_stride, w, key,
+                                         tm1, gamma, green_counts, z);
+    else
+      launch_detect<kSelfSalt, kMaxWidth>(positions, blocks, st, tokens, N, L, row_stride, w, key,
+                                          tm1, gamma, green_counts, z);
+  }
   return after_launch();
+}
+
+sbw_status_t sbw_detect(const int32_t* tokens, int64_t N, int64_t L, int64_t row_stride,
+                        uint64_t key, double gamma, sbw_seeding_t seeding,
+                        int32_t* green_counts, double* z, void* stream) {
+  return sbw_detect_window(tokens, N, L, row_stride, 1, key, gamma, seeding, green_counts, z,
+                           stream);
 }
 
 const char* sbw_strerror(sbw_status_t status) {
@@ -502,7 +603,7 @@ const char* sbw_strerror(sbw_status_t status) {
     case SBW_ERR_INVALID_ARG: return "invalid argument (null pointer, negative size or stride too small)";
     case SBW_ERR_GAMMA: return "gamma out of range";
     case SBW_ERR_DELTA: return "delta is not finite";
-    case SBW_ERR_UNSUPPORTED: return "unsupported dtype, seeding or size";
+    case SBW_ERR_UNSUPPORTED: return "unsupported dtype, seeding, width or size";
     case SBW_ERR_NO_DEVICE: return "no HIP device available";
     case SBW_ERR_HIP: return "HIP runtime or launch error";
   }
@@ -511,6 +612,6 @@ const char* sbw_strerror(sbw_status_t status) {
 
 const char* sbw_last_hip_error(void) { return hipGetErrorName(g_last_hip_error); }
 
-const char* sbw_version(void) { return "0.1.0"; }
+const char* sbw_version(void) { return "0.2.0"; }
 
 }  // extern "C"

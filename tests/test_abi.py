@@ -36,8 +36,9 @@ def _declared():
 
 
 def test_header_declares_the_boundary():
-    assert _declared() == ["sbw_detect", "sbw_green_mask", "sbw_last_hip_error", "sbw_strerror",
-                           "sbw_version", "sbw_watermark"]
+    assert _declared() == ["sbw_detect", "sbw_detect_window", "sbw_green_mask",
+                           "sbw_green_mask_window", "sbw_last_hip_error", "sbw_strerror",
+                           "sbw_version", "sbw_watermark", "sbw_watermark_window"]
 
 
 def test_library_exports_every_declared_symbol(sbw, lib):
@@ -193,3 +194,44 @@ def test_status_and_enum_values_match_the_header():
     # the oracle's scheme codes agree with the library's by value (no shared header)
     import oracle
     assert oracle.SEED_CONTEXT == sbw.SEED_CONTEXT and oracle.SEED_SELF_SALT == sbw.SEED_SELF_SALT
+
+
+def wmw(lib, width=4, context=DUMMY, **kw):
+    a = dict(logits=DUMMY, dtype=0, B=2, V=8, stride=8, gamma=0.25, delta=2.0, seeding=0)
+    a.update(kw)
+    return lib.sbw_watermark_window(a["logits"], a["dtype"], a["B"], a["V"], a["stride"], context,
+                                    width, KEY, a["gamma"], a["delta"], a["seeding"], None)
+
+
+def test_window_entry_points_reject_bad_arguments(lib):
+    for fn in (lambda **k: wmw(lib, **k),
+               lambda width=4, context=DUMMY: lib.sbw_green_mask_window(
+                   DUMMY, 2, 8, context, width, KEY, 0.25, 0, None),
+               lambda width=4, context=DUMMY: lib.sbw_detect_window(
+                   context, 2, 8, 8, width, KEY, 0.25, 0, DUMMY, DUMMY, None)):
+        assert fn(width=0) == INVALID
+        assert fn(width=-3) == INVALID
+        assert fn(width=9) == UNSUPPORTED
+        assert fn(context=NULL) == INVALID
+    assert wmw(lib, B=0) == OK
+    assert wmw(lib, seeding=5) == UNSUPPORTED
+    assert wmw(lib, gamma=1.5) == GAMMA
+    assert lib.sbw_detect_window(DUMMY, 0, 8, 8, 4, KEY, 0.25, 0, NULL, NULL, None) == OK
+
+
+def test_window_no_device_is_reported():
+    import paper_2609_03844_amd as sbw
+    if _gpu_visible():
+        pytest.skip("a GPU is visible; the no-device path cannot be exercised")
+    lib = sbw.raw()
+    assert wmw(lib, width=8) == NO_DEVICE
+    assert lib.sbw_detect_window(DUMMY, 2, 8, 8, 1, KEY, 0.25, 1, DUMMY, DUMMY, None) == NO_DEVICE
+
+
+def test_python_binding_window_shapes():
+    import torch
+    import paper_2609_03844_amd as sbw
+    with pytest.raises(ValueError):
+        sbw.watermark(torch.zeros(2, 3), torch.zeros(3, 4, dtype=torch.int32), KEY, 0.25, 2.0)
+    with pytest.raises(ValueError):
+        sbw.watermark(torch.zeros(2, 3), torch.zeros(2, 4, 1, dtype=torch.int32), KEY, 0.25, 2.0)

@@ -73,6 +73,11 @@ def prev_tokens(B: int, V: int, rng: np.random.Generator) -> np.ndarray:
     return rng.integers(0, V, size=B, dtype=np.int64).astype(np.int32)
 
 
+def context_tokens(B: int, width: int, V: int, rng: np.random.Generator) -> np.ndarray:
+    """[B, width] windows of uniform token ids (the tokens before a decode step)."""
+    return rng.integers(0, V, size=(B, width), dtype=np.int64).astype(np.int32)
+
+
 def uniform_tokens(N: int, L: int, V: int, rng: np.random.Generator) -> np.ndarray:
     return rng.integers(0, V, size=(N, L), dtype=np.int64).astype(np.int32)
 
@@ -103,12 +108,14 @@ Membership = Callable[[np.ndarray, np.ndarray], np.ndarray]
 
 def sample_watermarked(N: int, L: int, V: int, gamma: float, delta: float,
                        is_green: Membership, rng: np.random.Generator,
-                       candidates: int = 16) -> np.ndarray:
+                       candidates: int = 16, width: int = 1) -> np.ndarray:
     """Token sequences as a watermarked sampler would emit them from i.i.d. logits.
 
-    tok[:, 0] is uniform.  At each later step the colour is drawn (green with
+    At each step after the first `width` the colour is drawn (green with
     probability green_probability(gamma, delta)), then uniform candidates are drawn
-    until one has that colour under is_green(prev, cand).  Candidates come in
+    until one has that colour under is_green(window, cand), where window is the
+    previous token ([n] ids) for width 1, or the `width` tokens before the step
+    ([n, width] ids).  The first `width` tokens are uniform.  Candidates come in
     batches of ``candidates`` per row; the first match in draw order is kept, which
     is plain rejection sampling.  ``is_green`` is the caller's membership test.
     """
@@ -116,15 +123,19 @@ def sample_watermarked(N: int, L: int, V: int, gamma: float, delta: float,
     tok = np.empty((N, L), dtype=np.int32)
     if L == 0:
         return tok
-    tok[:, 0] = rng.integers(0, V, size=N, dtype=np.int64).astype(np.int32)
-    for i in range(1, L):
+    head = min(width, L)
+    tok[:, :head] = rng.integers(0, V, size=(N, head), dtype=np.int64).astype(np.int32)
+    for i in range(head, L):
         want = rng.random(N) < q
         chosen = np.full(N, -1, dtype=np.int64)
         pending = np.arange(N)
         while pending.size:
             cand = rng.integers(0, V, size=(pending.size, candidates), dtype=np.int64)
-            prev = np.repeat(tok[pending, i - 1], candidates)
-            green = np.asarray(is_green(prev.astype(np.int32),
+            if width == 1:
+                window = np.repeat(tok[pending, i - 1], candidates)
+            else:
+                window = np.repeat(tok[pending, i - width:i], candidates, axis=0)
+            green = np.asarray(is_green(window.astype(np.int32),
                                         cand.reshape(-1).astype(np.int32)), dtype=bool)
             match = green.reshape(pending.size, candidates) == want[pending][:, None]
             hit = match.any(axis=1)
@@ -136,10 +147,10 @@ def sample_watermarked(N: int, L: int, V: int, gamma: float, delta: float,
 
 
 def detect_inputs(N: int, L: int, V: int, gamma: float, delta: float, seeding: str,
-                  is_green: Membership, config: str = "c5") -> np.ndarray:
+                  is_green: Membership, config: str = "c5", width: int = 1) -> np.ndarray:
     """c5-style detect batch: first half uniform (null), second half watermarked."""
-    rng = rng_for(config, salt=1 if seeding == "context" else 2)
+    rng = rng_for(config, salt=(1 if seeding == "context" else 2) + 10 * (width - 1))
     n_null = N // 2
     null = uniform_tokens(n_null, L, V, rng)
-    wm = sample_watermarked(N - n_null, L, V, gamma, delta, is_green, rng)
+    wm = sample_watermarked(N - n_null, L, V, gamma, delta, is_green, rng, width=width)
     return np.concatenate([null, wm], axis=0)
