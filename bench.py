@@ -217,6 +217,51 @@ def other_configs(torch, sbw, dev, steps):
     return res
 
 
+# The paper's isolated logits-processor latency on an RTX 3090 (App. E, full-latency
+# table; V = 151936, p50 in ms, dtype not stated): context only, not a target.
+PAPER_B = (1, 2, 4, 8, 16, 32, 64, 128, 256, 512)
+PAPER_P50_MS = {
+    "SBW-4": (0.090, 0.104, 0.102, 0.100, 0.102, 0.121, 0.167, 0.262, 0.445, 0.814),
+    "SBW-ss-V": (0.097, 0.112, 0.105, 0.107, 0.106, 0.134, 0.189, 0.322, 0.599, 1.154),
+}
+
+
+def paper_table(torch, sbw, dev, calls=200, warmup=20):
+    """SBW-4 (context seeding, width 4) and SBW-ss-V (self-salt, width 4) at
+    V = 151936 fp32 for the paper's batch sizes, timed with the paper's protocol:
+    events around each call and a synchronisation between calls, 20 warmup + 200
+    timed calls (p50/p95/p99), plus the graph-replayed GPU time per launch.  Logits
+    rotate over > 400 MB of buffers so that calls read HBM."""
+    key, V, gamma, delta = workloads.PAPER_KEY, 151936, 0.25, 2.0
+    rng = np.random.default_rng(workloads.PAPER_SEED)
+    out = {}
+    for B in PAPER_B:
+        nbuf = max(2, -(-(400 << 20) // (B * V * 4)))
+        bufs = [torch.randn(B, V, device=dev) for _ in range(nbuf)]
+        ctx = torch.from_numpy(workloads.context_tokens(B, 4, V, rng)).to(dev)
+        for k, (scheme, seeding) in enumerate((("SBW-4", "context"), ("SBW-ss-V", "self_salt"))):
+            def call(i, s=seeding):
+                sbw.watermark(bufs[i % nbuf], ctx, key, gamma, delta, s)
+            lat = []
+            for i in range(warmup + calls):
+                a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                a.record()
+                call(i)
+                b.record()
+                torch.cuda.synchronize()
+                if i >= warmup:
+                    lat.append(a.elapsed_time(b))
+            gpu_us = _mean_us(torch, call, 50)
+            row = out.setdefault(scheme, {})
+            row[str(B)] = {"p50_ms": percentile(lat, 50), "p95_ms": percentile(lat, 95),
+                           "p99_ms": percentile(lat, 99), "gpu_us": gpu_us,
+                           "gelem_per_s": B * V / gpu_us / 1e3,
+                           "paper_rtx3090_p50_ms": PAPER_P50_MS[scheme][PAPER_B.index(B)]}
+        del bufs
+        torch.cuda.empty_cache()
+    return out
+
+
 def _cpu_model():
     try:
         for line in open("/proc/cpuinfo"):
@@ -389,6 +434,7 @@ def main():
         del bufs
         torch.cuda.empty_cache()
         out["configs"] = other_configs(torch, sbw, dev, args.steps)
+        out["paper_table"] = paper_table(torch, sbw, dev)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(x, prev, toks["self_salt"], args.cpu_seconds)
     print(json.dumps(out))
