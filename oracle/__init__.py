@@ -81,6 +81,8 @@ def _declare(l: ctypes.CDLL) -> ctypes.CDLL:
         "oracle_detect_w": (None, [P, i64, i64, i64, i64, u64, f64, i32, P, P]),
         "oracle_seed_w_many": (None, [u64, P, i64, P, i64, i32, P]),
         "oracle_is_green_w_many": (None, [u64, P, i64, P, i64, f64, i32, P]),
+        "oracle_watermark_argmax_f32_w": (None, [P, i64, i64, i64, P, i64, u64, f64, f32, i32, P, P]),
+        "oracle_watermark_argmax_bf16_w": (None, [P, i64, i64, i64, P, i64, u64, f64, f32, i32, P, P]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(l, name)
@@ -292,3 +294,24 @@ def detect_w(tokens: np.ndarray, width: int, key: int, gamma: float, seeding="co
     lib().oracle_detect_w(_ptr(tok), N, L, L, int(width), key, float(gamma), _seeding(seeding),
                           _ptr(counts), _ptr(z))
     return counts, z
+
+
+def watermark_argmax(logits: np.ndarray, context, key: int, gamma: float, delta: float,
+                     seeding="context"):
+    """Greedy decoding of the watermarked logits: (tokens int32 [B], values float32 [B]).
+    context: [B] previous tokens or [B, h] windows.  Ties -> smallest index; NaN is
+    the largest value (first NaN wins); -0 == +0; bf16 values are widened to fp32."""
+    x = np.ascontiguousarray(logits)
+    B, V = x.shape
+    c = _context(context, B)
+    tokens = np.empty(B, dtype=np.int32)
+    values = np.empty(B, dtype=np.float32)
+    if x.dtype == np.float32:
+        fn = lib().oracle_watermark_argmax_f32_w
+    elif x.dtype == np.uint16:
+        fn = lib().oracle_watermark_argmax_bf16_w
+    else:
+        raise TypeError("logits must be float32 or uint16 (bf16 bits)")
+    fn(_ptr(x), B, V, V, _ptr(c), c.shape[1], key, float(gamma), float(delta), _seeding(seeding),
+       _ptr(tokens), _ptr(values))
+    return tokens, values

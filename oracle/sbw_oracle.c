@@ -419,3 +419,59 @@ void oracle_is_green_w_many(uint64_t key, const int32_t *context, int64_t width,
         out[i] = (uint8_t)oracle_is_green_w(key, context + i * width, width, (uint32_t)cand[i],
                                             threshold, seeding);
 }
+
+/* ------------------------------------------------------------------------- */
+/* Greedy decoding of the watermarked logits (Eq. 2 followed by argmax): the   */
+/* index of the largest watermarked logit per row.  Ties go to the smallest    */
+/* index, a NaN counts as larger than any number (the first NaN wins), and     */
+/* -0 equals +0.  The value returned is the watermarked logit at that index    */
+/* (bf16 widened exactly to fp32).                                             */
+/* ------------------------------------------------------------------------- */
+
+static void argmax_update(float value, int64_t v, float *best, int64_t *best_v, int *best_nan)
+{
+    if (*best_nan) return;
+    if (isnan(value)) {
+        *best = value; *best_v = v; *best_nan = 1;
+        return;
+    }
+    if (*best_v < 0 || value > *best) { *best = value; *best_v = v; }
+}
+
+void oracle_watermark_argmax_f32_w(const float *logits, int64_t B, int64_t V, int64_t row_stride,
+                                   const int32_t *context, int64_t width, uint64_t key,
+                                   double gamma, float delta, int seeding, int32_t *tokens,
+                                   float *values)
+{
+    uint64_t threshold = oracle_threshold(gamma);
+    for (int64_t b = 0; b < B; ++b) {
+        float best = 0.0f; int64_t best_v = -1; int best_nan = 0;
+        for (int64_t v = 0; v < V; ++v) {
+            float l = logits[b * row_stride + v];
+            if (oracle_is_green_w(key, context + b * width, width, (uint32_t)v, threshold, seeding))
+                l = oracle_bias_f32(l, delta);
+            argmax_update(l, v, &best, &best_v, &best_nan);
+        }
+        tokens[b] = (int32_t)best_v;
+        values[b] = best;
+    }
+}
+
+void oracle_watermark_argmax_bf16_w(const uint16_t *logits, int64_t B, int64_t V,
+                                    int64_t row_stride, const int32_t *context, int64_t width,
+                                    uint64_t key, double gamma, float delta, int seeding,
+                                    int32_t *tokens, float *values)
+{
+    uint64_t threshold = oracle_threshold(gamma);
+    for (int64_t b = 0; b < B; ++b) {
+        float best = 0.0f; int64_t best_v = -1; int best_nan = 0;
+        for (int64_t v = 0; v < V; ++v) {
+            uint16_t l = logits[b * row_stride + v];
+            if (oracle_is_green_w(key, context + b * width, width, (uint32_t)v, threshold, seeding))
+                l = oracle_bias_bf16(l, delta);
+            argmax_update(f32_from_bits((uint32_t)l << 16), v, &best, &best_v, &best_nan);
+        }
+        tokens[b] = (int32_t)best_v;
+        values[b] = best;
+    }
+}
