@@ -198,6 +198,24 @@ def other_configs(torch, sbw, dev, steps):
                  "philox_gblocks_per_s": c["B"] * c["V"] / us / 1e3}
     del bufs
 
+    # fused watermark + greedy decoding on the c4 batch (B=256): one read of each logit
+    c = workloads.C4
+    x, prev = workloads.watermark_inputs("c4")
+    bufs, p = rotating(x), torch.from_numpy(prev).to(dev)
+    n = c["B"] * c["V"]
+    tokens = torch.empty(c["B"], dtype=torch.int32, device=dev)
+    values = torch.empty(c["B"], dtype=torch.float32, device=dev)
+    ws = torch.empty(sbw.argmax_workspace_size(c["B"], c["V"]), dtype=torch.int64, device=dev)
+    fused = {}
+    for seeding in ("context", "self_salt"):
+        us = _mean_us(torch, lambda i, s=seeding: sbw.watermark_argmax(
+            bufs[i % len(bufs)], p, key, c["gamma"], c["delta"], s, tokens=tokens, values=values,
+            workspace=ws), steps)
+        fused[seeding] = {"us": us, "gelem_per_s": n / us / 1e3, "hbm_gbps": 4 * n / us / 1e3,
+                          "hbm_frac": 4 * n / us / 1e3 / HBM_PEAK_GBPS}
+    res["c4_watermark_argmax"] = fused
+    del bufs
+
     # c4 at B=1024 (623 MB per buffer), both seedings
     c = workloads.C4
     x, prev = workloads.watermark_inputs("c4", B=c["B_large"])

@@ -166,6 +166,39 @@ sbw_status_t sbw_detect_window(const int32_t *tokens, int64_t N, int64_t L, int6
                                int64_t width, uint64_t key, double gamma, sbw_seeding_t seeding,
                                int32_t *green_counts, double *z, void *stream);
 
+/*
+ * sbw_watermark_argmax -- greedy decoding fused with the watermark: for every row,
+ * the index of the largest watermarked logit (Eq. 2 applied on the fly; the logits
+ * are only read, never written).  One read of each logit instead of a read and a
+ * write plus a separate argmax pass.  (A decoding epilogue of the paper's logits
+ * processor, Sec. 5.1, fused into the watermark pass.)
+ *
+ *   logits, dtype, B, V, row_stride, context, width, key, gamma, delta, seeding
+ *                as for sbw_watermark_window, except that logits is read-only and
+ *                V == 0 with B > 0 is SBW_ERR_INVALID_ARG (no token to choose).
+ *   tokens       device, [B] int32, written: the chosen token of each row.  Among
+ *                equal maxima the smallest index wins; a NaN counts as larger than
+ *                any number (the first NaN wins); -0 and +0 are equal.
+ *   values       device, [B] float, written (may be NULL): the watermarked logit at
+ *                the chosen index (bf16 logits widened exactly to fp32).
+ *   workspace    device, at least sbw_watermark_argmax_workspace(B, V) uint64
+ *                elements, caller-owned scratch (partial results per row segment);
+ *                its contents on entry do not matter and are undefined on return.
+ *                Calls that share a workspace must be ordered (same stream);
+ *                concurrent calls race.
+ * Enqueues two kernels on `stream` (the fused pass, then a per-row read-out) and no
+ * memset, so the call can be captured in a HIP graph.
+ */
+sbw_status_t sbw_watermark_argmax(const void *logits, sbw_dtype_t dtype, int64_t B, int64_t V,
+                                  int64_t row_stride, const int32_t *context, int64_t width,
+                                  uint64_t key, double gamma, float delta, sbw_seeding_t seeding,
+                                  int32_t *tokens, float *values, uint64_t *workspace,
+                                  void *stream);
+
+/* Workspace size, in uint64 elements, that sbw_watermark_argmax needs for B rows of
+ * V logits: B * ceil(V / 2048) (0 when B or V is not positive). */
+int64_t sbw_watermark_argmax_workspace(int64_t B, int64_t V);
+
 /* Static description of a status code (never NULL). */
 const char *sbw_strerror(sbw_status_t status);
 

@@ -6,6 +6,7 @@ watermark and detect path runs in the HIP kernels of ``libsbw.so``.  There is no
 fallback: if the library is missing this module raises on import.
 
     watermark(logits, prev_tokens, key, gamma, delta, seeding="context")   in place
+    watermark_argmax(logits, prev_tokens, key, gamma, delta) -> (tokens [B], values [B])
     green_mask(prev_tokens, V, key, gamma, seeding="context") -> int32 [B, ceil(V/32)]
     detect(tokens, key, gamma, seeding="context") -> (counts int32 [N], z float64 [N])
 
@@ -21,8 +22,8 @@ import torch  # loads torch's HIP runtime first, so libsbw binds to the same one
 
 from ._build import LIBRARY, build  # noqa: F401  (build is re-exported)
 
-__all__ = ["watermark", "green_mask", "detect", "SbwError", "version", "library_path",
-           "SEED_CONTEXT", "SEED_SELF_SALT"]
+__all__ = ["watermark", "watermark_argmax", "green_mask", "detect", "SbwError", "version",
+           "library_path", "SEED_CONTEXT", "SEED_SELF_SALT"]
 
 SEED_CONTEXT = 0
 SEED_SELF_SALT = 1
@@ -40,8 +41,8 @@ _STATUS = {
 }
 
 EXPORTED = ("sbw_watermark", "sbw_green_mask", "sbw_detect", "sbw_watermark_window",
-            "sbw_green_mask_window", "sbw_detect_window", "sbw_strerror", "sbw_last_hip_error",
-            "sbw_version")
+            "sbw_green_mask_window", "sbw_detect_window", "sbw_watermark_argmax",
+            "sbw_watermark_argmax_workspace", "sbw_strerror", "sbw_last_hip_error", "sbw_version")
 MAX_WIDTH = 8
 
 
@@ -75,6 +76,11 @@ def _load() -> ctypes.CDLL:
     lib.sbw_green_mask_window.argtypes = [P, i64, i64, P, i64, u64, f64, i32, P]
     lib.sbw_detect_window.restype = i32
     lib.sbw_detect_window.argtypes = [P, i64, i64, i64, i64, u64, f64, i32, P, P, P]
+    lib.sbw_watermark_argmax.restype = i32
+    lib.sbw_watermark_argmax.argtypes = [P, i32, i64, i64, i64, P, i64, u64, f64, f32, i32, P, P,
+                                         P, P]
+    lib.sbw_watermark_argmax_workspace.restype = i64
+    lib.sbw_watermark_argmax_workspace.argtypes = [i64, i64]
     lib.sbw_strerror.restype = ctypes.c_char_p
     lib.sbw_strerror.argtypes = [i32]
     lib.sbw_last_hip_error.restype = ctypes.c_char_p
@@ -164,6 +170,57 @@ def watermark(logits: torch.Tensor, prev_tokens: torch.Tensor, key: int, gamma: 
                                      context.data_ptr(), width, _key(key), float(gamma),
                                      float(delta), _seeding(seeding), _stream(stream)))
     return logits
+
+
+def watermark_argmax(logits: torch.Tensor, prev_tokens: torch.Tensor, key: int, gamma: float,
+                     delta: float, seeding="context", tokens: torch.Tensor | None = None,
+                     values: torch.Tensor | None = None, workspace: torch.Tensor | None = None,
+                     with_values: bool = True, stream=None):
+    """Greedy decoding of the watermarked logits in one read-only pass.
+
+    Returns (tokens int32 [B], values float32 [B] or None).  ``workspace`` is an int64
+    scratch tensor of at least argmax_workspace_size(B, V) elements (allocated here
+    when not given)."""
+    if logits.dim() != 2:
+        raise ValueError("logits must be [B, V]")
+    if logits.dtype == torch.float32:
+        dtype = F32
+    elif logits.dtype == torch.bfloat16:
+        dtype = BF16
+    else:
+        raise TypeError("logits must be float32 or bfloat16")
+    B, V = logits.shape
+    if B > 0 and V > 0 and logits.stride(1) != 1:
+        raise ValueError("logits must have unit stride along the vocabulary")
+    context, width = _window(prev_tokens, B)
+    dev = logits.device
+    if tokens is None:
+        tokens = torch.empty(B, dtype=torch.int32, device=dev)
+    if values is None and with_values:
+        values = torch.empty(B, dtype=torch.float32, device=dev)
+    need = argmax_workspace_size(B, V)
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.int64, device=dev)
+    if tokens.shape != (B,) or tokens.dtype != torch.int32 or not tokens.is_contiguous():
+        raise ValueError("tokens must be contiguous int32 [B]")
+    if (workspace.dtype != torch.int64 or not workspace.is_contiguous()
+            or workspace.numel() < need):
+        raise ValueError(f"workspace must be contiguous int64 with >= {need} elements")
+    if values is not None and (values.shape != (B,) or values.dtype != torch.float32
+                               or not values.is_contiguous()):
+        raise ValueError("values must be contiguous float32 [B]")
+    row_stride = logits.stride(0) if B > 1 else max(V, logits.stride(0))
+    _check(_lib.sbw_watermark_argmax(logits.data_ptr(), dtype, B, V, row_stride,
+                                     context.data_ptr(), width, _key(key), float(gamma),
+                                     float(delta), _seeding(seeding), tokens.data_ptr(),
+                                     values.data_ptr() if values is not None else None,
+                                     workspace.data_ptr(), _stream(stream)))
+    return tokens, values
+
+
+def argmax_workspace_size(B: int, V: int) -> int:
+    """uint64 elements of scratch that watermark_argmax needs for B rows of V logits."""
+    return int(_lib.sbw_watermark_argmax_workspace(int(B), int(V)))
 
 
 def green_mask(prev_tokens: torch.Tensor, V: int, key: int, gamma: float, seeding="context",

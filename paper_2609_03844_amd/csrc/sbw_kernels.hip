@@ -236,6 +236,235 @@ watermark_elem_kernel(T* __restrict__ logits, int64_t row_stride, uint32_t V, in
 }
 
 // ---------------------------------------------------------------------------
+// Greedy decoding fused with the watermark: the argmax of each watermarked row in
+// one read-only pass.  A row is cut into segments; one workgroup scans a segment
+// (kSegTiles tiles, the next tile's loads in flight while the current one is
+// reduced), keeps a running (value, index) per lane, reduces them and writes one
+// partial (value bits, index) to the workspace.  A read-out kernel then reduces the
+// partials of each row.  Candidates compare through a 64-bit key: the high word
+// orders the values (every NaN above +inf, -0 equal to +0), the low word is
+// ~index, so the maximum key is the largest value at its smallest index.
+// ---------------------------------------------------------------------------
+// Tiles per workgroup segment of the fused argmax: several for the HBM-bound context
+// pass (the next tile's loads overlap the current one's work), one for the
+// Philox-bound self-salt pass (more workgroups, more waves to hide latency).
+#ifndef SBW_ARGMAX_SEG_CONTEXT
+#define SBW_ARGMAX_SEG_CONTEXT 8
+#endif
+#ifndef SBW_ARGMAX_SEG_SELF_SALT
+#define SBW_ARGMAX_SEG_SELF_SALT 1
+#endif
+#ifndef SBW_ARGMAX_CONTEXT_UNROLL
+#define SBW_ARGMAX_CONTEXT_UNROLL 2   // 16-byte vectors per lane per tile, context pass
+#endif
+constexpr int kElemSegSteps = 8;                                // element kernel
+constexpr int64_t kArgmaxSegElems = kThreads * kElemSegSteps;   // element-kernel segment
+
+__device__ __forceinline__ uint32_t order_bits(float f) {
+  uint32_t b = __float_as_uint(f);
+  if (f != f) return 0xFFFFFFFFu;
+  if (b == 0x80000000u) b = 0u;
+  return (b & 0x80000000u) ? ~b : (b | 0x80000000u);
+}
+
+__device__ __forceinline__ uint64_t arg_key(float f, uint32_t v) {
+  return (static_cast<uint64_t>(order_bits(f)) << 32) | static_cast<uint32_t>(~v);
+}
+
+// Running argmax of one lane, which visits its indices in increasing order: a strict
+// greater-than keeps the first of equal values (and -0 == +0); the first NaN wins and
+// then stays.  `any` is false until the lane has seen an element.  (Measured faster
+// than a NaN-seeded form with fewer operations, and than a form without NaN handling.)
+struct LaneBest {
+  float v;
+  uint32_t i;
+  bool any;
+};
+
+__device__ __forceinline__ LaneBest lane_best_init() { return LaneBest{0.0f, 0u, false}; }
+
+__device__ __forceinline__ void consider(LaneBest& b, float x, uint32_t i) {
+  // Bitwise, not short-circuit, operators keep the update branch-free.
+  const bool take = static_cast<bool>(static_cast<int>(!b.any) | static_cast<int>(x > b.v) |
+                                      (static_cast<int>(x != x) & static_cast<int>(b.v == b.v)));
+  b.v = take ? x : b.v;
+  b.i = take ? i : b.i;
+  b.any = true;
+}
+
+__device__ __forceinline__ void consider_vec(LaneBest& b, f32x4 o, uint32_t j) {
+  const uint32_t v = j * 4u;
+  consider(b, o.x, v);
+  consider(b, o.y, v + 1u);
+  consider(b, o.z, v + 2u);
+  consider(b, o.w, v + 3u);
+}
+
+__device__ __forceinline__ void consider_vec(LaneBest& b, u32x4 o, uint32_t j) {
+  const uint32_t v = j * 8u;
+  const uint32_t w[4] = {o.x, o.y, o.z, o.w};
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    consider(b, __uint_as_float(w[q] << 16), v + 2u * q);
+    consider(b, __uint_as_float(w[q] & 0xFFFF0000u), v + 2u * q + 1u);
+  }
+}
+
+__device__ __forceinline__ float widen(float x) { return x; }
+__device__ __forceinline__ float widen(uint16_t x) { return __uint_as_float(static_cast<uint32_t>(x) << 16); }
+
+// A partial result: value bits in the high word, index in the low word (0 = none is
+// never produced: a workgroup's segment always holds at least one element).
+__device__ __forceinline__ uint64_t pack_partial(float v, uint32_t i) {
+  return (static_cast<uint64_t>(__float_as_uint(v)) << 32) | i;
+}
+__device__ __forceinline__ uint64_t partial_key(uint64_t p) {
+  return arg_key(__uint_as_float(static_cast<uint32_t>(p >> 32)), static_cast<uint32_t>(p));
+}
+
+// Block-wide argmax of the lanes' running bests; thread 0 stores the partial.
+__device__ __forceinline__ void block_argmax_store(const LaneBest& lb, uint64_t* out,
+                                                   uint64_t* lds_key, uint64_t* lds_part) {
+  uint64_t k = lb.any ? arg_key(lb.v, lb.i) : 0u;
+  uint64_t p = pack_partial(lb.v, lb.i);
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) {
+    const uint64_t ok = __shfl_xor(k, off, 64);
+    const uint64_t op = __shfl_xor(p, off, 64);
+    if (ok > k) { k = ok; p = op; }
+  }
+  if (threadIdx.x % 64 == 0) {
+    lds_key[threadIdx.x / 64] = k;
+    lds_part[threadIdx.x / 64] = p;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint64_t bk = lds_key[0], bp = lds_part[0];
+#pragma unroll
+    for (int w = 1; w < kThreads / 64; ++w)
+      if (lds_key[w] > bk) { bk = lds_key[w]; bp = lds_part[w]; }
+    *out = bp;
+  }
+  __syncthreads();  // the LDS slots are reused by the next row of this workgroup
+}
+
+template <typename T, int kSeeding, int kU, int kW, int kSegTiles>
+__global__ void __launch_bounds__(kThreads)
+argmax_vec_kernel(const T* __restrict__ logits, int64_t row_stride, uint32_t V, int64_t B,
+                  const int32_t* __restrict__ context, int width, uint64_t key, uint32_t tm1,
+                  int none_green, float delta, uint32_t segments, uint64_t* __restrict__ partials) {
+  using VecT = typename std::conditional<sizeof(T) == 4, f32x4, u32x4>::type;
+  __shared__ uint64_t lds_key[kThreads / 64], lds_part[kThreads / 64];
+  constexpr uint32_t kPer = 16u / sizeof(T);
+  constexpr uint32_t kTile = kThreads * kU;     // vectors per tile
+  const uint32_t full = V / kPer;
+  const uint32_t tail = V % kPer;
+  const uint32_t seg_first = blockIdx.x * (kTile * kSegTiles);
+  for (int64_t row = blockIdx.y; row < B; row += gridDim.y) {
+    const T* row_ptr = logits + row * row_stride;
+    const VecT* vec = reinterpret_cast<const VecT*>(row_ptr);
+    LaneBest lb = lane_best_init();
+    const RowSeed<kW> rs = row_seed<kSeeding, kW>(key, context + row * width, width);
+    // Whole tiles of this segment, with the next tile's loads issued before the
+    // current tile is reduced.
+    uint32_t whole = 0;
+    if (full > seg_first) whole = min((full - seg_first) / kTile, static_cast<uint32_t>(kSegTiles));
+    VecT cur[kU], nxt[kU];
+    if (whole > 0) {
+#pragma unroll
+      for (int u = 0; u < kU; ++u) cur[u] = stream_load(vec + seg_first + u * kThreads + threadIdx.x);
+    }
+    for (uint32_t t = 0; t < whole; ++t) {
+      const uint32_t first = seg_first + t * kTile;
+      if (t + 1 < whole) {
+#pragma unroll
+        for (int u = 0; u < kU; ++u) nxt[u] = stream_load(vec + first + kTile + u * kThreads + threadIdx.x);
+      }
+#pragma unroll
+      for (int u = 0; u < kU; ++u) {
+        const uint32_t j = first + u * kThreads + threadIdx.x;
+        consider_vec(lb, none_green ? cur[u] : bias_vec<kSeeding>(cur[u], j, rs, tm1, delta), j);
+      }
+#pragma unroll
+      for (int u = 0; u < kU; ++u) cur[u] = nxt[u];
+    }
+    // The part of the segment past its whole tiles: guarded vectors, then the row's
+    // partial last vector (lane 0 of the segment that holds it).
+    if (whole < kSegTiles) {
+      const uint32_t first = seg_first + whole * kTile;
+#pragma unroll
+      for (int u = 0; u < kU; ++u) {
+        const uint32_t j = first + u * kThreads + threadIdx.x;
+        if (j < full) {
+          const VecT x = stream_load(vec + j);
+          consider_vec(lb, none_green ? x : bias_vec<kSeeding>(x, j, rs, tm1, delta), j);
+        }
+      }
+      if (tail != 0u && threadIdx.x == 0 && full >= seg_first &&
+          full - seg_first < kTile * kSegTiles) {
+        for (uint32_t e = 0; e < tail; ++e) {
+          const uint32_t v = full * kPer + e;
+          const bool g = !none_green && is_green(draw<kSeeding>(rs, v), tm1);
+          consider(lb, widen(bias_elem(row_ptr[v], delta, g)), v);
+        }
+      }
+    }
+    block_argmax_store(lb, partials + row * segments + blockIdx.x, lds_key, lds_part);
+  }
+}
+
+// Rows that are not 16-byte aligned: one element per thread per step, a segment of
+// kArgmaxSegElems elements per workgroup.
+template <typename T, int kSeeding, int kW>
+__global__ void __launch_bounds__(kThreads)
+argmax_elem_kernel(const T* __restrict__ logits, int64_t row_stride, uint32_t V, int64_t B,
+                   const int32_t* __restrict__ context, int width, uint64_t key, uint32_t tm1,
+                   int none_green, float delta, uint32_t segments, uint64_t* __restrict__ partials) {
+  __shared__ uint64_t lds_key[kThreads / 64], lds_part[kThreads / 64];
+  const uint64_t seg_first = static_cast<uint64_t>(blockIdx.x) * kArgmaxSegElems;
+  for (int64_t row = blockIdx.y; row < B; row += gridDim.y) {
+    const RowSeed<kW> rs = row_seed<kSeeding, kW>(key, context + row * width, width);
+    LaneBest lb = lane_best_init();
+    for (int s = 0; s < kElemSegSteps; ++s) {
+      const uint64_t v64 = seg_first + static_cast<uint64_t>(s) * kThreads + threadIdx.x;
+      if (v64 < V) {
+        const uint32_t v = static_cast<uint32_t>(v64);
+        const bool g = !none_green && is_green(draw<kSeeding>(rs, v), tm1);
+        consider(lb, widen(bias_elem(logits[row * row_stride + v], delta, g)), v);
+      }
+    }
+    block_argmax_store(lb, partials + row * segments + blockIdx.x, lds_key, lds_part);
+  }
+}
+
+// Read-out: one wavefront per row loads the row's partials at once, reduces their
+// keys with shuffles, and lane 0 unpacks the winner.
+__global__ void __launch_bounds__(kThreads)
+argmax_finish_kernel(const uint64_t* __restrict__ partials, uint32_t segments, int64_t B,
+                     int32_t* __restrict__ tokens, float* __restrict__ values) {
+  const int lane = threadIdx.x % 64;
+  for (int64_t b = static_cast<int64_t>(blockIdx.x) * (kThreads / 64) + threadIdx.x / 64; b < B;
+       b += static_cast<int64_t>(gridDim.x) * (kThreads / 64)) {
+    const uint64_t* p = partials + b * segments;
+    uint64_t bk = 0u, bp = 0u;
+    for (uint32_t s = lane; s < segments; s += 64) {
+      const uint64_t k = partial_key(p[s]);
+      if (k > bk) { bk = k; bp = p[s]; }
+    }
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) {
+      const uint64_t ok = __shfl_xor(bk, off, 64);
+      const uint64_t op = __shfl_xor(bp, off, 64);
+      if (ok > bk) { bk = ok; bp = op; }
+    }
+    if (lane == 0) {
+      tokens[b] = static_cast<int32_t>(static_cast<uint32_t>(bp));
+      if (values != nullptr) values[b] = __uint_as_float(static_cast<uint32_t>(bp >> 32));
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
 // Green mask: one lane per 32-bit word (tokens 32w .. 32w+31).
 // ---------------------------------------------------------------------------
 template <int kSeeding, int kW>
@@ -441,6 +670,67 @@ void dispatch_watermark(void* logits, int64_t B, uint32_t V, int64_t row_stride,
                                               delta, aligned, st);
 }
 
+// Segments per row of the fused argmax: vector path and element path.
+template <int kSeeding>
+constexpr int argmax_unroll_for() {
+  return kSeeding == kContext ? SBW_ARGMAX_CONTEXT_UNROLL : SBW_SELF_SALT_UNROLL;
+}
+template <int kSeeding>
+constexpr int seg_tiles_for() {
+  return kSeeding == kContext ? SBW_ARGMAX_SEG_CONTEXT : SBW_ARGMAX_SEG_SELF_SALT;
+}
+template <typename T>
+constexpr uint64_t vec_segment_elems(int kU, int kSeg) { return (16u / sizeof(T)) * kThreads * kU * kSeg; }
+// The workspace is sized for the element path; vector segments must be at least as long.
+static_assert(vec_segment_elems<float>(SBW_ARGMAX_CONTEXT_UNROLL, SBW_ARGMAX_SEG_CONTEXT) >= kArgmaxSegElems &&
+                  vec_segment_elems<float>(SBW_SELF_SALT_UNROLL, SBW_ARGMAX_SEG_SELF_SALT) >=
+                      kArgmaxSegElems,
+              "vector segments must not outnumber element segments");
+
+template <typename T, int kSeeding, int kW>
+void launch_argmax(const void* logits, int64_t B, uint32_t V, int64_t row_stride,
+                   const int32_t* context, int width, uint64_t key, uint32_t tm1, int none,
+                   float delta, bool aligned, int32_t* tokens, float* values, uint64_t* partials,
+                   hipStream_t stream) {
+  const T* p = static_cast<const T*>(logits);
+  const uint32_t rows = static_cast<uint32_t>(B < kMaxGridY ? B : kMaxGridY);
+  uint32_t segments;
+  if (aligned) {
+    constexpr int kU = argmax_unroll_for<kSeeding>();
+    constexpr int kSeg = seg_tiles_for<kSeeding>();
+    const uint64_t seg = vec_segment_elems<T>(kU, kSeg);
+    segments = static_cast<uint32_t>((static_cast<uint64_t>(V) + seg - 1) / seg);
+    hipLaunchKernelGGL((argmax_vec_kernel<T, kSeeding, kU, kW, kSeg>), dim3(segments, rows),
+                       dim3(kThreads), 0, stream, p, row_stride, V, B, context, width, key, tm1,
+                       none, delta, segments, partials);
+  } else {
+    segments = static_cast<uint32_t>((static_cast<uint64_t>(V) + kArgmaxSegElems - 1) /
+                                     kArgmaxSegElems);
+    hipLaunchKernelGGL((argmax_elem_kernel<T, kSeeding, kW>), dim3(segments, rows), dim3(kThreads),
+                       0, stream, p, row_stride, V, B, context, width, key, tm1, none, delta,
+                       segments, partials);
+  }
+  const int64_t row_blocks = grid_for((B + kThreads / 64 - 1) / (kThreads / 64));
+  hipLaunchKernelGGL(argmax_finish_kernel, dim3(row_blocks), dim3(kThreads), 0, stream, partials,
+                     segments, B, tokens, values);
+}
+
+template <typename T>
+void dispatch_argmax(const void* logits, int64_t B, uint32_t V, int64_t row_stride,
+                     const int32_t* context, int width, uint64_t key, uint32_t tm1, int none,
+                     float delta, sbw_seeding_t seeding, bool aligned, int32_t* tokens,
+                     float* values, uint64_t* best, hipStream_t st) {
+  if (seeding == SBW_SEED_CONTEXT)
+    launch_argmax<T, kContext, kMaxWidth>(logits, B, V, row_stride, context, width, key, tm1,
+                                          none, delta, aligned, tokens, values, best, st);
+  else if (width == 1)
+    launch_argmax<T, kSelfSalt, 1>(logits, B, V, row_stride, context, width, key, tm1, none,
+                                   delta, aligned, tokens, values, best, st);
+  else
+    launch_argmax<T, kSelfSalt, kMaxWidth>(logits, B, V, row_stride, context, width, key, tm1,
+                                           none, delta, aligned, tokens, values, best, st);
+}
+
 template <int kSeeding, int kW>
 void launch_detect(int64_t positions, int64_t blocks, hipStream_t st, const int32_t* tokens,
                    int64_t N, int64_t L, int64_t row_stride, int width, uint64_t key, uint32_t tm1,
@@ -507,6 +797,54 @@ sbw_status_t sbw_watermark(void* logits, sbw_dtype_t dtype, int64_t B, int64_t V
                            double gamma, float delta, sbw_seeding_t seeding, void* stream) {
   return sbw_watermark_window(logits, dtype, B, V, row_stride, prev_tokens, 1, key, gamma, delta,
                               seeding, stream);
+}
+
+sbw_status_t sbw_watermark_argmax(const void* logits, sbw_dtype_t dtype, int64_t B, int64_t V,
+                                  int64_t row_stride, const int32_t* context, int64_t width,
+                                  uint64_t key, double gamma, float delta, sbw_seeding_t seeding,
+                                  int32_t* tokens, float* values, uint64_t* workspace,
+                                  void* stream) {
+  if (B < 0 || V < 0 || row_stride < V) return SBW_ERR_INVALID_ARG;
+  sbw_status_t s = check_width(width);
+  if (s != SBW_OK) return s;
+  if (dtype != SBW_F32 && dtype != SBW_BF16) return SBW_ERR_UNSUPPORTED;
+  if (!valid_seeding(seeding)) return SBW_ERR_UNSUPPORTED;
+  if (!(gamma >= 0.0 && gamma <= 1.0)) return SBW_ERR_GAMMA;
+  if (!isfinite(delta)) return SBW_ERR_DELTA;
+  if (V >= (int64_t{1} << 32)) return SBW_ERR_UNSUPPORTED;
+  if (B == 0) return SBW_OK;
+  if (V == 0) return SBW_ERR_INVALID_ARG;  // no token to choose
+  if (logits == nullptr || context == nullptr || tokens == nullptr || workspace == nullptr)
+    return SBW_ERR_INVALID_ARG;
+  if (B > INT64_MAX / 4 / row_stride) return SBW_ERR_UNSUPPORTED;
+  s = check_device();
+  if (s != SBW_OK) return s;
+
+  // gamma == 0: nothing is green, every logit (and the value returned) is unchanged.
+  const uint64_t T = threshold_of(gamma);
+  const int none = T == 0 ? 1 : 0;
+  const uint32_t tm1 = none ? 0u : static_cast<uint32_t>(T - 1);
+  const float d = delta;
+  const size_t esize = dtype == SBW_F32 ? 4 : 2;
+  const bool aligned = (reinterpret_cast<uintptr_t>(logits) % 16 == 0) &&
+                       ((static_cast<uint64_t>(row_stride) * esize) % 16 == 0);
+  const uint32_t v32 = static_cast<uint32_t>(V);
+  const int w = static_cast<int>(width);
+  uint64_t* best = workspace;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if (dtype == SBW_F32)
+    dispatch_argmax<float>(logits, B, v32, row_stride, context, w, key, tm1, none, d, seeding,
+                           aligned, tokens, values, best, st);
+  else
+    dispatch_argmax<uint16_t>(logits, B, v32, row_stride, context, w, key, tm1, none, d, seeding,
+                              aligned, tokens, values, best, st);
+  return after_launch();
+}
+
+int64_t sbw_watermark_argmax_workspace(int64_t B, int64_t V) {
+  if (B <= 0 || V <= 0) return 0;
+  // the element path has the most segments per row (the vector paths fewer)
+  return B * ((V + kArgmaxSegElems - 1) / kArgmaxSegElems);
 }
 
 sbw_status_t sbw_green_mask_window(uint32_t* bits, int64_t B, int64_t V, const int32_t* context,

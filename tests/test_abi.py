@@ -32,13 +32,14 @@ def lib(sbw):
 
 def _declared():
     text = open(HEADER).read()
-    return sorted(set(re.findall(r"^\s*(?:const\s+)?[a-z_0-9]+\s*\*?\s*(sbw_[a-z_]+)\s*\(", text, re.M)))
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?[a-z_0-9]+\s*\*?\s*(sbw_[a-z_0-9]+)\s*\(", text, re.M)))
 
 
 def test_header_declares_the_boundary():
     assert _declared() == ["sbw_detect", "sbw_detect_window", "sbw_green_mask",
                            "sbw_green_mask_window", "sbw_last_hip_error", "sbw_strerror",
-                           "sbw_version", "sbw_watermark", "sbw_watermark_window"]
+                           "sbw_version", "sbw_watermark", "sbw_watermark_argmax",
+                           "sbw_watermark_argmax_workspace", "sbw_watermark_window"]
 
 
 def test_library_exports_every_declared_symbol(sbw, lib):
@@ -235,3 +236,34 @@ def test_python_binding_window_shapes():
         sbw.watermark(torch.zeros(2, 3), torch.zeros(3, 4, dtype=torch.int32), KEY, 0.25, 2.0)
     with pytest.raises(ValueError):
         sbw.watermark(torch.zeros(2, 3), torch.zeros(2, 4, 1, dtype=torch.int32), KEY, 0.25, 2.0)
+
+
+def am(lib, logits=DUMMY, dtype=0, B=2, V=8, stride=8, context=DUMMY, width=1, gamma=0.25,
+       delta=2.0, seeding=0, tokens=DUMMY, values=DUMMY, workspace=DUMMY):
+    return lib.sbw_watermark_argmax(logits, dtype, B, V, stride, context, width, KEY, gamma, delta,
+                                    seeding, tokens, values, workspace, None)
+
+
+def test_argmax_rejects_bad_arguments(lib):
+    assert am(lib, V=0, stride=0) == INVALID       # no token to choose
+    assert am(lib, B=-1) == INVALID
+    assert am(lib, stride=7) == INVALID
+    for name in ("logits", "context", "tokens", "workspace"):
+        assert am(lib, **{name: NULL}) == INVALID, name
+    assert am(lib, width=0) == INVALID
+    assert am(lib, width=9) == UNSUPPORTED
+    assert am(lib, dtype=3) == UNSUPPORTED
+    assert am(lib, gamma=-1.0) == GAMMA
+    assert am(lib, delta=math.inf) == DELTA
+    assert am(lib, B=0) == OK
+    if not _gpu_visible():
+        assert am(lib, values=NULL) == NO_DEVICE   # values may be NULL
+
+
+def test_argmax_workspace_size(lib):
+    assert lib.sbw_watermark_argmax_workspace(0, 10) == 0
+    assert lib.sbw_watermark_argmax_workspace(3, 0) == 0
+    assert lib.sbw_watermark_argmax_workspace(1, 1) == 1
+    assert lib.sbw_watermark_argmax_workspace(256, 152064) == 256 * 75
+    assert lib.sbw_watermark_argmax_workspace(2, 2048) == 2
+    assert lib.sbw_watermark_argmax_workspace(2, 2049) == 4

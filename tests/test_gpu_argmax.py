@@ -1,0 +1,139 @@
+"""GPU parity of the fused watermark + greedy decoding (sbw_watermark_argmax).
+
+Tokens must equal the oracle's exactly and the values bit for bit (NaN as NaN),
+over ragged shapes, both dtypes and seedings, windows, the gamma = 0 and 1
+extremes, ties, NaN rows and signed zeros, unaligned rows, graph replay, and the
+c4 workload at full size.
+"""
+import numpy as np
+import pytest
+
+import oracle
+import workloads
+from test_gpu_parity import KEY, WIDE, env, say, special_logits, _to_device  # noqa: F401
+
+pytestmark = pytest.mark.gpu
+
+
+def run_argmax(env, x, ctx, key, gamma, delta, seeding, offset=0, stride_pad=0, workspace=None):
+    torch, sbw, dev = env
+    B, V = x.shape
+    stride = V + stride_pad
+    base = np.zeros(offset + B * stride + 8, dtype=x.dtype)
+    np.lib.stride_tricks.as_strided(base[offset:], shape=(B, V),
+                                    strides=(stride * x.itemsize, x.itemsize))[...] = x
+    tb = _to_device(torch, dev, base)
+    t = tb[offset:offset + B * stride].view(B, stride)[:, :V]
+    c = torch.from_numpy(np.ascontiguousarray(ctx, dtype=np.int32)).to(dev)
+    tokens, values = sbw.watermark_argmax(t, c, key, gamma, delta, seeding, workspace=workspace)
+    torch.cuda.synchronize()
+    assert np.array_equal(tb.cpu().numpy().view(np.uint8) if x.dtype != np.uint16 else
+                          tb.view(torch.int16).cpu().numpy().view(np.uint8),
+                          base.view(np.uint8)), "logits were modified"
+    return tokens.cpu().numpy(), values.cpu().numpy()
+
+
+def assert_argmax_equal(got, expect, what=""):
+    gt, gv = got
+    et, ev = expect
+    assert np.array_equal(gt, et), f"{what}: tokens differ at rows {np.flatnonzero(gt != et)[:5]}"
+    nan = np.isnan(ev)
+    assert np.array_equal(np.isnan(gv), nan), what
+    assert np.array_equal(gv.view(np.uint32)[~nan], ev.view(np.uint32)[~nan]), what
+
+
+def hard_rows(rng, B, V, dtype):
+    x = special_logits(rng, B, V, "f32")
+    if B >= 4:
+        x[0, :] = 1.5                     # all equal: ties everywhere
+        x[1, 3] = np.nan                  # NaN rows (first NaN wins)
+        x[1, V // 2] = np.nan
+        x[2, :] = -0.0                    # signed zeros
+        x[2, ::3] = 0.0
+        x[3, :] = -np.inf
+    if dtype == "bf16":
+        return workloads.f32_to_bf16_bits(x)
+    return x
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("seeding", ["context", "self_salt"])
+@pytest.mark.parametrize("width", [1, 4])
+@pytest.mark.parametrize("B,V", [(1, 1), (4, 7), (5, 1000), (6, 4097), (4, 40001)])
+def test_argmax_small(env, dtype, seeding, width, B, V):
+    rng = np.random.default_rng(70 + width * 3 + B * 11 + V)
+    x = hard_rows(rng, B, V, dtype)
+    ctx = workloads.context_tokens(B, width, max(V, 2), rng)
+    for gamma, delta in [(0.25, 2.0), (0.5, -1.0), (0.0, 3.0), (1.0, 0.5)]:
+        say(f"argmax {dtype} {seeding} h={width} B={B} V={V} gamma={gamma}")
+        assert_argmax_equal(run_argmax(env, x, ctx, WIDE, gamma, delta, seeding),
+                            oracle.watermark_argmax(x, ctx, WIDE, gamma, delta, seeding),
+                            f"{dtype}/{seeding}/{B}x{V}/{gamma}")
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("seeding", ["context", "self_salt"])
+@pytest.mark.parametrize("offset,stride_pad", [(1, 0), (0, 3), (8, 8)])
+def test_argmax_layouts(env, dtype, seeding, offset, stride_pad):
+    rng = np.random.default_rng(80 + offset + stride_pad)
+    B, V = 5, 9001
+    x = hard_rows(rng, B, V, dtype)
+    prev = rng.integers(0, V, B).astype(np.int32)
+    say(f"argmax layout {dtype} {seeding} offset={offset} pad={stride_pad}")
+    assert_argmax_equal(run_argmax(env, x, prev, KEY, 0.25, 2.0, seeding, offset, stride_pad),
+                        oracle.watermark_argmax(x, prev, KEY, 0.25, 2.0, seeding))
+
+
+def test_argmax_reuses_a_larger_workspace(env):
+    torch, sbw, dev = env
+    need = max(sbw.argmax_workspace_size(40, 3000), sbw.argmax_workspace_size(7, 50000))
+    ws = torch.full((need + 5,), -1, dtype=torch.int64, device=dev)   # contents must not matter
+    rng = np.random.default_rng(90)
+    for B, V in [(40, 3000), (7, 50000), (40, 3000)]:
+        x = rng.standard_normal((B, V)).astype(np.float32)
+        prev = rng.integers(0, V, B).astype(np.int32)
+        say(f"argmax workspace reuse B={B} V={V}")
+        assert_argmax_equal(run_argmax(env, x, prev, KEY, 0.25, 2.0, "self_salt", workspace=ws),
+                            oracle.watermark_argmax(x, prev, KEY, 0.25, 2.0, "self_salt"))
+
+
+def test_argmax_graph_replay(env):
+    torch, sbw, dev = env
+    rng = np.random.default_rng(91)
+    B, V = 16, 50003
+    x = rng.standard_normal((B, V)).astype(np.float32)
+    ctx = workloads.context_tokens(B, 4, V, rng)
+    t = torch.from_numpy(x).to(dev)
+    c = torch.from_numpy(ctx).to(dev)
+    tokens = torch.empty(B, dtype=torch.int32, device=dev)
+    values = torch.empty(B, dtype=torch.float32, device=dev)
+    ws = torch.empty(sbw.argmax_workspace_size(B, V), dtype=torch.int64, device=dev)
+    expect = oracle.watermark_argmax(x, ctx, KEY, 0.25, 2.0, "self_salt")
+    sbw.watermark_argmax(t, c, KEY, 0.25, 2.0, "self_salt", tokens=tokens, values=values,
+                         workspace=ws)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        sbw.watermark_argmax(t, c, KEY, 0.25, 2.0, "self_salt", tokens=tokens, values=values,
+                             workspace=ws)
+    for replay in range(4):
+        tokens.fill_(-7)
+        values.fill_(0.0)
+        ws.fill_(123)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert_argmax_equal((tokens.cpu().numpy(), values.cpu().numpy()), expect, f"replay {replay}")
+
+
+@pytest.mark.parametrize("seeding", ["context", "self_salt"])
+def test_argmax_c4_full_size(env, seeding):
+    c = workloads.C4
+    x, prev = workloads.watermark_inputs("c4")
+    say(f"argmax c4 {seeding}")
+    got = run_argmax(env, x, prev, KEY, c["gamma"], c["delta"], seeding)
+    expect = oracle.watermark_argmax(x, prev, KEY, c["gamma"], c["delta"], seeding)
+    assert_argmax_equal(got, expect, f"c4 {seeding}")
+    # the bias moves the argmax: most rows now pick a green token
+    green = oracle.is_green_many(KEY, prev, expect[0], c["gamma"], seeding)
+    assert green.mean() > 0.5
