@@ -43,17 +43,18 @@ CUS, LANES, CLOCK_GHZ = 256, 64, 2.4   # MI355X compute units, wave width, peak 
 # 20 32x32->64-bit products (v_mad_u64_u32), 20 three-input xors, 18 key-schedule adds.
 PHILOX_LANE_OPS = 58
 PHILOX_PEAK_GBLOCKS = CUS * LANES * CLOCK_GHZ / PHILOX_LANE_OPS
-PROFILE = os.path.join(ROOT, "profiles", "watermark_detect_c4_c5.json")
+PROFILE = os.path.join(ROOT, "profiles", "watermark_detect_c4_c5.json")          # main step
+PROFILE_CONFIGS = os.path.join(ROOT, "profiles", "configs_c1_c4_argmax_paper_table.json")
 KERNEL_SOURCES = ("paper_2609_03844_amd/csrc/sbw_kernels.hip",
                   "paper_2609_03844_amd/csrc/sbw_device.hpp")
 
 
-def measured_traffic():
-    """HBM bytes per launch from the committed FETCH_SIZE / WRITE_SIZE summary, only
+def measured_traffic(path=PROFILE):
+    """HBM bytes per launch from a committed FETCH_SIZE / WRITE_SIZE summary, only
     while the kernel sources are the ones the counters were taken on."""
     import hashlib
     try:
-        prof = json.load(open(PROFILE))
+        prof = json.load(open(path))
     except (OSError, ValueError):
         return {}
     h = hashlib.sha256()
@@ -407,8 +408,12 @@ def main():
     ss_blocks = elems / (mean_ms["wm_self_salt"] * 1e-3) / 1e9   # one Philox block per logit
     traffic = measured_traffic()
 
-    def traffic_of(prefix):
-        hits = [v for k, v in traffic.items() if k.startswith(prefix)]
+    # The profile keys kernels by name and workgroup count; an fp32 watermark launch
+    # covers 2048 logits of one row per workgroup.
+    wm_groups = B * -(-V // 2048)
+
+    def traffic_of(prefix, groups):
+        hits = [v for k, v in traffic.items() if k.startswith(prefix) and k.endswith(f"@{groups}")]
         return hits[0] if len(hits) == 1 else None
 
     out = {
@@ -438,13 +443,13 @@ def main():
         "roofline": {"bound": "alu", "kernel": "watermark_vec_kernel<float, self-salt>",
                      "achieved": ss_blocks, "peak": PHILOX_PEAK_GBLOCKS,
                      "unit": "G Philox4x32-10 blocks/s", "frac": ss_blocks / PHILOX_PEAK_GBLOCKS,
-                     "traffic": traffic_of("sbw::watermark_vec_kernel<float, 1,"),
+                     "traffic": traffic_of("sbw::watermark_vec_kernel<float, 1,", wm_groups),
                      "algorithmic_per_launch": f"{elems} Philox blocks (one per logit), "
                                                f"{bytes_wm} HBM bytes"},
         "roofline_context": {"bound": "hbm", "kernel": "watermark_vec_kernel<float, context>",
                              "achieved": ctx["hbm_gbps"], "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                              "frac": ctx["hbm_frac"],
-                             "traffic": traffic_of("sbw::watermark_vec_kernel<float, 0,"),
+                             "traffic": traffic_of("sbw::watermark_vec_kernel<float, 0,", wm_groups),
                              "algorithmic_per_launch": f"{bytes_wm} bytes"},
         "wall_s_timed": wall,
     }
@@ -452,6 +457,13 @@ def main():
         del bufs
         torch.cuda.empty_cache()
         out["configs"] = other_configs(torch, sbw, dev, args.steps)
+        # The fused argmax pass runs at one shape only, so its name alone keys it.
+        traffic_cfg = measured_traffic(PROFILE_CONFIGS)
+        for seeding, code in (("context", 0), ("self_salt", 1)):
+            hits = [v for k, v in traffic_cfg.items()
+                    if k.startswith(f"sbw::argmax_vec_kernel<float, {code},")]
+            out["configs"]["c4_watermark_argmax"][seeding]["traffic"] = (
+                hits[0] if len(hits) == 1 else None)
         out["paper_table"] = paper_table(torch, sbw, dev)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(x, prev, toks["self_salt"], args.cpu_seconds)

@@ -8,6 +8,10 @@
 //             workgroup in scalar registers.  Context seeding shares one Philox
 //             block between the 4 tokens of a counter; self-salt needs one block
 //             per token.
+// argmax      greedy decoding of the watermarked logits without writing them: one
+//             read of each logit, a per-segment (value, index) partial, a read-out
+//             kernel per row.  Colours are drawn only for logits that can still
+//             reach the segment's maximum.
 // green_mask  one lane per 32-token word of the bit set.
 // detect      one wavefront per sequence; each lane scores positions i, i+64, ...
 //             and the wave counts green positions with a ballot + popcount.
@@ -237,25 +241,21 @@ watermark_elem_kernel(T* __restrict__ logits, int64_t row_stride, uint32_t V, in
 
 // ---------------------------------------------------------------------------
 // Greedy decoding fused with the watermark: the argmax of each watermarked row in
-// one read-only pass.  A row is cut into segments; one workgroup scans a segment
-// (kSegTiles tiles, the next tile's loads in flight while the current one is
-// reduced), keeps a running (value, index) per lane, reduces them and writes one
-// partial (value bits, index) to the workspace.  A read-out kernel then reduces the
+// one read-only pass.  A row is cut into segments; one workgroup scans a segment,
+// keeps a running (value, index) per lane, reduces them and writes one partial
+// (value bits, index) to the workspace.  A read-out kernel then reduces the
 // partials of each row.  Candidates compare through a 64-bit key: the high word
 // orders the values (every NaN above +inf, -0 equal to +0), the low word is
 // ~index, so the maximum key is the largest value at its smallest index.
 // ---------------------------------------------------------------------------
-// Tiles per workgroup segment of the fused argmax: several for the HBM-bound context
-// pass (the next tile's loads overlap the current one's work), one for the
-// Philox-bound self-salt pass (more workgroups, more waves to hide latency).
-#ifndef SBW_ARGMAX_SEG_CONTEXT
-#define SBW_ARGMAX_SEG_CONTEXT 8
+// 16-byte vectors per lane in a workgroup's segment of the fused argmax.  A longer
+// segment gives each wave a larger sample for its skip bound; every lane holds its
+// whole share in registers.
+#ifndef SBW_ARGMAX_VECS_CONTEXT
+#define SBW_ARGMAX_VECS_CONTEXT 8
 #endif
-#ifndef SBW_ARGMAX_SEG_SELF_SALT
-#define SBW_ARGMAX_SEG_SELF_SALT 1
-#endif
-#ifndef SBW_ARGMAX_CONTEXT_UNROLL
-#define SBW_ARGMAX_CONTEXT_UNROLL 2   // 16-byte vectors per lane per tile, context pass
+#ifndef SBW_ARGMAX_VECS_SELF_SALT
+#define SBW_ARGMAX_VECS_SELF_SALT 8
 #endif
 constexpr int kElemSegSteps = 8;                                // element kernel
 constexpr int64_t kArgmaxSegElems = kThreads * kElemSegSteps;   // element-kernel segment
@@ -348,7 +348,98 @@ __device__ __forceinline__ void block_argmax_store(const LaneBest& lb, uint64_t*
   __syncthreads();  // the LDS slots are reused by the next row of this workgroup
 }
 
-template <typename T, int kSeeding, int kU, int kW, int kSegTiles>
+// Skipping elements that cannot win.  An element's watermarked value is either its
+// logit x or bias(x) (the value it takes when green), and bias is non-decreasing in
+// x for both dtypes (one rounded add; bf16 rounding is monotone too).  So if m is
+// the largest logit of some set of elements, one of them ends at least at
+// lb = min(m, bias(m)), and an element with x < lb and bias(x) < lb can be neither
+// the maximum nor tied with it: its colour need not be drawn.  A NaN compares false
+// and is always kept (it wins), so NaN logits never make the test skip anything;
+// delta is finite, so bias(x) is NaN only when x is.
+__device__ __forceinline__ float raw_max(f32x4 o) { return fmaxf(fmaxf(o.x, o.y), fmaxf(o.z, o.w)); }
+__device__ __forceinline__ float raw_max(u32x4 o) {
+  float m = __uint_as_float(o.x << 16);
+  const uint32_t w[4] = {o.x, o.y, o.z, o.w};
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    m = fmaxf(m, __uint_as_float(w[q] << 16));
+    m = fmaxf(m, __uint_as_float(w[q] & 0xFFFF0000u));
+  }
+  return m;
+}
+
+// The lower bound from the largest logit m (-inf when there is none).
+__device__ __forceinline__ float reach_bound(float m, float delta, float) {
+  return fminf(m, m + delta);
+}
+__device__ __forceinline__ float reach_bound(float m, float delta, uint16_t) {
+  const uint32_t b = __float_as_uint(m) >> 16;   // m is a widened bf16
+  return fminf(m, widen(bias_bf16(static_cast<uint16_t>(b), delta, true)));
+}
+
+// Whether some element of the vector may end at or above lb.  fp32: with
+// dplus = max(delta, 0), x + dplus is the larger of x and bias(x) (x itself when
+// delta < 0, where x + 0 only turns -0 into +0, which compares equal).
+__device__ __forceinline__ bool may_reach(f32x4 o, float dplus, float, float lb) {
+  return !(static_cast<bool>(static_cast<int>(o.x + dplus < lb) & static_cast<int>(o.y + dplus < lb) &
+                             static_cast<int>(o.z + dplus < lb) & static_cast<int>(o.w + dplus < lb)));
+}
+__device__ __forceinline__ bool may_reach(u32x4 o, float, float delta, float lb) {
+  const uint32_t w[4] = {o.x, o.y, o.z, o.w};
+  int below = 1;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const uint32_t g = bias_bf16x2(w[q], delta, true, true);
+    below &= static_cast<int>(__uint_as_float(w[q] << 16) < lb) &
+             static_cast<int>(__uint_as_float(w[q] & 0xFFFF0000u) < lb) &
+             static_cast<int>(__uint_as_float(g << 16) < lb) &
+             static_cast<int>(__uint_as_float(g & 0xFFFF0000u) < lb);
+  }
+  return !below;
+}
+
+// Self-salt draws one Philox block per token, so it tests and draws token by token:
+// the elements of a vector as (x, bias(x)) pairs, then only those that may reach lb.
+__device__ __forceinline__ void green_values(f32x4 o, float delta, float (&x)[4], float (&gv)[4]) {
+  x[0] = o.x; x[1] = o.y; x[2] = o.z; x[3] = o.w;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) gv[e] = bias_f32(x[e], delta, true);
+}
+__device__ __forceinline__ void green_values(u32x4 o, float delta, float (&x)[8], float (&gv)[8]) {
+  const uint32_t w[4] = {o.x, o.y, o.z, o.w};
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const uint32_t g = bias_bf16x2(w[q], delta, true, true);
+    x[2 * q] = __uint_as_float(w[q] << 16);
+    x[2 * q + 1] = __uint_as_float(w[q] & 0xFFFF0000u);
+    gv[2 * q] = __uint_as_float(g << 16);
+    gv[2 * q + 1] = __uint_as_float(g & 0xFFFF0000u);
+  }
+}
+
+template <typename VecT, int kW>
+__device__ __forceinline__ void scan_self_salt(LaneBest& b, VecT o, uint32_t j, const RowSeed<kW>& rs,
+                                               uint32_t tm1, int none_green, float delta, float lb) {
+  constexpr int kE = std::is_same<VecT, f32x4>::value ? 4 : 8;
+  float x[kE], gv[kE];
+  green_values(o, delta, x, gv);
+#pragma unroll
+  for (int e = 0; e < kE; ++e) {
+    if (!(static_cast<bool>(static_cast<int>(x[e] < lb) & static_cast<int>(gv[e] < lb)))) {
+      const uint32_t v = j * kE + e;
+      const bool g = !none_green && is_green(draw<kSelfSalt>(rs, v), tm1);
+      consider(b, g ? gv[e] : x[e], v);
+    }
+  }
+}
+
+// Vector path.  A segment is kThreads * kN vectors, vector n of lane t at offset
+// n * kThreads + t; every lane loads all of its kN vectors at once.  Each wave
+// then takes the largest logit of its share, derives lb, and draws colours and
+// updates its running argmax only for the vectors that may reach lb, in increasing
+// index order (self-salt: the elements that may).  The skipped elements cannot be
+// the segment's maximum, so the partial is the same as that of a full scan.
+template <typename T, int kSeeding, int kN, int kW>
 __global__ void __launch_bounds__(kThreads)
 argmax_vec_kernel(const T* __restrict__ logits, int64_t row_stride, uint32_t V, int64_t B,
                   const int32_t* __restrict__ context, int width, uint64_t key, uint32_t tm1,
@@ -356,60 +447,61 @@ argmax_vec_kernel(const T* __restrict__ logits, int64_t row_stride, uint32_t V, 
   using VecT = typename std::conditional<sizeof(T) == 4, f32x4, u32x4>::type;
   __shared__ uint64_t lds_key[kThreads / 64], lds_part[kThreads / 64];
   constexpr uint32_t kPer = 16u / sizeof(T);
-  constexpr uint32_t kTile = kThreads * kU;     // vectors per tile
+  constexpr uint32_t kSegVecs = kThreads * kN;       // vectors per segment
   const uint32_t full = V / kPer;
   const uint32_t tail = V % kPer;
-  const uint32_t seg_first = blockIdx.x * (kTile * kSegTiles);
+  const uint32_t seg_base = blockIdx.x * kSegVecs;
+  const float dplus = delta > 0.0f ? delta : 0.0f;
   for (int64_t row = blockIdx.y; row < B; row += gridDim.y) {
     const T* row_ptr = logits + row * row_stride;
     const VecT* vec = reinterpret_cast<const VecT*>(row_ptr);
-    LaneBest lb = lane_best_init();
-    const RowSeed<kW> rs = row_seed<kSeeding, kW>(key, context + row * width, width);
-    // Whole tiles of this segment, with the next tile's loads issued before the
-    // current tile is reduced.
-    uint32_t whole = 0;
-    if (full > seg_first) whole = min((full - seg_first) / kTile, static_cast<uint32_t>(kSegTiles));
-    VecT cur[kU], nxt[kU];
-    if (whole > 0) {
+    // Opaque to the optimiser: otherwise the first Philox round of every vector,
+    // which depends on the counter only, is hoisted out of the row loop and pins
+    // registers for the whole kernel.
+    uint32_t seg_first = seg_base;
+    asm volatile("" : "+s"(seg_first));
+    VecT buf[kN];
+    float m = -INFINITY;
+    const bool whole = seg_first + kSegVecs <= full;
+    if (whole) {
 #pragma unroll
-      for (int u = 0; u < kU; ++u) cur[u] = stream_load(vec + seg_first + u * kThreads + threadIdx.x);
-    }
-    for (uint32_t t = 0; t < whole; ++t) {
-      const uint32_t first = seg_first + t * kTile;
-      if (t + 1 < whole) {
+      for (int n = 0; n < kN; ++n) buf[n] = stream_load(vec + seg_first + n * kThreads + threadIdx.x);
 #pragma unroll
-        for (int u = 0; u < kU; ++u) nxt[u] = stream_load(vec + first + kTile + u * kThreads + threadIdx.x);
-      }
+      for (int n = 0; n < kN; ++n) m = fmaxf(m, raw_max(buf[n]));
+    } else {
 #pragma unroll
-      for (int u = 0; u < kU; ++u) {
-        const uint32_t j = first + u * kThreads + threadIdx.x;
-        consider_vec(lb, none_green ? cur[u] : bias_vec<kSeeding>(cur[u], j, rs, tm1, delta), j);
-      }
-#pragma unroll
-      for (int u = 0; u < kU; ++u) cur[u] = nxt[u];
-    }
-    // The part of the segment past its whole tiles: guarded vectors, then the row's
-    // partial last vector (lane 0 of the segment that holds it).
-    if (whole < kSegTiles) {
-      const uint32_t first = seg_first + whole * kTile;
-#pragma unroll
-      for (int u = 0; u < kU; ++u) {
-        const uint32_t j = first + u * kThreads + threadIdx.x;
+      for (int n = 0; n < kN; ++n) {
+        const uint32_t j = seg_first + n * kThreads + threadIdx.x;
         if (j < full) {
-          const VecT x = stream_load(vec + j);
-          consider_vec(lb, none_green ? x : bias_vec<kSeeding>(x, j, rs, tm1, delta), j);
-        }
-      }
-      if (tail != 0u && threadIdx.x == 0 && full >= seg_first &&
-          full - seg_first < kTile * kSegTiles) {
-        for (uint32_t e = 0; e < tail; ++e) {
-          const uint32_t v = full * kPer + e;
-          const bool g = !none_green && is_green(draw<kSeeding>(rs, v), tm1);
-          consider(lb, widen(bias_elem(row_ptr[v], delta, g)), v);
+          buf[n] = stream_load(vec + j);
+          m = fmaxf(m, raw_max(buf[n]));
         }
       }
     }
-    block_argmax_store(lb, partials + row * segments + blockIdx.x, lds_key, lds_part);
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) m = fmaxf(m, __shfl_xor(m, off, 64));
+    const float lb = reach_bound(m, delta, T{});
+    const RowSeed<kW> rs = row_seed<kSeeding, kW>(key, context + row * width, width);
+    LaneBest lb_lane = lane_best_init();
+#pragma unroll
+    for (int n = 0; n < kN; ++n) {
+      const uint32_t j = seg_first + n * kThreads + threadIdx.x;
+      if (!(whole || j < full)) continue;
+      if (kSeeding == kSelfSalt)
+        scan_self_salt(lb_lane, buf[n], j, rs, tm1, none_green, delta, lb);
+      else if (may_reach(buf[n], dplus, delta, lb))
+        consider_vec(lb_lane, none_green ? buf[n] : bias_vec<kSeeding>(buf[n], j, rs, tm1, delta), j);
+    }
+    // The row's partial last vector, element by element, by lane 0 of the segment
+    // that holds it (never skipped).
+    if (!whole && tail != 0u && threadIdx.x == 0 && full >= seg_first && full - seg_first < kSegVecs) {
+      for (uint32_t e = 0; e < tail; ++e) {
+        const uint32_t v = full * kPer + e;
+        const bool g = !none_green && is_green(draw<kSeeding>(rs, v), tm1);
+        consider(lb_lane, widen(bias_elem(row_ptr[v], delta, g)), v);
+      }
+    }
+    block_argmax_store(lb_lane, partials + row * segments + blockIdx.x, lds_key, lds_part);
   }
 }
 
@@ -672,19 +764,14 @@ void dispatch_watermark(void* logits, int64_t B, uint32_t V, int64_t row_stride,
 
 // Segments per row of the fused argmax: vector path and element path.
 template <int kSeeding>
-constexpr int argmax_unroll_for() {
-  return kSeeding == kContext ? SBW_ARGMAX_CONTEXT_UNROLL : SBW_SELF_SALT_UNROLL;
-}
-template <int kSeeding>
-constexpr int seg_tiles_for() {
-  return kSeeding == kContext ? SBW_ARGMAX_SEG_CONTEXT : SBW_ARGMAX_SEG_SELF_SALT;
+constexpr int argmax_vecs_for() {
+  return kSeeding == kContext ? SBW_ARGMAX_VECS_CONTEXT : SBW_ARGMAX_VECS_SELF_SALT;
 }
 template <typename T>
-constexpr uint64_t vec_segment_elems(int kU, int kSeg) { return (16u / sizeof(T)) * kThreads * kU * kSeg; }
+constexpr uint64_t vec_segment_elems(int kN) { return (16u / sizeof(T)) * kThreads * kN; }
 // The workspace is sized for the element path; vector segments must be at least as long.
-static_assert(vec_segment_elems<float>(SBW_ARGMAX_CONTEXT_UNROLL, SBW_ARGMAX_SEG_CONTEXT) >= kArgmaxSegElems &&
-                  vec_segment_elems<float>(SBW_SELF_SALT_UNROLL, SBW_ARGMAX_SEG_SELF_SALT) >=
-                      kArgmaxSegElems,
+static_assert(vec_segment_elems<float>(SBW_ARGMAX_VECS_CONTEXT) >= kArgmaxSegElems &&
+                  vec_segment_elems<float>(SBW_ARGMAX_VECS_SELF_SALT) >= kArgmaxSegElems,
               "vector segments must not outnumber element segments");
 
 template <typename T, int kSeeding, int kW>
@@ -696,11 +783,10 @@ void launch_argmax(const void* logits, int64_t B, uint32_t V, int64_t row_stride
   const uint32_t rows = static_cast<uint32_t>(B < kMaxGridY ? B : kMaxGridY);
   uint32_t segments;
   if (aligned) {
-    constexpr int kU = argmax_unroll_for<kSeeding>();
-    constexpr int kSeg = seg_tiles_for<kSeeding>();
-    const uint64_t seg = vec_segment_elems<T>(kU, kSeg);
+    constexpr int kN = argmax_vecs_for<kSeeding>();
+    const uint64_t seg = vec_segment_elems<T>(kN);
     segments = static_cast<uint32_t>((static_cast<uint64_t>(V) + seg - 1) / seg);
-    hipLaunchKernelGGL((argmax_vec_kernel<T, kSeeding, kU, kW, kSeg>), dim3(segments, rows),
+    hipLaunchKernelGGL((argmax_vec_kernel<T, kSeeding, kN, kW>), dim3(segments, rows),
                        dim3(kThreads), 0, stream, p, row_stride, V, B, context, width, key, tm1,
                        none, delta, segments, partials);
   } else {

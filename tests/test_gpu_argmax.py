@@ -137,3 +137,39 @@ def test_argmax_c4_full_size(env, seeding):
     # the bias moves the argmax: most rows now pick a green token
     green = oracle.is_green_many(KEY, prev, expect[0], c["gamma"], seeding)
     assert green.mean() > 0.5
+
+
+def bound_rows(rng, V, dtype):
+    """Rows aimed at the pass's skip test, which leaves out elements whose logit and
+    whose green value both lie below the largest logit m of a wave's share (or below
+    m + delta when delta < 0): elements whose green value lands exactly on m, earlier
+    and later than m; NaN and +inf after a spike; a single finite value among -inf;
+    a row of equal values; a bf16 row where x + delta rounds (to even) onto m."""
+    rows = []
+    base = (0.05 * rng.standard_normal(V)).astype(np.float32)
+    r = base.copy(); r[V - 5] = 4.0; r[7:V:977] = 2.0; rows.append(r)          # 2 + 2 == 4
+    r = base.copy(); r[3] = 4.0; r[100:V:613] = 2.0; rows.append(r)           # m first
+    r = base.copy(); r[V // 3] = 5.0; r[11:V:501] = 4.0; rows.append(r)       # delta < 0: 5 - 1 == 4
+    r = base.copy(); r[50] = 9.0; r[V - 2] = np.nan; rows.append(r)           # NaN after a spike
+    r = base.copy(); r[50] = 9.0; r[V // 2] = np.inf; rows.append(r)
+    r = np.full(V, -np.inf, dtype=np.float32); r[V - 9] = -3.0; rows.append(r)
+    rows.append(np.full(V, 2.0, dtype=np.float32))
+    r = base.copy(); r[V - 100] = 256.0; r[13:V:389] = 254.0; rows.append(r)  # bf16: 254 + 1.5 -> 256
+    x = np.stack(rows)
+    return workloads.f32_to_bf16_bits(x) if dtype == "bf16" else x
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("seeding", ["context", "self_salt"])
+def test_argmax_skip_bound_edges(env, dtype, seeding):
+    rng = np.random.default_rng(92)
+    V = 40001
+    x = bound_rows(rng, V, dtype)
+    B = x.shape[0]
+    ctx = workloads.context_tokens(B, 1, V, rng)[:, 0].copy()
+    for gamma, delta in [(0.25, 2.0), (0.5, 2.0), (1.0, 2.0), (0.5, -1.0), (1.0, -1.0),
+                         (0.5, 1.5), (1.0, 1.5), (0.0, 2.0)]:
+        say(f"argmax bound edges {dtype} {seeding} gamma={gamma} delta={delta}")
+        assert_argmax_equal(run_argmax(env, x, ctx, WIDE, gamma, delta, seeding),
+                            oracle.watermark_argmax(x, ctx, WIDE, gamma, delta, seeding),
+                            f"{dtype}/{seeding}/{gamma}/{delta}")
