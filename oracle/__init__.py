@@ -83,6 +83,8 @@ def _declare(l: ctypes.CDLL) -> ctypes.CDLL:
         "oracle_is_green_w_many": (None, [u64, P, i64, P, i64, f64, i32, P]),
         "oracle_watermark_argmax_f32_w": (None, [P, i64, i64, i64, P, i64, u64, f64, f32, i32, P, P]),
         "oracle_watermark_argmax_bf16_w": (None, [P, i64, i64, i64, P, i64, u64, f64, f32, i32, P, P]),
+        "oracle_watermark_candidates_f32_w": (None, [P, i64, i64, i64, P, i64, P, i64, u64, f64, f32, i32]),
+        "oracle_watermark_candidates_bf16_w": (None, [P, i64, i64, i64, P, i64, P, i64, u64, f64, f32, i32]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(l, name)
@@ -315,3 +317,24 @@ def watermark_argmax(logits: np.ndarray, context, key: int, gamma: float, delta:
     fn(_ptr(x), B, V, V, _ptr(c), c.shape[1], key, float(gamma), float(delta), _seeding(seeding),
        _ptr(tokens), _ptr(values))
     return tokens, values
+
+
+def watermark_candidates(logits: np.ndarray, candidates, context, key: int, gamma: float,
+                         delta: float, seeding="self_salt") -> np.ndarray:
+    """Watermark restricted to candidate ids [B, k] (SBW-ss: top-k candidates, the rest
+    of the row unbiased).  Ids outside [0, V) are ignored; a repeated id is biased once."""
+    out = np.array(logits, copy=True, order="C")
+    B, V = out.shape
+    cand = np.ascontiguousarray(candidates, dtype=np.int32)
+    if cand.ndim != 2 or cand.shape[0] != B:
+        raise ValueError("candidates must be [B, k]")
+    c = _context(context, B)
+    if out.dtype == np.float32:
+        fn = lib().oracle_watermark_candidates_f32_w
+    elif out.dtype == np.uint16:
+        fn = lib().oracle_watermark_candidates_bf16_w
+    else:
+        raise TypeError("logits must be float32 or uint16 (bf16 bits)")
+    fn(_ptr(out), B, V, V, _ptr(cand), cand.shape[1], _ptr(c), c.shape[1], key, float(gamma),
+       float(delta), _seeding(seeding))
+    return out

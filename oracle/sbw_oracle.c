@@ -475,3 +475,54 @@ void oracle_watermark_argmax_bf16_w(const uint16_t *logits, int64_t B, int64_t V
         values[b] = best;
     }
 }
+
+/* ------------------------------------------------------------------------- */
+/* Watermark restricted to candidate tokens: SBW-ss of the scheme table       */
+/* (Sec. 4), the width-4 self-salt watermark applied to the top-40 candidates */
+/* of a step only, the rest of the vocabulary left unbiased.  Row b's         */
+/* candidates are cand[b*k .. b*k+k-1] (any order).  A candidate id outside   */
+/* [0, V) is ignored and a repeated id is biased once; every other logit      */
+/* keeps its bits.                                                            */
+/* ------------------------------------------------------------------------- */
+
+static int first_valid_candidate(const int32_t *row_cand, int64_t j, int64_t V)
+{
+    if (row_cand[j] < 0 || (int64_t)row_cand[j] >= V) return 0;
+    for (int64_t i = 0; i < j; ++i)
+        if (row_cand[i] == row_cand[j]) return 0;
+    return 1;
+}
+
+void oracle_watermark_candidates_f32_w(float *logits, int64_t B, int64_t V, int64_t row_stride,
+                                       const int32_t *cand, int64_t k, const int32_t *context,
+                                       int64_t width, uint64_t key, double gamma, float delta,
+                                       int seeding)
+{
+    uint64_t threshold = oracle_threshold(gamma);
+    for (int64_t b = 0; b < B; ++b)
+        for (int64_t j = 0; j < k; ++j) {
+            if (!first_valid_candidate(cand + b * k, j, V)) continue;
+            uint32_t v = (uint32_t)cand[b * k + j];
+            if (oracle_is_green_w(key, context + b * width, width, v, threshold, seeding)) {
+                float *l = &logits[b * row_stride + v];
+                *l = oracle_bias_f32(*l, delta);
+            }
+        }
+}
+
+void oracle_watermark_candidates_bf16_w(uint16_t *logits, int64_t B, int64_t V, int64_t row_stride,
+                                        const int32_t *cand, int64_t k, const int32_t *context,
+                                        int64_t width, uint64_t key, double gamma, float delta,
+                                        int seeding)
+{
+    uint64_t threshold = oracle_threshold(gamma);
+    for (int64_t b = 0; b < B; ++b)
+        for (int64_t j = 0; j < k; ++j) {
+            if (!first_valid_candidate(cand + b * k, j, V)) continue;
+            uint32_t v = (uint32_t)cand[b * k + j];
+            if (oracle_is_green_w(key, context + b * width, width, v, threshold, seeding)) {
+                uint16_t *l = &logits[b * row_stride + v];
+                *l = oracle_bias_bf16(*l, delta);
+            }
+        }
+}
