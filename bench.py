@@ -217,6 +217,22 @@ def other_configs(torch, sbw, dev, steps):
     res["c4_watermark_argmax"] = fused
     del bufs
 
+    # SBW-ss on the c4 batch: the self-salt watermark (width 4) on the top-40 ids only
+    c = workloads.C4
+    x, _ = workloads.watermark_inputs("c4")
+    rng = workloads.rng_for("c4", salt=7)
+    win = torch.from_numpy(workloads.context_tokens(c["B"], 4, c["V"], rng)).to(dev)
+    topk = {}
+    for dt in ("f32", "bf16"):
+        xb = x if dt == "f32" else workloads.f32_to_bf16_bits(x)
+        bufs = rotating(xb)
+        cand = torch.topk(bufs[0].float(), 40, dim=1).indices.to(torch.int32).contiguous()
+        us = _mean_us(torch, lambda i: sbw.watermark_candidates(
+            bufs[i % len(bufs)], win, cand, key, c["gamma"], c["delta"], "self_salt"), steps)
+        topk[dt] = {"us": us, "candidates_per_s": c["B"] * 40 / us * 1e6}
+        del bufs
+    res["c4_sbw_ss_top40"] = topk
+
     # c4 at B=1024 (623 MB per buffer), both seedings
     c = workloads.C4
     x, prev = workloads.watermark_inputs("c4", B=c["B_large"])

@@ -167,6 +167,30 @@ sbw_status_t sbw_detect_window(const int32_t *tokens, int64_t N, int64_t L, int6
                                int32_t *green_counts, double *z, void *stream);
 
 /*
+ * sbw_watermark_candidates -- the watermark restricted to given candidate tokens:
+ * SBW-ss of the paper's scheme table (Sec. 4; self-salt, width 4, top-40
+ * candidates), where only the top-k candidates of a step are tested and biased and
+ * the rest of the vocabulary keeps its logits.  The caller's sampler supplies the
+ * candidates (for example its top-k); membership and bias are as for
+ * sbw_watermark_window with the same window, so a candidate is biased exactly when
+ * the full-vocabulary watermark would bias it.
+ *
+ *   logits, dtype, B, V, row_stride, context, width, key, gamma, delta, seeding
+ *                as for sbw_watermark_window (logits mutated in place).
+ *   candidates   device, [B, k] int32 row-major: row b's candidate token ids, in any
+ *                order.  An id outside [0, V) is ignored; an id repeated within a
+ *                row is biased once.
+ *   k            candidates per row, 0 <= k <= 1024 (k > 1024: SBW_ERR_UNSUPPORTED;
+ *                k < 0: SBW_ERR_INVALID_ARG; k == 0: no-op).
+ * One kernel on `stream` (one workgroup per row); nothing is allocated.
+ */
+sbw_status_t sbw_watermark_candidates(void *logits, sbw_dtype_t dtype, int64_t B, int64_t V,
+                                      int64_t row_stride, const int32_t *candidates, int64_t k,
+                                      const int32_t *context, int64_t width, uint64_t key,
+                                      double gamma, float delta, sbw_seeding_t seeding,
+                                      void *stream);
+
+/*
  * sbw_watermark_argmax -- greedy decoding fused with the watermark: for every row,
  * the index of the largest watermarked logit (Eq. 2 applied on the fly; the logits
  * are only read, never written).  One read of each logit instead of a read and a

@@ -42,7 +42,9 @@ _STATUS = {
 
 EXPORTED = ("sbw_watermark", "sbw_green_mask", "sbw_detect", "sbw_watermark_window",
             "sbw_green_mask_window", "sbw_detect_window", "sbw_watermark_argmax",
-            "sbw_watermark_argmax_workspace", "sbw_strerror", "sbw_last_hip_error", "sbw_version")
+            "sbw_watermark_argmax_workspace", "sbw_watermark_candidates", "sbw_strerror",
+            "sbw_last_hip_error", "sbw_version")
+MAX_CANDIDATES = 1024
 MAX_WIDTH = 8
 
 
@@ -79,6 +81,9 @@ def _load() -> ctypes.CDLL:
     lib.sbw_watermark_argmax.restype = i32
     lib.sbw_watermark_argmax.argtypes = [P, i32, i64, i64, i64, P, i64, u64, f64, f32, i32, P, P,
                                          P, P]
+    lib.sbw_watermark_candidates.restype = i32
+    lib.sbw_watermark_candidates.argtypes = [P, i32, i64, i64, i64, P, i64, P, i64, u64, f64, f32,
+                                             i32, P]
     lib.sbw_watermark_argmax_workspace.restype = i64
     lib.sbw_watermark_argmax_workspace.argtypes = [i64, i64]
     lib.sbw_strerror.restype = ctypes.c_char_p
@@ -169,6 +174,35 @@ def watermark(logits: torch.Tensor, prev_tokens: torch.Tensor, key: int, gamma: 
     _check(_lib.sbw_watermark_window(logits.data_ptr(), dtype, B, V, row_stride,
                                      context.data_ptr(), width, _key(key), float(gamma),
                                      float(delta), _seeding(seeding), _stream(stream)))
+    return logits
+
+
+def watermark_candidates(logits: torch.Tensor, prev_tokens: torch.Tensor,
+                         candidates: torch.Tensor, key: int, gamma: float, delta: float,
+                         seeding="self_salt", stream=None) -> torch.Tensor:
+    """The watermark restricted to candidates [B, k] int32 (k <= 1024), in place; the
+    top-k self-salt scheme (SBW-ss) with its top-k ids as candidates.  Ids outside
+    [0, V) are ignored, a repeated id is biased once; returns ``logits``."""
+    if logits.dim() != 2:
+        raise ValueError("logits must be [B, V]")
+    if logits.dtype == torch.float32:
+        dtype = F32
+    elif logits.dtype == torch.bfloat16:
+        dtype = BF16
+    else:
+        raise TypeError("logits must be float32 or bfloat16")
+    B, V = logits.shape
+    if B > 0 and V > 0 and logits.stride(1) != 1:
+        raise ValueError("logits must have unit stride along the vocabulary")
+    if (candidates.dim() != 2 or candidates.shape[0] != B or candidates.dtype != torch.int32
+            or not candidates.is_contiguous()):
+        raise ValueError("candidates must be contiguous int32 [B, k]")
+    context, width = _window(prev_tokens, B)
+    row_stride = logits.stride(0) if B > 1 else max(V, logits.stride(0))
+    _check(_lib.sbw_watermark_candidates(logits.data_ptr(), dtype, B, V, row_stride,
+                                         candidates.data_ptr(), candidates.shape[1],
+                                         context.data_ptr(), width, _key(key), float(gamma),
+                                         float(delta), _seeding(seeding), _stream(stream)))
     return logits
 
 

@@ -12,6 +12,8 @@
 //             read of each logit, a per-segment (value, index) partial, a read-out
 //             kernel per row.  Colours are drawn only for logits that can still
 //             reach the segment's maximum.
+// candidates  the watermark restricted to caller-given candidate ids per row (the
+//             top-k self-salt scheme): one workgroup per row.
 // green_mask  one lane per 32-token word of the bit set.
 // detect      one wavefront per sequence; each lane scores positions i, i+64, ...
 //             and the wave counts green positions with a ballot + popcount.
@@ -557,6 +559,45 @@ argmax_finish_kernel(const uint64_t* __restrict__ partials, uint32_t segments, i
 }
 
 // ---------------------------------------------------------------------------
+// Candidate-restricted watermark (top-k self-salt).  One workgroup per row; lane t
+// takes candidates t, t + kThreads, ...  A candidate's logit load is issued as soon
+// as its id arrives, and the row's window loads, the repeat test and the colour
+// draw overlap it.  An id outside [0, V), or equal to an earlier id of the row, is
+// skipped, so every logit is written by at most one lane.
+// ---------------------------------------------------------------------------
+constexpr int kMaxCandidates = 1024;
+
+template <typename T, int kSeeding, int kW>
+__global__ void __launch_bounds__(kThreads)
+candidates_kernel(T* __restrict__ logits, int64_t row_stride, uint32_t V, int64_t B,
+                  const int32_t* __restrict__ cand, int k, const int32_t* __restrict__ context,
+                  int width, uint64_t key, uint32_t tm1, float delta) {
+  __shared__ int32_t ids[kMaxCandidates];
+  for (int64_t row = blockIdx.x; row < B; row += gridDim.x) {
+    const int32_t* row_cand = cand + row * k;
+    T* row_ptr = logits + row * row_stride;
+    for (int j = threadIdx.x; j < k; j += kThreads) ids[j] = row_cand[j];
+    const RowSeed<kW> rs = row_seed<kSeeding, kW>(key, context + row * width, width);
+    __syncthreads();
+    for (int base = 0; base < k; base += kThreads) {
+      const int j = base + static_cast<int>(threadIdx.x);
+      const int32_t id = j < k ? ids[j] : -1;
+      const bool in_range = id >= 0 && static_cast<uint32_t>(id) < V;
+      T l{};
+      if (in_range) l = row_ptr[id];
+      // repeat test: a loop of uniform length over broadcast LDS reads
+      const int upto = min(k, base + kThreads) - 1;
+      int repeat = 0;
+#pragma unroll 8
+      for (int i = 0; i < upto; ++i) repeat |= static_cast<int>(ids[i] == id) & static_cast<int>(i < j);
+      if (in_range && !repeat && is_green(draw<kSeeding>(rs, static_cast<uint32_t>(id)), tm1))
+        row_ptr[id] = bias_elem(l, delta, true);
+    }
+    __syncthreads();  // ids is refilled for the next row of this workgroup
+  }
+}
+
+// ---------------------------------------------------------------------------
 // Green mask: one lane per 32-bit word (tokens 32w .. 32w+31).
 // ---------------------------------------------------------------------------
 template <int kSeeding, int kW>
@@ -762,6 +803,24 @@ void dispatch_watermark(void* logits, int64_t B, uint32_t V, int64_t row_stride,
                                               delta, aligned, st);
 }
 
+template <typename T>
+void dispatch_candidates(void* logits, int64_t B, uint32_t V, int64_t row_stride,
+                         const int32_t* cand, int k, const int32_t* context, int width,
+                         uint64_t key, uint32_t tm1, float delta, sbw_seeding_t seeding,
+                         hipStream_t st) {
+  T* p = static_cast<T*>(logits);
+  const dim3 grid(static_cast<uint32_t>(grid_for(B)));
+  if (seeding == SBW_SEED_CONTEXT)
+    hipLaunchKernelGGL((candidates_kernel<T, kContext, kMaxWidth>), grid, dim3(kThreads), 0, st, p,
+                       row_stride, V, B, cand, k, context, width, key, tm1, delta);
+  else if (width == 1)
+    hipLaunchKernelGGL((candidates_kernel<T, kSelfSalt, 1>), grid, dim3(kThreads), 0, st, p,
+                       row_stride, V, B, cand, k, context, width, key, tm1, delta);
+  else
+    hipLaunchKernelGGL((candidates_kernel<T, kSelfSalt, kMaxWidth>), grid, dim3(kThreads), 0, st,
+                       p, row_stride, V, B, cand, k, context, width, key, tm1, delta);
+}
+
 // Segments per row of the fused argmax: vector path and element path.
 template <int kSeeding>
 constexpr int argmax_vecs_for() {
@@ -883,6 +942,41 @@ sbw_status_t sbw_watermark(void* logits, sbw_dtype_t dtype, int64_t B, int64_t V
                            double gamma, float delta, sbw_seeding_t seeding, void* stream) {
   return sbw_watermark_window(logits, dtype, B, V, row_stride, prev_tokens, 1, key, gamma, delta,
                               seeding, stream);
+}
+
+sbw_status_t sbw_watermark_candidates(void* logits, sbw_dtype_t dtype, int64_t B, int64_t V,
+                                      int64_t row_stride, const int32_t* candidates, int64_t k,
+                                      const int32_t* context, int64_t width, uint64_t key,
+                                      double gamma, float delta, sbw_seeding_t seeding,
+                                      void* stream) {
+  if (B < 0 || V < 0 || row_stride < V || k < 0) return SBW_ERR_INVALID_ARG;
+  sbw_status_t s = check_width(width);
+  if (s != SBW_OK) return s;
+  if (dtype != SBW_F32 && dtype != SBW_BF16) return SBW_ERR_UNSUPPORTED;
+  if (!valid_seeding(seeding)) return SBW_ERR_UNSUPPORTED;
+  if (!(gamma >= 0.0 && gamma <= 1.0)) return SBW_ERR_GAMMA;
+  if (!isfinite(delta)) return SBW_ERR_DELTA;
+  if (V >= (int64_t{1} << 32) || k > kMaxCandidates) return SBW_ERR_UNSUPPORTED;
+  if (B == 0 || V == 0 || k == 0) return SBW_OK;
+  if (logits == nullptr || candidates == nullptr || context == nullptr) return SBW_ERR_INVALID_ARG;
+  if (B > INT64_MAX / 4 / row_stride) return SBW_ERR_UNSUPPORTED;
+  const uint64_t T = threshold_of(gamma);
+  if (T == 0) return SBW_OK;  // nothing is green
+  s = check_device();
+  if (s != SBW_OK) return s;
+
+  const uint32_t tm1 = static_cast<uint32_t>(T - 1);
+  const uint32_t v32 = static_cast<uint32_t>(V);
+  const int w = static_cast<int>(width);
+  const int kk = static_cast<int>(k);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if (dtype == SBW_F32)
+    dispatch_candidates<float>(logits, B, v32, row_stride, candidates, kk, context, w, key, tm1,
+                               delta, seeding, st);
+  else
+    dispatch_candidates<uint16_t>(logits, B, v32, row_stride, candidates, kk, context, w, key,
+                                  tm1, delta, seeding, st);
+  return after_launch();
 }
 
 sbw_status_t sbw_watermark_argmax(const void* logits, sbw_dtype_t dtype, int64_t B, int64_t V,
@@ -1036,6 +1130,6 @@ const char* sbw_strerror(sbw_status_t status) {
 
 const char* sbw_last_hip_error(void) { return hipGetErrorName(g_last_hip_error); }
 
-const char* sbw_version(void) { return "0.2.0"; }
+const char* sbw_version(void) { return "0.3.0"; }
 
 }  // extern "C"

@@ -39,7 +39,8 @@ def test_header_declares_the_boundary():
     assert _declared() == ["sbw_detect", "sbw_detect_window", "sbw_green_mask",
                            "sbw_green_mask_window", "sbw_last_hip_error", "sbw_strerror",
                            "sbw_version", "sbw_watermark", "sbw_watermark_argmax",
-                           "sbw_watermark_argmax_workspace", "sbw_watermark_window"]
+                           "sbw_watermark_argmax_workspace", "sbw_watermark_candidates",
+                           "sbw_watermark_window"]
 
 
 def test_library_exports_every_declared_symbol(sbw, lib):
@@ -267,3 +268,30 @@ def test_argmax_workspace_size(lib):
     assert lib.sbw_watermark_argmax_workspace(256, 152064) == 256 * 75
     assert lib.sbw_watermark_argmax_workspace(2, 2048) == 2
     assert lib.sbw_watermark_argmax_workspace(2, 2049) == 4
+
+
+def wc(lib, logits=DUMMY, dtype=0, B=2, V=8, stride=8, cand=DUMMY, k=3, context=DUMMY, width=4,
+       gamma=0.25, delta=2.0, seeding=1):
+    return lib.sbw_watermark_candidates(logits, dtype, B, V, stride, cand, k, context, width, KEY,
+                                        gamma, delta, seeding, None)
+
+
+def test_candidates_rejects_bad_arguments(lib):
+    assert wc(lib, k=-1) == INVALID
+    assert wc(lib, B=-1) == INVALID
+    assert wc(lib, stride=7) == INVALID
+    for name in ("logits", "cand", "context"):
+        assert wc(lib, **{name: NULL}) == INVALID, name
+    assert wc(lib, k=1025) == UNSUPPORTED
+    assert wc(lib, width=9) == UNSUPPORTED
+    assert wc(lib, dtype=2) == UNSUPPORTED
+    assert wc(lib, seeding=5) == UNSUPPORTED
+    assert wc(lib, gamma=1.5) == GAMMA
+    assert wc(lib, delta=math.nan) == DELTA
+    # no-ops succeed without a device: nothing to do
+    assert wc(lib, k=0, cand=NULL) == OK
+    assert wc(lib, B=0) == OK
+    assert wc(lib, gamma=0.0) == OK
+    if not _gpu_visible():
+        assert wc(lib) == NO_DEVICE
+        assert wc(lib, k=1024) == NO_DEVICE
