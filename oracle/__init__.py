@@ -84,6 +84,7 @@ def _declare(l: ctypes.CDLL) -> ctypes.CDLL:
         "oracle_watermark_argmax_f32_w": (None, [P, i64, i64, i64, P, i64, u64, f64, f32, i32, P, P]),
         "oracle_watermark_argmax_bf16_w": (None, [P, i64, i64, i64, P, i64, u64, f64, f32, i32, P, P]),
         "oracle_watermark_candidates_f32_w": (None, [P, i64, i64, i64, P, i64, P, i64, u64, f64, f32, i32]),
+        "oracle_detect_ex": (None, [P, i64, i64, i64, P, i64, u64, f64, i32, i32, P, P, P]),
         "oracle_watermark_candidates_bf16_w": (None, [P, i64, i64, i64, P, i64, P, i64, u64, f64, f32, i32]),
     }
     for name, (res, args) in sig.items():
@@ -338,3 +339,22 @@ def watermark_candidates(logits: np.ndarray, candidates, context, key: int, gamm
     fn(_ptr(out), B, V, V, _ptr(cand), cand.shape[1], _ptr(c), c.shape[1], key, float(gamma),
        float(delta), _seeding(seeding))
     return out
+
+
+def detect_ex(tokens: np.ndarray, width: int, key: int, gamma: float, seeding="context",
+              lengths=None, ignore_repeated: bool = False):
+    """Detection with per-sequence lengths (clamped to [0, L]; None = all L) and,
+    optionally, each distinct (width+1)-gram scored once.  Returns (green counts,
+    scored positions T, z)."""
+    tok = np.ascontiguousarray(tokens, dtype=np.int32)
+    N, L = tok.shape
+    lens = None if lengths is None else np.ascontiguousarray(lengths, dtype=np.int32)
+    if lens is not None and lens.shape != (N,):
+        raise ValueError("lengths must be [N]")
+    counts = np.empty(N, dtype=np.int32)
+    scored = np.empty(N, dtype=np.int32)
+    z = np.empty(N, dtype=np.float64)
+    lib().oracle_detect_ex(_ptr(tok), N, L, L, None if lens is None else _ptr(lens), int(width),
+                           key, float(gamma), _seeding(seeding), int(bool(ignore_repeated)),
+                           _ptr(counts), _ptr(scored), _ptr(z))
+    return counts, scored, z

@@ -526,3 +526,52 @@ void oracle_watermark_candidates_bf16_w(uint16_t *logits, int64_t B, int64_t V, 
             }
         }
 }
+
+/* ------------------------------------------------------------------------- */
+/* Detection with per-sequence lengths and, optionally, each distinct n-gram  */
+/* scored once.  Sequence n holds len_n = lengths[n] tokens (clamped to       */
+/* [0, L]; all L when lengths is NULL) and positions width..len_n-1 are        */
+/* scored under the width tokens before each, as in oracle_detect_w.  With    */
+/* ignore_repeated, a position whose (width+1)-gram (its window and itself)   */
+/* already occurred at an earlier scored position of the sequence is left     */
+/* out of both T and the green count; a repeat has the same colour, so only   */
+/* the number of trials changes.  z as in Sec. 3 with that T.                 */
+/* ------------------------------------------------------------------------- */
+
+static int same_ngram(const int32_t *seq, int64_t a, int64_t b, int64_t width)
+{
+    for (int64_t k = 0; k <= width; ++k)
+        if (seq[a - width + k] != seq[b - width + k]) return 0;
+    return 1;
+}
+
+void oracle_detect_ex(const int32_t *tokens, int64_t N, int64_t L, int64_t row_stride,
+                      const int32_t *lengths, int64_t width, uint64_t key, double gamma,
+                      int seeding, int ignore_repeated, int32_t *green_counts, int32_t *scored,
+                      double *z)
+{
+    uint64_t threshold = oracle_threshold(gamma);
+    for (int64_t n = 0; n < N; ++n) {
+        const int32_t *seq = tokens + n * row_stride;
+        int64_t len = L;
+        if (lengths != 0) {
+            len = lengths[n];
+            if (len < 0) len = 0;
+            if (len > L) len = L;
+        }
+        int64_t green = 0, T = 0;
+        for (int64_t i = width; i < len; ++i) {
+            if (ignore_repeated) {
+                int seen = 0;
+                for (int64_t j = width; j < i && !seen; ++j) seen = same_ngram(seq, j, i, width);
+                if (seen) continue;
+            }
+            ++T;
+            green += oracle_is_green_w(key, seq + i - width, width, (uint32_t)seq[i], threshold,
+                                       seeding);
+        }
+        green_counts[n] = (int32_t)green;
+        if (scored != 0) scored[n] = (int32_t)T;
+        z[n] = oracle_z_score(green, T, gamma);
+    }
+}
