@@ -148,7 +148,7 @@ def _mean_us(torch, launch, n_launch, warmup=10):
     return a.elapsed_time(b) / n_launch * 1e3
 
 
-def other_configs(torch, sbw, dev, steps):
+def other_configs(torch, sbw, dev, steps, c5_tokens):
     """The remaining workload configurations, each timed back to back with enough
     rotating buffers (> 256 MB in total) that no launch is served from the Infinity
     Cache left by the previous one."""
@@ -232,6 +232,24 @@ def other_configs(torch, sbw, dev, steps):
         topk[dt] = {"us": us, "candidates_per_s": c["B"] * 40 / us * 1e6}
         del bufs
     res["c4_sbw_ss_top40"] = topk
+
+    # c5 detection, texts of lengths drawn in [L/2, L], every position or each distinct
+    # n-gram once
+    c5 = workloads.C5
+    lens = torch.from_numpy(workloads.rng_for("c5", salt=9).integers(
+        c5["L"] // 2, c5["L"] + 1, c5["N"]).astype(np.int32)).to(dev)
+    det = {}
+    for seeding, t in c5_tokens.items():
+        td = torch.from_numpy(t).to(dev)
+        outs = (torch.empty(c5["N"], dtype=torch.int32, device=dev),
+                torch.empty(c5["N"], dtype=torch.int32, device=dev),
+                torch.empty(c5["N"], dtype=torch.float64, device=dev))
+        for rule, ignore in (("lengths", False), ("lengths_distinct_ngrams", True)):
+            us = _mean_us(torch, lambda i, s=seeding, ig=ignore: sbw.detect_ex(
+                td, key, c5["gamma"], s, lengths=lens, ignore_repeated=ig, counts=outs[0],
+                scored=outs[1], z=outs[2]), steps)
+            det[f"{seeding}/{rule}"] = {"us": us, "seq_per_s": c5["N"] / us * 1e6}
+    res["c5_detect_ex"] = det
 
     # c4 at B=1024 (623 MB per buffer), both seedings
     c = workloads.C4
@@ -472,7 +490,7 @@ def main():
     if not args.no_configs:
         del bufs
         torch.cuda.empty_cache()
-        out["configs"] = other_configs(torch, sbw, dev, args.steps)
+        out["configs"] = other_configs(torch, sbw, dev, args.steps, toks)
         # The fused argmax pass runs at one shape only, so its name alone keys it.
         traffic_cfg = measured_traffic(PROFILE_CONFIGS)
         for seeding, code in (("context", 0), ("self_salt", 1)):

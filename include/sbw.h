@@ -166,6 +166,38 @@ sbw_status_t sbw_detect_window(const int32_t *tokens, int64_t N, int64_t L, int6
                                int64_t width, uint64_t key, double gamma, sbw_seeding_t seeding,
                                int32_t *green_counts, double *z, void *stream);
 
+/* Flags of sbw_detect_ex. */
+typedef enum {
+    SBW_DETECT_IGNORE_REPEATED = 1   /* score each distinct (width+1)-gram once */
+} sbw_detect_flags_t;
+
+/*
+ * sbw_detect_ex -- detection for a batch of texts of different lengths, optionally
+ * scoring every distinct n-gram once (a production extension of the z-test of
+ * Sec. 3; the paper scores every position and fixes neither rule).
+ *
+ *   tokens, N, L, row_stride, width, key, gamma, seeding
+ *                as for sbw_detect_window; L is the longest length (row capacity).
+ *   lengths      device, [N] int32 or NULL: sequence n holds lengths[n] tokens,
+ *                clamped to [0, L] (all L when NULL).  Positions width..len-1 are
+ *                scored, T = max(len - width, 0).
+ *   flags        0 or SBW_DETECT_IGNORE_REPEATED: then a position whose window and
+ *                token (its (width+1)-gram) already occurred at an earlier scored
+ *                position of the same sequence is left out of T and of the green
+ *                count (a repeat has the same colour).  Supported for
+ *                L - width <= 4096 (else SBW_ERR_UNSUPPORTED); other bits are
+ *                SBW_ERR_UNSUPPORTED.
+ *   green_counts device, [N] int32, written.
+ *   scored       device, [N] int32 or NULL: T of each sequence, written.
+ *   z            device, [N] double, written; NaN when T == 0.
+ * One kernel on `stream`: one wavefront per sequence, or, with the repeat rule, one
+ * workgroup per sequence with an LDS hash set (no global memory is allocated).
+ */
+sbw_status_t sbw_detect_ex(const int32_t *tokens, int64_t N, int64_t L, int64_t row_stride,
+                           const int32_t *lengths, int64_t width, uint64_t key, double gamma,
+                           sbw_seeding_t seeding, uint32_t flags, int32_t *green_counts,
+                           int32_t *scored, double *z, void *stream);
+
 /*
  * sbw_watermark_candidates -- the watermark restricted to given candidate tokens:
  * SBW-ss of the paper's scheme table (Sec. 4; self-salt, width 4, top-40

@@ -42,8 +42,10 @@ _STATUS = {
 
 EXPORTED = ("sbw_watermark", "sbw_green_mask", "sbw_detect", "sbw_watermark_window",
             "sbw_green_mask_window", "sbw_detect_window", "sbw_watermark_argmax",
-            "sbw_watermark_argmax_workspace", "sbw_watermark_candidates", "sbw_strerror",
-            "sbw_last_hip_error", "sbw_version")
+            "sbw_watermark_argmax_workspace", "sbw_watermark_candidates", "sbw_detect_ex",
+            "sbw_strerror", "sbw_last_hip_error", "sbw_version")
+DETECT_IGNORE_REPEATED = 1
+MAX_UNIQUE_POSITIONS = 4096
 MAX_CANDIDATES = 1024
 MAX_WIDTH = 8
 
@@ -81,6 +83,9 @@ def _load() -> ctypes.CDLL:
     lib.sbw_watermark_argmax.restype = i32
     lib.sbw_watermark_argmax.argtypes = [P, i32, i64, i64, i64, P, i64, u64, f64, f32, i32, P, P,
                                          P, P]
+    lib.sbw_detect_ex.restype = i32
+    lib.sbw_detect_ex.argtypes = [P, i64, i64, i64, P, i64, u64, f64, i32, ctypes.c_uint32, P, P,
+                                  P, P]
     lib.sbw_watermark_candidates.restype = i32
     lib.sbw_watermark_candidates.argtypes = [P, i32, i64, i64, i64, P, i64, P, i64, u64, f64, f32,
                                              i32, P]
@@ -300,3 +305,36 @@ def detect(tokens: torch.Tensor, key: int, gamma: float, seeding="context",
                                   int(width), _key(key), float(gamma), _seeding(seeding),
                                   counts.data_ptr(), z.data_ptr(), _stream(stream)))
     return counts, z
+
+
+def detect_ex(tokens: torch.Tensor, key: int, gamma: float, seeding="context", width: int = 1,
+              lengths: torch.Tensor | None = None, ignore_repeated: bool = False,
+              counts: torch.Tensor | None = None, scored: torch.Tensor | None = None,
+              z: torch.Tensor | None = None, stream=None):
+    """Detection of texts of different lengths: tokens int32 [N, L] (L the longest),
+    lengths int32 [N] or None (clamped to [0, L]); with ignore_repeated, each distinct
+    (width+1)-gram of a text is scored once (L - width <= 4096).  Returns (green
+    counts int32 [N], scored positions int32 [N], z float64 [N])."""
+    if tokens.dtype != torch.int32 or tokens.dim() != 2:
+        raise ValueError("tokens must be int32 [N, L]")
+    N, L = tokens.shape
+    if N > 0 and L > 0 and tokens.stride(1) != 1:
+        raise ValueError("tokens must have unit stride along L")
+    dev = tokens.device
+    if lengths is not None and (lengths.shape != (N,) or lengths.dtype != torch.int32
+                                or not lengths.is_contiguous()):
+        raise ValueError("lengths must be contiguous int32 [N]")
+    counts = torch.empty(N, dtype=torch.int32, device=dev) if counts is None else counts
+    scored = torch.empty(N, dtype=torch.int32, device=dev) if scored is None else scored
+    z = torch.empty(N, dtype=torch.float64, device=dev) if z is None else z
+    for name, t, dt in (("counts", counts, torch.int32), ("scored", scored, torch.int32),
+                        ("z", z, torch.float64)):
+        if t.shape != (N,) or t.dtype != dt or not t.is_contiguous():
+            raise ValueError(f"{name} must be contiguous {dt} [N]")
+    row_stride = tokens.stride(0) if N > 1 else max(L, tokens.stride(0))
+    _check(_lib.sbw_detect_ex(tokens.data_ptr(), N, L, row_stride,
+                              lengths.data_ptr() if lengths is not None else None, int(width),
+                              _key(key), float(gamma), _seeding(seeding),
+                              DETECT_IGNORE_REPEATED if ignore_repeated else 0, counts.data_ptr(),
+                              scored.data_ptr(), z.data_ptr(), _stream(stream)))
+    return counts, scored, z

@@ -16,7 +16,9 @@
 //             top-k self-salt scheme): one workgroup per row.
 // green_mask  one lane per 32-token word of the bit set.
 // detect      one wavefront per sequence; each lane scores positions i, i+64, ...
-//             and the wave counts green positions with a ballot + popcount.
+//             and the wave counts green positions with a ballot + popcount.  With
+//             repeated n-grams scored once: one workgroup per sequence and an LDS
+//             hash set of first occurrences.
 //
 // The context window: row b of a watermark call sees the `width` tokens
 // context[b*width .. b*width+width-1] (the tokens before the step); position i of a
@@ -669,17 +671,42 @@ __device__ __forceinline__ bool window_green(uint64_t key, const uint32_t (&w)[k
 // Positions handled per lane per pass: a pass covers 64 * kChunk positions and
 // issues all of its token loads before any arithmetic.  The host picks kChunk from
 // the number of scored positions so that short sequences do not compute idle slots.
+// Outputs of a detect launch; `lengths` (per-sequence token counts, clamped to
+// [0, L]) and `scored` (T per sequence) may be null.
+struct DetectIO {
+  const int32_t* lengths;
+  int32_t* counts;
+  int32_t* scored;
+  double* z;
+};
+
+__device__ __forceinline__ int64_t sequence_length(const int32_t* lengths, int64_t n, int64_t L) {
+  if (lengths == nullptr) return L;
+  const int64_t len = lengths[n];
+  return len < 0 ? 0 : (len > L ? L : len);
+}
+
+__device__ __forceinline__ void detect_store(const DetectIO& io, int64_t n, uint32_t green,
+                                             int64_t T, double gamma) {
+  const double t = static_cast<double>(T);
+  const double numerator = static_cast<double>(green) - t * gamma;
+  const double denominator = sqrt(t * gamma * (1.0 - gamma));
+  io.counts[n] = static_cast<int32_t>(green);
+  if (io.scored != nullptr) io.scored[n] = static_cast<int32_t>(T);
+  io.z[n] = numerator / denominator;
+}
+
 template <int kSeeding, int kChunk, int kW>
 __global__ void __launch_bounds__(kThreads)
 detect_kernel(const int32_t* __restrict__ tokens, int64_t N, int64_t L, int64_t row_stride,
-              int width, uint64_t key, uint32_t tm1, double gamma, int32_t* __restrict__ counts,
-              double* __restrict__ z) {
+              int width, uint64_t key, uint32_t tm1, double gamma, DetectIO io) {
   const int lane = threadIdx.x % kWave;
   const int64_t wave0 = static_cast<int64_t>(blockIdx.x) * kWavesPerBlock + threadIdx.x / kWave;
   for (int64_t n = wave0; n < N; n += static_cast<int64_t>(gridDim.x) * kWavesPerBlock) {
     const int32_t* seq = tokens + n * row_stride;
+    const int64_t len = sequence_length(io.lengths, n, L);
     uint32_t green = 0u;  // wave-uniform count
-    for (int64_t base = width; base < L; base += kWave * kChunk) {
+    for (int64_t base = width; base < len; base += kWave * kChunk) {
       uint32_t w[kChunk][kW], v[kChunk];
 #pragma unroll
       for (int c = 0; c < kChunk; ++c) {
@@ -687,7 +714,7 @@ detect_kernel(const int32_t* __restrict__ tokens, int64_t N, int64_t L, int64_t 
         v[c] = 0u;
 #pragma unroll
         for (int k = 0; k < kW; ++k) w[c][k] = 0u;
-        if (i < L) {
+        if (i < len) {
           v[c] = static_cast<uint32_t>(seq[i]);
 #pragma unroll
           for (int k = 0; k < kW; ++k)
@@ -700,19 +727,83 @@ detect_kernel(const int32_t* __restrict__ tokens, int64_t N, int64_t L, int64_t 
 #pragma unroll
       for (int c = 0; c < kChunk; ++c) {
         const int64_t i = base + c * kWave + lane;
-        g[c] = window_green<kSeeding, kW>(key, w[c], width, v[c], tm1) && i < L;
+        g[c] = window_green<kSeeding, kW>(key, w[c], width, v[c], tm1) && i < len;
       }
 #pragma unroll
       for (int c = 0; c < kChunk; ++c) green += static_cast<uint32_t>(__popcll(__ballot(g[c])));
     }
-    if (lane == 0) {
-      const int64_t T = L > width ? L - width : 0;
-      const double t = static_cast<double>(T);
-      const double numerator = static_cast<double>(green) - t * gamma;
-      const double denominator = sqrt(t * gamma * (1.0 - gamma));
-      counts[n] = static_cast<int32_t>(green);
-      z[n] = numerator / denominator;
+    if (lane == 0) detect_store(io, n, green, len > width ? len - width : 0, gamma);
+  }
+}
+
+// Detection with each distinct (width+1)-gram scored once.  One workgroup per
+// sequence and an insert-only hash set of positions in LDS (linear probing, at most
+// half full): a lane claims an empty slot with a compare-and-swap, or meets a slot
+// holding an equal n-gram and stops there, so exactly one position of every
+// distinct n-gram is claimed and scored, whatever the interleaving.
+constexpr uint32_t kMaxUniqueSlots = 8192;   // 32 KB of LDS: up to 4096 scored positions
+
+__device__ __forceinline__ uint32_t ngram_hash(const int32_t* seq, int64_t i, int width) {
+  uint32_t h = 0x9E3779B9u;
+  for (int k = 0; k <= width; ++k) {
+    h = (h ^ static_cast<uint32_t>(seq[i - width + k])) * 0x85EBCA6Bu;
+    h ^= h >> 13;
+  }
+  return h ^ (h >> 16);
+}
+
+__device__ __forceinline__ bool same_ngram(const int32_t* seq, int64_t a, int64_t b, int width) {
+  bool same = true;
+  for (int k = 0; k <= width; ++k) same = same && seq[a - width + k] == seq[b - width + k];
+  return same;
+}
+
+template <int kSeeding, int kW>
+__global__ void __launch_bounds__(kThreads)
+detect_unique_kernel(const int32_t* __restrict__ tokens, int64_t N, int64_t L, int64_t row_stride,
+                     int width, uint64_t key, uint32_t tm1, double gamma, uint32_t slots,
+                     DetectIO io) {
+  extern __shared__ int32_t table[];   // `slots` entries, a power of two
+  __shared__ uint32_t sums[2];
+  for (int64_t n = blockIdx.x; n < N; n += gridDim.x) {
+    const int32_t* seq = tokens + n * row_stride;
+    const int64_t len = sequence_length(io.lengths, n, L);
+    for (uint32_t sl = threadIdx.x; sl < slots; sl += kThreads) table[sl] = -1;
+    if (threadIdx.x < 2) sums[threadIdx.x] = 0u;
+    __syncthreads();
+    uint32_t trials = 0u, green = 0u;
+    for (int64_t i = width + threadIdx.x; i < len; i += kThreads) {
+      uint32_t slot = ngram_hash(seq, i, width) & (slots - 1u);
+      bool claimed = false;
+      // at most `slots` probes; the set never fills, so a lane stops long before
+      for (uint32_t probe = 0; probe < slots; ++probe) {
+        const int32_t held = atomicCAS(&table[slot], -1, static_cast<int32_t>(i));
+        if (held == -1) { claimed = true; break; }
+        if (same_ngram(seq, held, i, width)) break;
+        slot = (slot + 1u) & (slots - 1u);
+      }
+      if (claimed) {
+        uint32_t w[kW];
+#pragma unroll
+        for (int k = 0; k < kW; ++k)
+          w[k] = (kW == 1 || k < width) ? static_cast<uint32_t>(seq[i - width + k]) : 0u;
+        ++trials;
+        green += window_green<kSeeding, kW>(key, w, width, static_cast<uint32_t>(seq[i]), tm1)
+                     ? 1u : 0u;
+      }
     }
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) {
+      trials += __shfl_xor(trials, off, 64);
+      green += __shfl_xor(green, off, 64);
+    }
+    if (threadIdx.x % 64 == 0) {
+      atomicAdd(&sums[0], trials);
+      atomicAdd(&sums[1], green);
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) detect_store(io, n, sums[1], sums[0], gamma);
+    __syncthreads();  // table and sums are reset for the next sequence
   }
 }
 
@@ -879,19 +970,78 @@ void dispatch_argmax(const void* logits, int64_t B, uint32_t V, int64_t row_stri
 template <int kSeeding, int kW>
 void launch_detect(int64_t positions, int64_t blocks, hipStream_t st, const int32_t* tokens,
                    int64_t N, int64_t L, int64_t row_stride, int width, uint64_t key, uint32_t tm1,
-                   double gamma, int32_t* counts, double* z) {
+                   double gamma, const DetectIO& io) {
   if (positions <= kWave)
     hipLaunchKernelGGL((detect_kernel<kSeeding, 1, kW>), dim3(blocks), dim3(kThreads), 0, st,
-                       tokens, N, L, row_stride, width, key, tm1, gamma, counts, z);
+                       tokens, N, L, row_stride, width, key, tm1, gamma, io);
   else if (positions <= 2 * kWave)
     hipLaunchKernelGGL((detect_kernel<kSeeding, 2, kW>), dim3(blocks), dim3(kThreads), 0, st,
-                       tokens, N, L, row_stride, width, key, tm1, gamma, counts, z);
+                       tokens, N, L, row_stride, width, key, tm1, gamma, io);
   else if (positions <= 4 * kWave || kW > 1)
     hipLaunchKernelGGL((detect_kernel<kSeeding, 4, kW>), dim3(blocks), dim3(kThreads), 0, st,
-                       tokens, N, L, row_stride, width, key, tm1, gamma, counts, z);
+                       tokens, N, L, row_stride, width, key, tm1, gamma, io);
   else
     hipLaunchKernelGGL((detect_kernel<kSeeding, 8, kW>), dim3(blocks), dim3(kThreads), 0, st,
-                       tokens, N, L, row_stride, width, key, tm1, gamma, counts, z);
+                       tokens, N, L, row_stride, width, key, tm1, gamma, io);
+}
+
+template <int kSeeding, int kW>
+void launch_detect_unique(int64_t N, hipStream_t st, const int32_t* tokens, int64_t L,
+                          int64_t row_stride, int width, uint64_t key, uint32_t tm1, double gamma,
+                          uint32_t slots, const DetectIO& io) {
+  hipLaunchKernelGGL((detect_unique_kernel<kSeeding, kW>), dim3(static_cast<uint32_t>(grid_for(N))),
+                     dim3(kThreads), slots * sizeof(int32_t), st, tokens, N, L, row_stride, width,
+                     key, tm1, gamma, slots, io);
+}
+
+// Every detect entry point: validation, then one launch.
+sbw_status_t detect_impl(const int32_t* tokens, int64_t N, int64_t L, int64_t row_stride,
+                         const int32_t* lengths, int64_t width, uint64_t key, double gamma,
+                         sbw_seeding_t seeding, uint32_t flags, int32_t* green_counts,
+                         int32_t* scored, double* z, hipStream_t st) {
+  if (N < 0 || L < 0 || row_stride < L) return SBW_ERR_INVALID_ARG;
+  sbw_status_t s = check_width(width);
+  if (s != SBW_OK) return s;
+  if (!valid_seeding(seeding)) return SBW_ERR_UNSUPPORTED;
+  if ((flags & ~static_cast<uint32_t>(SBW_DETECT_IGNORE_REPEATED)) != 0u) return SBW_ERR_UNSUPPORTED;
+  if (!(gamma > 0.0 && gamma < 1.0)) return SBW_ERR_GAMMA;
+  if (L > INT32_MAX) return SBW_ERR_UNSUPPORTED;
+  const bool unique = (flags & SBW_DETECT_IGNORE_REPEATED) != 0u;
+  const int64_t positions = L > width ? L - width : 0;
+  if (unique && 2 * positions > static_cast<int64_t>(kMaxUniqueSlots)) return SBW_ERR_UNSUPPORTED;
+  if (N == 0) return SBW_OK;
+  if (green_counts == nullptr || z == nullptr || (L > 0 && tokens == nullptr))
+    return SBW_ERR_INVALID_ARG;
+  if (row_stride > 0 && N > INT64_MAX / 4 / row_stride) return SBW_ERR_UNSUPPORTED;
+  s = check_device();
+  if (s != SBW_OK) return s;
+
+  const uint64_t T = threshold_of(gamma);  // in [1, 2^32 - 1] for 0 < gamma < 1
+  const uint32_t tm1 = static_cast<uint32_t>(T - 1);
+  const int w = static_cast<int>(width);
+  const DetectIO io{lengths, green_counts, scored, z};
+  const bool ctx = seeding == SBW_SEED_CONTEXT;
+  if (unique) {
+    uint32_t slots = 64u;   // a power of two, at least twice the scored positions
+    while (slots < 2 * positions) slots *= 2u;
+    if (w == 1) {
+      if (ctx) launch_detect_unique<kContext, 1>(N, st, tokens, L, row_stride, w, key, tm1, gamma, slots, io);
+      else launch_detect_unique<kSelfSalt, 1>(N, st, tokens, L, row_stride, w, key, tm1, gamma, slots, io);
+    } else {
+      if (ctx) launch_detect_unique<kContext, kMaxWidth>(N, st, tokens, L, row_stride, w, key, tm1, gamma, slots, io);
+      else launch_detect_unique<kSelfSalt, kMaxWidth>(N, st, tokens, L, row_stride, w, key, tm1, gamma, slots, io);
+    }
+    return after_launch();
+  }
+  const int64_t blocks = grid_for((N + kWavesPerBlock - 1) / kWavesPerBlock);
+  if (w == 1) {
+    if (ctx) launch_detect<kContext, 1>(positions, blocks, st, tokens, N, L, row_stride, w, key, tm1, gamma, io);
+    else launch_detect<kSelfSalt, 1>(positions, blocks, st, tokens, N, L, row_stride, w, key, tm1, gamma, io);
+  } else {
+    if (ctx) launch_detect<kContext, kMaxWidth>(positions, blocks, st, tokens, N, L, row_stride, w, key, tm1, gamma, io);
+    else launch_detect<kSelfSalt, kMaxWidth>(positions, blocks, st, tokens, N, L, row_stride, w, key, tm1, gamma, io);
+  }
+  return after_launch();
 }
 
 }  // namespace
@@ -1071,41 +1221,16 @@ sbw_status_t sbw_green_mask(uint32_t* bits, int64_t B, int64_t V, const int32_t*
 sbw_status_t sbw_detect_window(const int32_t* tokens, int64_t N, int64_t L, int64_t row_stride,
                                int64_t width, uint64_t key, double gamma, sbw_seeding_t seeding,
                                int32_t* green_counts, double* z, void* stream) {
-  if (N < 0 || L < 0 || row_stride < L) return SBW_ERR_INVALID_ARG;
-  sbw_status_t s = check_width(width);
-  if (s != SBW_OK) return s;
-  if (!valid_seeding(seeding)) return SBW_ERR_UNSUPPORTED;
-  if (!(gamma > 0.0 && gamma < 1.0)) return SBW_ERR_GAMMA;
-  if (L > INT32_MAX) return SBW_ERR_UNSUPPORTED;
-  if (N == 0) return SBW_OK;
-  if (green_counts == nullptr || z == nullptr || (L > 0 && tokens == nullptr))
-    return SBW_ERR_INVALID_ARG;
-  if (row_stride > 0 && N > INT64_MAX / 4 / row_stride) return SBW_ERR_UNSUPPORTED;
-  s = check_device();
-  if (s != SBW_OK) return s;
+  return detect_impl(tokens, N, L, row_stride, nullptr, width, key, gamma, seeding, 0u,
+                     green_counts, nullptr, z, static_cast<hipStream_t>(stream));
+}
 
-  const uint64_t T = threshold_of(gamma);  // in [1, 2^32 - 1] for 0 < gamma < 1
-  const uint32_t tm1 = static_cast<uint32_t>(T - 1);
-  const int64_t blocks = grid_for((N + kWavesPerBlock - 1) / kWavesPerBlock);
-  const int64_t positions = L > width ? L - width : 0;
-  const int w = static_cast<int>(width);
-  hipStream_t st = static_cast<hipStream_t>(stream);
-  if (w == 1) {
-    if (seeding == SBW_SEED_CONTEXT)
-      launch_detect<kContext, 1>(positions, blocks, st, tokens, N, L, row_stride, w, key, tm1,
-                                 gamma, green_counts, z);
-    else
-      launch_detect<kSelfSalt, 1>(positions, blocks, st, tokens, N, L, row_stride, w, key, tm1,
-                                  gamma, green_counts, z);
-  } else {
-    if (seeding == SBW_SEED_CONTEXT)
-      launch_detect<kContext, kMaxWidth>(positions, blocks, st, tokens, N, L, row_stride, w, key,
-                                         tm1, gamma, green_counts, z);
-    else
-      launch_detect<kSelfSalt, kMaxWidth>(positions, blocks, st, tokens, N, L, row_stride, w, key,
-                                          tm1, gamma, green_counts, z);
-  }
-  return after_launch();
+sbw_status_t sbw_detect_ex(const int32_t* tokens, int64_t N, int64_t L, int64_t row_stride,
+                           const int32_t* lengths, int64_t width, uint64_t key, double gamma,
+                           sbw_seeding_t seeding, uint32_t flags, int32_t* green_counts,
+                           int32_t* scored, double* z, void* stream) {
+  return detect_impl(tokens, N, L, row_stride, lengths, width, key, gamma, seeding, flags,
+                     green_counts, scored, z, static_cast<hipStream_t>(stream));
 }
 
 sbw_status_t sbw_detect(const int32_t* tokens, int64_t N, int64_t L, int64_t row_stride,

@@ -36,7 +36,7 @@ def _declared():
 
 
 def test_header_declares_the_boundary():
-    assert _declared() == ["sbw_detect", "sbw_detect_window", "sbw_green_mask",
+    assert _declared() == ["sbw_detect", "sbw_detect_ex", "sbw_detect_window", "sbw_green_mask",
                            "sbw_green_mask_window", "sbw_last_hip_error", "sbw_strerror",
                            "sbw_version", "sbw_watermark", "sbw_watermark_argmax",
                            "sbw_watermark_argmax_workspace", "sbw_watermark_candidates",
@@ -295,3 +295,27 @@ def test_candidates_rejects_bad_arguments(lib):
     if not _gpu_visible():
         assert wc(lib) == NO_DEVICE
         assert wc(lib, k=1024) == NO_DEVICE
+
+
+def dx(lib, tokens=DUMMY, N=2, L=8, stride=8, lengths=NULL, width=1, gamma=0.25, seeding=0,
+       flags=0, counts=DUMMY, scored=NULL, z=DUMMY):
+    return lib.sbw_detect_ex(tokens, N, L, stride, lengths, width, KEY, gamma, seeding, flags,
+                             counts, scored, z, None)
+
+
+def test_detect_ex_rejects_bad_arguments(lib):
+    assert dx(lib, N=-1) == INVALID
+    assert dx(lib, stride=7) == INVALID
+    for name in ("tokens", "counts", "z"):
+        assert dx(lib, **{name: NULL}) == INVALID, name
+    assert dx(lib, flags=2) == UNSUPPORTED
+    assert dx(lib, width=9) == UNSUPPORTED
+    assert dx(lib, seeding=2) == UNSUPPORTED
+    assert dx(lib, gamma=0.0) == GAMMA and dx(lib, gamma=1.0) == GAMMA
+    # the repeat rule holds up to 4096 scored positions
+    assert dx(lib, flags=1, L=4098, stride=4098, width=1) == UNSUPPORTED
+    assert dx(lib, N=0, flags=1, L=4097, stride=4097) == OK
+    assert dx(lib, N=0) == OK
+    if not _gpu_visible():
+        assert dx(lib, flags=1, L=4097, stride=4097) == NO_DEVICE
+        assert dx(lib, lengths=DUMMY, scored=DUMMY) == NO_DEVICE
