@@ -42,6 +42,12 @@ namespace {
 #ifndef SBW_SELF_SALT_UNROLL
 #define SBW_SELF_SALT_UNROLL 2 // 16-byte vectors per lane, self-salt (Philox-bound)
 #endif
+// Self-salt rows per workgroup (sharing the candidate terms) are chosen per launch:
+// the most rows, up to 4 for fp32 and 2 for bf16 (register pressure), that still
+// leave kSelfSaltMinGroups workgroups to fill the chip.
+#ifndef SBW_SELF_SALT_MIN_GROUPS
+#define SBW_SELF_SALT_MIN_GROUPS 4096
+#endif
 
 constexpr int kThreads = 256;            // 4 wavefronts of 64
 constexpr int kMaxWidth = 8;             // longest context window
@@ -224,6 +230,129 @@ watermark_vec_kernel(T* __restrict__ logits, int64_t row_stride, uint32_t V, int
           full - first < static_cast<uint32_t>(kThreads * kU)) {
         for (uint32_t e = 0; e < tail; ++e)
           bias_one<T, kSeeding>(row_ptr, full * kPer + e, rs, tm1, delta);
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Self-salt watermark over kRows rows per workgroup.  The rows of a workgroup share
+// their columns, so a candidate's J(v) and the row-independent term key*J(v)*J(v)
+// of its seed are computed once per lane and reused for every row; the window terms
+// key*J(p_i)*J(v), the minimum and the Philox draw are per row.
+// ---------------------------------------------------------------------------
+struct CandTerm {
+  uint32_t jv;     // J(v)
+  uint64_t self;   // key * J(v) * J(v)
+};
+
+__device__ __forceinline__ CandTerm cand_term(uint64_t key, uint32_t v) {
+  const uint32_t jv = jenkins32(v);
+  return CandTerm{jv, mul_64x64(key, wide_mul(jv, jv))};
+}
+
+// The self-salt seed from a candidate's terms: the same minimum as self_salt_seed_w.
+template <int kW>
+__device__ __forceinline__ uint64_t self_salt_seed_t(const RowSeed<kW>& rs, const CandTerm& t) {
+  uint64_t best = t.self;
+#pragma unroll
+  for (int i = 0; i < kW; ++i) {
+    if (kW == 1 || i < rs.width) {
+      const uint64_t x = mul_64x32(rs.kjp[i], t.jv);
+      best = x < best ? x : best;
+    }
+  }
+  return best;
+}
+
+template <int kW>
+__device__ __forceinline__ f32x4 bias_vec_terms(f32x4 l, uint32_t j, const CandTerm (&ct)[4],
+                                                const RowSeed<kW>& rs, uint32_t tm1, float delta) {
+  const uint32_t x0 = philox_block(j, key_of(self_salt_seed_t(rs, ct[0]))).w0;
+  const uint32_t x1 = philox_block(j, key_of(self_salt_seed_t(rs, ct[1]))).w1;
+  const uint32_t x2 = philox_block(j, key_of(self_salt_seed_t(rs, ct[2]))).w2;
+  const uint32_t x3 = philox_block(j, key_of(self_salt_seed_t(rs, ct[3]))).w3;
+  f32x4 o;
+  o.x = bias_f32(l.x, delta, is_green(x0, tm1));
+  o.y = bias_f32(l.y, delta, is_green(x1, tm1));
+  o.z = bias_f32(l.z, delta, is_green(x2, tm1));
+  o.w = bias_f32(l.w, delta, is_green(x3, tm1));
+  return o;
+}
+
+template <int kW>
+__device__ __forceinline__ u32x4 bias_vec_terms(u32x4 raw, uint32_t j, const CandTerm (&ct)[8],
+                                                const RowSeed<kW>& rs, uint32_t tm1, float delta) {
+  uint32_t x[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e)
+    x[e] = block_word(philox_block(2u * j + static_cast<uint32_t>(e >> 2),
+                                   key_of(self_salt_seed_t(rs, ct[e]))),
+                      static_cast<uint32_t>(e & 3));
+  const uint32_t in[4] = {raw.x, raw.y, raw.z, raw.w};
+  uint32_t out[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q)
+    out[q] = bias_bf16x2(in[q], delta, is_green(x[2 * q], tm1), is_green(x[2 * q + 1], tm1));
+  return u32x4{out[0], out[1], out[2], out[3]};
+}
+
+// Grid: x = tile of kThreads * kU vectors of a row, y = group of kRows rows
+// (grid-stride over groups beyond 65535).  All rows' loads are issued first; the
+// candidate terms are computed while they are in flight.
+template <typename T, int kU, int kW, int kRows>
+__global__ void __launch_bounds__(kThreads)
+watermark_ss_rows_kernel(T* __restrict__ logits, int64_t row_stride, uint32_t V, int64_t B,
+                         const int32_t* __restrict__ context, int width, uint64_t key, uint32_t tm1,
+                         float delta) {
+  using VecT = typename std::conditional<sizeof(T) == 4, f32x4, u32x4>::type;
+  constexpr uint32_t kPer = 16u / sizeof(T);
+  const uint32_t full = V / kPer;
+  const uint32_t tail = V % kPer;
+  const uint32_t first = blockIdx.x * (kThreads * kU);
+  const bool whole = first + kThreads * kU <= full;
+  const int64_t groups = (B + kRows - 1) / kRows;
+  for (int64_t g = blockIdx.y; g < groups; g += gridDim.y) {
+    const int64_t row0 = g * kRows;
+    const int nrows = static_cast<int>(B - row0 < kRows ? B - row0 : kRows);
+    VecT buf[kRows][kU];
+#pragma unroll
+    for (int r = 0; r < kRows; ++r) {
+      if (r < nrows) {
+        const VecT* vec = reinterpret_cast<const VecT*>(logits + (row0 + r) * row_stride);
+#pragma unroll
+        for (int u = 0; u < kU; ++u) {
+          const uint32_t j = first + u * kThreads + threadIdx.x;
+          if (whole || j < full) buf[r][u] = stream_load(vec + j);
+        }
+      }
+    }
+    CandTerm ct[kU][kPer];
+#pragma unroll
+    for (int u = 0; u < kU; ++u)
+#pragma unroll
+      for (uint32_t e = 0; e < kPer; ++e)
+        ct[u][e] = cand_term(key, (first + u * kThreads + threadIdx.x) * kPer + e);
+    // unrolled for width 1 only: the wider instantiations are too large to unroll
+    constexpr int kRowUnroll = kW == 1 ? kRows : 1;
+#pragma unroll kRowUnroll
+    for (int r = 0; r < kRows; ++r) {
+      if (r < nrows) {
+        const int64_t row = row0 + r;
+        T* row_ptr = logits + row * row_stride;
+        VecT* vec = reinterpret_cast<VecT*>(row_ptr);
+        const RowSeed<kW> rs = row_seed<kSelfSalt, kW>(key, context + row * width, width);
+#pragma unroll
+        for (int u = 0; u < kU; ++u) {
+          const uint32_t j = first + u * kThreads + threadIdx.x;
+          if (whole || j < full) stream_store(vec + j, bias_vec_terms(buf[r][u], j, ct[u], rs, tm1, delta));
+        }
+        // the row's partial last vector, by lane 0 of the tile that covers it
+        if (!whole && tail != 0u && threadIdx.x == 0 && full >= first &&
+            full - first < static_cast<uint32_t>(kThreads * kU)) {
+          for (uint32_t e = 0; e < tail; ++e)
+            bias_one<T, kSelfSalt>(row_ptr, full * kPer + e, rs, tm1, delta);
+        }
       }
     }
   }
@@ -867,9 +996,28 @@ void launch_watermark(void* logits, int64_t B, uint32_t V, int64_t row_stride,
     constexpr uint32_t kPer = 16u / sizeof(T);
     const uint64_t vectors = (static_cast<uint64_t>(V) + kPer - 1) / kPer;
     const uint32_t tiles = static_cast<uint32_t>((vectors + kThreads * kU - 1) / (kThreads * kU));
-    hipLaunchKernelGGL((watermark_vec_kernel<T, kSeeding, kU, kW>), dim3(tiles, rows),
-                       dim3(kThreads), 0, stream, p, row_stride, V, B, context, width, key, tm1,
-                       delta);
+    if (kSeeding == kSelfSalt) {
+      constexpr int kMaxRows = sizeof(T) == 4 ? 4 : 2;
+      const int64_t work = static_cast<int64_t>(tiles) * B;
+      const int rows_per_group = work >= kMaxRows * int64_t{SBW_SELF_SALT_MIN_GROUPS} ? kMaxRows
+                                 : work >= 2 * int64_t{SBW_SELF_SALT_MIN_GROUPS}      ? 2
+                                                                                     : 1;
+      const int64_t groups = (B + rows_per_group - 1) / rows_per_group;
+      const dim3 grid(tiles, static_cast<uint32_t>(groups < kMaxGridY ? groups : kMaxGridY));
+      if (rows_per_group == 4)
+        hipLaunchKernelGGL((watermark_ss_rows_kernel<T, kU, kW, kMaxRows>), grid, dim3(kThreads), 0,
+                           stream, p, row_stride, V, B, context, width, key, tm1, delta);
+      else if (rows_per_group == 2)
+        hipLaunchKernelGGL((watermark_ss_rows_kernel<T, kU, kW, 2>), grid, dim3(kThreads), 0,
+                           stream, p, row_stride, V, B, context, width, key, tm1, delta);
+      else
+        hipLaunchKernelGGL((watermark_ss_rows_kernel<T, kU, kW, 1>), grid, dim3(kThreads), 0,
+                           stream, p, row_stride, V, B, context, width, key, tm1, delta);
+    } else {
+      hipLaunchKernelGGL((watermark_vec_kernel<T, kSeeding, kU, kW>), dim3(tiles, rows),
+                         dim3(kThreads), 0, stream, p, row_stride, V, B, context, width, key, tm1,
+                         delta);
+    }
   } else {
     const uint32_t tiles = static_cast<uint32_t>((static_cast<uint64_t>(V) + kThreads - 1) / kThreads);
     hipLaunchKernelGGL((watermark_elem_kernel<T, kSeeding, kW>), dim3(tiles, rows), dim3(kThreads),

@@ -330,3 +330,25 @@ def test_bf16_rounding_every_pattern(env, layout):
             got = run_watermark(env, x, prev, KEY, 1.0, delta, "context", offset=1)
         assert_logits_equal(got, oracle.watermark(x, prev, KEY, 1.0, delta, "context"),
                             f"bf16 delta={delta!r}")
+
+
+@pytest.mark.parametrize("dtype,B,V,width,rows", [
+    ("f32", 219, 152063, 1, 4),     # 75 tiles x 219 rows: 4 rows per workgroup, last group of 3
+    ("f32", 127, 152061, 1, 2),     # 2 rows per workgroup, last group of 1
+    ("bf16", 219, 152063, 1, 2),    # bf16 takes at most 2 rows
+    ("f32", 221, 151937, 4, 4),     # width 4 (SBW-ss-V), ragged tail, last group of 1
+])
+def test_self_salt_row_groups(env, dtype, B, V, width, rows):
+    """Self-salt launches large enough to share the candidate terms across `rows`
+    rows of a workgroup, with a partial last vector and a partial last row group."""
+    rng = np.random.default_rng(230 + B + width)
+    x = special_logits(rng, B, V, dtype)
+    ctx = workloads.context_tokens(B, width, V, rng)
+    say(f"self-salt row groups {dtype} B={B} V={V} h={width} rows={rows}")
+    torch, sbw, dev = env
+    t = _to_device(torch, dev, x)
+    c = torch.from_numpy(ctx).to(dev)
+    sbw.watermark(t, c if width > 1 else c[:, 0].contiguous(), WIDE, 0.25, 2.0, "self_salt")
+    torch.cuda.synchronize()
+    expect = oracle.watermark_w(x, ctx, WIDE, 0.25, 2.0, "self_salt")
+    assert_logits_equal(_from_device(torch, t), expect, f"{dtype} B={B} V={V} h={width}")
