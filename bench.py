@@ -442,12 +442,9 @@ def main():
     ss_blocks = elems / (mean_ms["wm_self_salt"] * 1e-3) / 1e9   # one Philox block per logit
     traffic = measured_traffic()
 
-    # The profile keys kernels by name and workgroup count; an fp32 watermark launch
-    # covers 2048 logits of one row per workgroup.
-    wm_groups = B * -(-V // 2048)
-
-    def traffic_of(prefix, groups):
-        hits = [v for k, v in traffic.items() if k.startswith(prefix) and k.endswith(f"@{groups}")]
+    # The main-step profile holds one launch shape per kernel, so the name keys it.
+    def traffic_of(prefix):
+        hits = [v for k, v in traffic.items() if k.startswith(prefix)]
         return hits[0] if len(hits) == 1 else None
 
     out = {
@@ -474,16 +471,16 @@ def main():
         "detect_seq_per_s": det_stats("det_self_salt")["seq_per_s"],
         "watermark": {"self_salt": ss, "context": ctx},
         "detect": {"self_salt": det_stats("det_self_salt"), "context": det_stats("det_context")},
-        "roofline": {"bound": "alu", "kernel": "watermark_vec_kernel<float, self-salt>",
+        "roofline": {"bound": "alu", "kernel": "watermark_ss_rows_kernel<float> (self-salt)",
                      "achieved": ss_blocks, "peak": PHILOX_PEAK_GBLOCKS,
                      "unit": "G Philox4x32-10 blocks/s", "frac": ss_blocks / PHILOX_PEAK_GBLOCKS,
-                     "traffic": traffic_of("sbw::watermark_vec_kernel<float, 1,", wm_groups),
+                     "traffic": traffic_of("sbw::watermark_ss_rows_kernel<float,"),
                      "algorithmic_per_launch": f"{elems} Philox blocks (one per logit), "
                                                f"{bytes_wm} HBM bytes"},
         "roofline_context": {"bound": "hbm", "kernel": "watermark_vec_kernel<float, context>",
                              "achieved": ctx["hbm_gbps"], "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                              "frac": ctx["hbm_frac"],
-                             "traffic": traffic_of("sbw::watermark_vec_kernel<float, 0,", wm_groups),
+                             "traffic": traffic_of("sbw::watermark_vec_kernel<float, 0,"),
                              "algorithmic_per_launch": f"{bytes_wm} bytes"},
         "wall_s_timed": wall,
     }
