@@ -42,11 +42,12 @@ namespace {
 #ifndef SBW_SELF_SALT_UNROLL
 #define SBW_SELF_SALT_UNROLL 2 // 16-byte vectors per lane, self-salt (Philox-bound)
 #endif
-// Self-salt rows per workgroup (sharing the candidate terms) are chosen per launch:
-// the most rows, up to 4 for fp32 and 2 for bf16 (register pressure), that still
-// leave kSelfSaltMinGroups workgroups to fill the chip.
+// Self-salt rows per workgroup (sharing the candidate terms) are chosen per launch,
+// for width 1 only (with a wider window the window terms dominate and sharing does
+// not pay): the most rows, up to 4 for fp32 and 2 for bf16 (register pressure), that
+// still leave SBW_SELF_SALT_MIN_GROUPS workgroups.
 #ifndef SBW_SELF_SALT_MIN_GROUPS
-#define SBW_SELF_SALT_MIN_GROUPS 4096
+#define SBW_SELF_SALT_MIN_GROUPS 2048
 #endif
 
 constexpr int kThreads = 256;            // 4 wavefronts of 64
@@ -333,9 +334,7 @@ watermark_ss_rows_kernel(T* __restrict__ logits, int64_t row_stride, uint32_t V,
 #pragma unroll
       for (uint32_t e = 0; e < kPer; ++e)
         ct[u][e] = cand_term(key, (first + u * kThreads + threadIdx.x) * kPer + e);
-    // unrolled for width 1 only: the wider instantiations are too large to unroll
-    constexpr int kRowUnroll = kW == 1 ? kRows : 1;
-#pragma unroll kRowUnroll
+#pragma unroll
     for (int r = 0; r < kRows; ++r) {
       if (r < nrows) {
         const int64_t row = row0 + r;
@@ -997,19 +996,22 @@ void launch_watermark(void* logits, int64_t B, uint32_t V, int64_t row_stride,
     const uint64_t vectors = (static_cast<uint64_t>(V) + kPer - 1) / kPer;
     const uint32_t tiles = static_cast<uint32_t>((vectors + kThreads * kU - 1) / (kThreads * kU));
     if (kSeeding == kSelfSalt) {
-      constexpr int kMaxRows = sizeof(T) == 4 ? 4 : 2;
+      constexpr int kMaxRows = kW > 1 ? 1 : (sizeof(T) == 4 ? 4 : 2);
       const int64_t work = static_cast<int64_t>(tiles) * B;
       const int rows_per_group = work >= kMaxRows * int64_t{SBW_SELF_SALT_MIN_GROUPS} ? kMaxRows
-                                 : work >= 2 * int64_t{SBW_SELF_SALT_MIN_GROUPS}      ? 2
-                                                                                     : 1;
+                                 : (kMaxRows >= 2 && work >= 2 * int64_t{SBW_SELF_SALT_MIN_GROUPS})
+                                     ? 2
+                                     : 1;
       const int64_t groups = (B + rows_per_group - 1) / rows_per_group;
       const dim3 grid(tiles, static_cast<uint32_t>(groups < kMaxGridY ? groups : kMaxGridY));
-      if (rows_per_group == 4)
-        hipLaunchKernelGGL((watermark_ss_rows_kernel<T, kU, kW, kMaxRows>), grid, dim3(kThreads), 0,
-                           stream, p, row_stride, V, B, context, width, key, tm1, delta);
-      else if (rows_per_group == 2)
-        hipLaunchKernelGGL((watermark_ss_rows_kernel<T, kU, kW, 2>), grid, dim3(kThreads), 0,
-                           stream, p, row_stride, V, B, context, width, key, tm1, delta);
+      if (kMaxRows == 4 && rows_per_group == 4)
+        hipLaunchKernelGGL((watermark_ss_rows_kernel<T, kU, kW, (kMaxRows > 2 ? kMaxRows : 1)>),
+                           grid, dim3(kThreads), 0, stream, p, row_stride, V, B, context, width,
+                           key, tm1, delta);
+      else if (kMaxRows >= 2 && rows_per_group == 2)
+        hipLaunchKernelGGL((watermark_ss_rows_kernel<T, kU, kW, (kMaxRows >= 2 ? 2 : 1)>), grid,
+                           dim3(kThreads), 0, stream, p, row_stride, V, B, context, width, key, tm1,
+                           delta);
       else
         hipLaunchKernelGGL((watermark_ss_rows_kernel<T, kU, kW, 1>), grid, dim3(kThreads), 0,
                            stream, p, row_stride, V, B, context, width, key, tm1, delta);

@@ -334,13 +334,14 @@ def test_bf16_rounding_every_pattern(env, layout):
 
 @pytest.mark.parametrize("dtype,B,V,width,rows", [
     ("f32", 219, 152063, 1, 4),     # 75 tiles x 219 rows: 4 rows per workgroup, last group of 3
-    ("f32", 127, 152061, 1, 2),     # 2 rows per workgroup, last group of 1
+    ("f32", 63, 152061, 1, 2),      # 2 rows per workgroup, last group of 1
     ("bf16", 219, 152063, 1, 2),    # bf16 takes at most 2 rows
-    ("f32", 221, 151937, 4, 4),     # width 4 (SBW-ss-V), ragged tail, last group of 1
+    ("f32", 221, 151937, 4, 1),     # width 4 (SBW-ss-V) keeps one row per workgroup
 ])
 def test_self_salt_row_groups(env, dtype, B, V, width, rows):
-    """Self-salt launches large enough to share the candidate terms across `rows`
-    rows of a workgroup, with a partial last vector and a partial last row group."""
+    """Self-salt launches of the sizes at which a workgroup shares the candidate terms
+    across `rows` rows (width 1 with enough workgroups), with a partial last vector
+    and a partial last row group."""
     rng = np.random.default_rng(230 + B + width)
     x = special_logits(rng, B, V, dtype)
     ctx = workloads.context_tokens(B, width, V, rng)
