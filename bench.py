@@ -128,9 +128,11 @@ def cpu_baseline(x, prev, tok_ss, seconds):
     }
 
 
-def _mean_us(torch, launch, n_launch, warmup=10):
-    """Mean GPU duration of one launch: n_launch launches captured in a HIP graph,
-    replayed once between two events (no host overhead inside the interval)."""
+def _mean_us(torch, launch, n_launch, warmup=10, warm_ms=5.0, reps=3):
+    """Mean GPU duration of one launch at steady state: n_launch launches captured in a
+    HIP graph; the graph is replayed until warm_ms of GPU time have passed (after the
+    idle gaps of an eager latency loop the clocks need that long to come back up), then
+    the median of `reps` timed replays between two events (no host overhead inside)."""
     for i in range(warmup):
         launch(i)
     torch.cuda.synchronize()
@@ -138,14 +140,20 @@ def _mean_us(torch, launch, n_launch, warmup=10):
     with torch.cuda.graph(g):
         for i in range(n_launch):
             launch(i)
-    g.replay()
     a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    a.record()
-    g.replay()
-    b.record()
-    torch.cuda.synchronize()
-    return a.elapsed_time(b) / n_launch * 1e3
+
+    def replay_ms():
+        a.record()
+        g.replay()
+        b.record()
+        torch.cuda.synchronize()
+        return a.elapsed_time(b)
+
+    spent = 0.0
+    while spent < warm_ms:
+        spent += replay_ms()
+    times = sorted(replay_ms() for _ in range(reps))
+    return times[len(times) // 2] / n_launch * 1e3
 
 
 def other_configs(torch, sbw, dev, steps, c5_tokens):
