@@ -488,7 +488,7 @@ def main():
         "roofline_context": {"bound": "hbm", "kernel": "watermark_vec_kernel<float, context>",
                              "achieved": ctx["hbm_gbps"], "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                              "frac": ctx["hbm_frac"],
-                             "traffic": traffic_of("sbw::watermark_vec_kernel<float, 0,"),
+                             "traffic": traffic_of("sbw::watermark_vec_kernel<float,"),
                              "algorithmic_per_launch": f"{bytes_wm} bytes"},
         "wall_s_timed": wall,
     }

@@ -1,13 +1,13 @@
 // HIP kernels and C ABI of libsbw (declared in include/sbw.h) for MI355X / gfx950.
 //
 // watermark   one streaming pass over the logits: each lane owns 16-byte vectors
-//             of one row (4 fp32 or 8 bf16 logits), loads them, derives the green
+//             of a row (4 fp32 or 8 bf16 logits), loads them, derives the green
 //             decision in registers (seed, Philox4x32-10 draw, threshold compare)
 //             and stores them back.  Row-uniform values (the window of previous
-//             tokens, the context seed, key * J(p_i)) are computed once per
-//             workgroup in scalar registers.  Context seeding shares one Philox
-//             block between the 4 tokens of a counter; self-salt needs one block
-//             per token.
+//             tokens, the context seed, key * J(p_i)) sit in scalar registers.
+//             Context seeding shares one Philox block between the 4 tokens of a
+//             counter; self-salt needs one block per token, and its workgroups
+//             share each candidate's hash and self term across up to 4 rows.
 // argmax      greedy decoding of the watermarked logits without writing them: one
 //             read of each logit, a per-segment (value, index) partial, a read-out
 //             kernel per row.  Colours are drawn only for logits that can still
@@ -96,19 +96,36 @@ __device__ __forceinline__ RowSeed<kW> row_seed(uint64_t key, const int32_t* win
   return rs;
 }
 
-// Self-salt seed of candidate v: min over the window and v itself of key*J(w)*J(v).
-template <int kW>
-__device__ __forceinline__ uint64_t self_salt_seed_w(const RowSeed<kW>& rs, uint32_t v) {
+// Self-salt seed of candidate v: the minimum over the window and v itself of
+// key*J(w)*J(v).  Split in two: the candidate's terms J(v) and key*J(v)*J(v), which
+// do not depend on the row, then the row's minimum.
+struct CandTerm {
+  uint32_t jv;     // J(v)
+  uint64_t self;   // key * J(v) * J(v)
+};
+
+__device__ __forceinline__ CandTerm cand_term(uint64_t key, uint32_t v) {
   const uint32_t jv = jenkins32(v);
-  uint64_t best = mul_64x64(rs.key, wide_mul(jv, jv));
+  return CandTerm{jv, mul_64x64(key, wide_mul(jv, jv))};
+}
+
+// The self-salt seed of a candidate from its terms and the row's key*J(p_i).
+template <int kW>
+__device__ __forceinline__ uint64_t self_salt_seed_t(const RowSeed<kW>& rs, const CandTerm& t) {
+  uint64_t best = t.self;
 #pragma unroll
   for (int i = 0; i < kW; ++i) {
     if (kW == 1 || i < rs.width) {
-      const uint64_t t = mul_64x32(rs.kjp[i], jv);
-      best = t < best ? t : best;
+      const uint64_t x = mul_64x32(rs.kjp[i], t.jv);
+      best = x < best ? x : best;
     }
   }
   return best;
+}
+
+template <int kW>
+__device__ __forceinline__ uint64_t self_salt_seed_w(const RowSeed<kW>& rs, uint32_t v) {
+  return self_salt_seed_t(rs, cand_term(rs.key, v));
 }
 
 template <int kSeeding, int kW>
@@ -118,51 +135,27 @@ __device__ __forceinline__ uint32_t draw(const RowSeed<kW>& rs, uint32_t v) {
 }
 
 // ---------------------------------------------------------------------------
-// Watermark vectors.
-// fp32: a vector is the 4 tokens 4j..4j+3, exactly the 4 words of the Philox
+// Context-seeded watermark vectors: one row seed, so the tokens of a Philox block
+// share it.  fp32: a vector is the 4 tokens 4j..4j+3, exactly the 4 words of the
 // block at counter j.  bf16: the 8 tokens 8j..8j+7 = blocks 2j and 2j+1.
 // ---------------------------------------------------------------------------
-template <int kSeeding, int kW>
-__device__ __forceinline__ f32x4 bias_vec(f32x4 l, uint32_t j, const RowSeed<kW>& rs, uint32_t tm1,
-                                          float delta) {
-  const uint32_t v = j * 4u;
-  uint32_t x0, x1, x2, x3;
-  if (kSeeding == kContext) {
-    const Block blk = philox_block(j, key_of(rs.seed));
-    x0 = blk.w0; x1 = blk.w1; x2 = blk.w2; x3 = blk.w3;
-  } else {
-    x0 = philox_block(j, key_of(self_salt_seed_w(rs, v + 0u))).w0;
-    x1 = philox_block(j, key_of(self_salt_seed_w(rs, v + 1u))).w1;
-    x2 = philox_block(j, key_of(self_salt_seed_w(rs, v + 2u))).w2;
-    x3 = philox_block(j, key_of(self_salt_seed_w(rs, v + 3u))).w3;
-  }
+__device__ __forceinline__ f32x4 bias_vec_context(f32x4 l, uint32_t j, uint64_t seed, uint32_t tm1,
+                                                  float delta) {
+  const Block blk = philox_block(j, key_of(seed));
   f32x4 o;
-  o.x = bias_f32(l.x, delta, is_green(x0, tm1));
-  o.y = bias_f32(l.y, delta, is_green(x1, tm1));
-  o.z = bias_f32(l.z, delta, is_green(x2, tm1));
-  o.w = bias_f32(l.w, delta, is_green(x3, tm1));
+  o.x = bias_f32(l.x, delta, is_green(blk.w0, tm1));
+  o.y = bias_f32(l.y, delta, is_green(blk.w1, tm1));
+  o.z = bias_f32(l.z, delta, is_green(blk.w2, tm1));
+  o.w = bias_f32(l.w, delta, is_green(blk.w3, tm1));
   return o;
 }
 
-template <int kSeeding, int kW>
-__device__ __forceinline__ u32x4 bias_vec(u32x4 raw, uint32_t j, const RowSeed<kW>& rs,
-                                          uint32_t tm1, float delta) {
-  const uint32_t v = j * 8u;
-  uint32_t x[8];
-  if (kSeeding == kContext) {
-    const Key k = key_of(rs.seed);
-    const Block a = philox_block(2u * j, k);
-    const Block b = philox_block(2u * j + 1u, k);
-    x[0] = a.w0; x[1] = a.w1; x[2] = a.w2; x[3] = a.w3;
-    x[4] = b.w0; x[5] = b.w1; x[6] = b.w2; x[7] = b.w3;
-  } else {
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const uint32_t t = v + static_cast<uint32_t>(e);
-      x[e] = block_word(philox_block(t >> 2, key_of(self_salt_seed_w(rs, t))),
-                        static_cast<uint32_t>(e & 3));
-    }
-  }
+__device__ __forceinline__ u32x4 bias_vec_context(u32x4 raw, uint32_t j, uint64_t seed, uint32_t tm1,
+                                                  float delta) {
+  const Key k = key_of(seed);
+  const Block a = philox_block(2u * j, k);
+  const Block b = philox_block(2u * j + 1u, k);
+  const uint32_t x[8] = {a.w0, a.w1, a.w2, a.w3, b.w0, b.w1, b.w2, b.w3};
   const uint32_t in[4] = {raw.x, raw.y, raw.z, raw.w};
   uint32_t out[4];
 #pragma unroll
@@ -184,11 +177,11 @@ __device__ __forceinline__ void bias_one(T* row, uint32_t v, const RowSeed<kW>& 
   row[v] = bias_elem(row[v], delta, is_green(x, tm1));
 }
 
-// Vectorised watermark for rows whose start is 16-byte aligned.  Grid: x = tile of
-// kThreads * kU vectors within a row, y = row (grid-stride over rows beyond 65535).
-// Each lane issues its logits load before reading the row's window, so the scalar
-// loads of the window overlap the HBM stream.
-template <typename T, int kSeeding, int kU, int kW>
+// Context-seeded watermark for rows whose start is 16-byte aligned.  Grid: x = tile
+// of kThreads * kU vectors within a row, y = row (grid-stride over rows beyond
+// 65535).  Each lane issues its logits load before reading the row's window, so the
+// scalar loads of the window overlap the HBM stream.
+template <typename T, int kU, int kW>
 __global__ void __launch_bounds__(kThreads)
 watermark_vec_kernel(T* __restrict__ logits, int64_t row_stride, uint32_t V, int64_t B,
                      const int32_t* __restrict__ context, int width, uint64_t key, uint32_t tm1,
@@ -207,11 +200,11 @@ watermark_vec_kernel(T* __restrict__ logits, int64_t row_stride, uint32_t V, int
       // Whole tile inside the row: no per-vector guards, all loads in flight at once.
 #pragma unroll
       for (int u = 0; u < kU; ++u) buf[u] = stream_load(vec + first + u * kThreads + threadIdx.x);
-      const RowSeed<kW> rs = row_seed<kSeeding, kW>(key, window, width);
+      const RowSeed<kW> rs = row_seed<kContext, kW>(key, window, width);
 #pragma unroll
       for (int u = 0; u < kU; ++u) {
         const uint32_t j = first + u * kThreads + threadIdx.x;
-        stream_store(vec + j, bias_vec<kSeeding>(buf[u], j, rs, tm1, delta));
+        stream_store(vec + j, bias_vec_context(buf[u], j, rs.seed, tm1, delta));
       }
     } else {
 #pragma unroll
@@ -219,18 +212,18 @@ watermark_vec_kernel(T* __restrict__ logits, int64_t row_stride, uint32_t V, int
         const uint32_t j = first + u * kThreads + threadIdx.x;
         if (j < full) buf[u] = stream_load(vec + j);
       }
-      const RowSeed<kW> rs = row_seed<kSeeding, kW>(key, window, width);
+      const RowSeed<kW> rs = row_seed<kContext, kW>(key, window, width);
 #pragma unroll
       for (int u = 0; u < kU; ++u) {
         const uint32_t j = first + u * kThreads + threadIdx.x;
-        if (j < full) stream_store(vec + j, bias_vec<kSeeding>(buf[u], j, rs, tm1, delta));
+        if (j < full) stream_store(vec + j, bias_vec_context(buf[u], j, rs.seed, tm1, delta));
       }
       // The partial vector at the end of the row, element by element, by lane 0 of
       // the tile that covers vector index `full`.
       if (tail != 0u && threadIdx.x == 0 && full >= first &&
           full - first < static_cast<uint32_t>(kThreads * kU)) {
         for (uint32_t e = 0; e < tail; ++e)
-          bias_one<T, kSeeding>(row_ptr, full * kPer + e, rs, tm1, delta);
+          bias_one<T, kContext>(row_ptr, full * kPer + e, rs, tm1, delta);
       }
     }
   }
@@ -242,30 +235,6 @@ watermark_vec_kernel(T* __restrict__ logits, int64_t row_stride, uint32_t V, int
 // of its seed are computed once per lane and reused for every row; the window terms
 // key*J(p_i)*J(v), the minimum and the Philox draw are per row.
 // ---------------------------------------------------------------------------
-struct CandTerm {
-  uint32_t jv;     // J(v)
-  uint64_t self;   // key * J(v) * J(v)
-};
-
-__device__ __forceinline__ CandTerm cand_term(uint64_t key, uint32_t v) {
-  const uint32_t jv = jenkins32(v);
-  return CandTerm{jv, mul_64x64(key, wide_mul(jv, jv))};
-}
-
-// The self-salt seed from a candidate's terms: the same minimum as self_salt_seed_w.
-template <int kW>
-__device__ __forceinline__ uint64_t self_salt_seed_t(const RowSeed<kW>& rs, const CandTerm& t) {
-  uint64_t best = t.self;
-#pragma unroll
-  for (int i = 0; i < kW; ++i) {
-    if (kW == 1 || i < rs.width) {
-      const uint64_t x = mul_64x32(rs.kjp[i], t.jv);
-      best = x < best ? x : best;
-    }
-  }
-  return best;
-}
-
 template <int kW>
 __device__ __forceinline__ f32x4 bias_vec_terms(f32x4 l, uint32_t j, const CandTerm (&ct)[4],
                                                 const RowSeed<kW>& rs, uint32_t tm1, float delta) {
@@ -619,10 +588,10 @@ argmax_vec_kernel(const T* __restrict__ logits, int64_t row_stride, uint32_t V, 
     for (int n = 0; n < kN; ++n) {
       const uint32_t j = seg_first + n * kThreads + threadIdx.x;
       if (!(whole || j < full)) continue;
-      if (kSeeding == kSelfSalt)
+      if constexpr (kSeeding == kSelfSalt)
         scan_self_salt(lb_lane, buf[n], j, rs, tm1, none_green, delta, lb);
       else if (may_reach(buf[n], dplus, delta, lb))
-        consider_vec(lb_lane, none_green ? buf[n] : bias_vec<kSeeding>(buf[n], j, rs, tm1, delta), j);
+        consider_vec(lb_lane, none_green ? buf[n] : bias_vec_context(buf[n], j, rs.seed, tm1, delta), j);
     }
     // The row's partial last vector, element by element, by lane 0 of the segment
     // that holds it (never skipped).
@@ -995,7 +964,7 @@ void launch_watermark(void* logits, int64_t B, uint32_t V, int64_t row_stride,
     constexpr uint32_t kPer = 16u / sizeof(T);
     const uint64_t vectors = (static_cast<uint64_t>(V) + kPer - 1) / kPer;
     const uint32_t tiles = static_cast<uint32_t>((vectors + kThreads * kU - 1) / (kThreads * kU));
-    if (kSeeding == kSelfSalt) {
+    if constexpr (kSeeding == kSelfSalt) {
       constexpr int kMaxRows = kW > 1 ? 1 : (sizeof(T) == 4 ? 4 : 2);
       const int64_t work = static_cast<int64_t>(tiles) * B;
       const int rows_per_group = work >= kMaxRows * int64_t{SBW_SELF_SALT_MIN_GROUPS} ? kMaxRows
@@ -1016,7 +985,7 @@ void launch_watermark(void* logits, int64_t B, uint32_t V, int64_t row_stride,
         hipLaunchKernelGGL((watermark_ss_rows_kernel<T, kU, kW, 1>), grid, dim3(kThreads), 0,
                            stream, p, row_stride, V, B, context, width, key, tm1, delta);
     } else {
-      hipLaunchKernelGGL((watermark_vec_kernel<T, kSeeding, kU, kW>), dim3(tiles, rows),
+      hipLaunchKernelGGL((watermark_vec_kernel<T, kU, kW>), dim3(tiles, rows),
                          dim3(kThreads), 0, stream, p, row_stride, V, B, context, width, key, tm1,
                          delta);
     }
