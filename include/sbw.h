@@ -2,17 +2,24 @@
  * sbw.h -- C ABI of libsbw, the MI355X (gfx950) hot path of Stateless Bernoulli
  * Watermarking ("Flip, Don't Shuffle", arXiv 2609.03844).
  *
- * Two operations, each one hand-written HIP kernel launch on the caller's stream:
+ * Operations, each hand-written HIP kernels launched on the caller's stream:
  *
  *   watermark  For every row b of a decode batch and every token v of the
- *              vocabulary: derive the seed r from the row's previous token (and,
- *              for self-salt, from v), draw x = CBRNG(v, r), and add delta to the
- *              logit when x < gamma (Sec. 2.2, Eq. 1 and Eq. 2; full-vocabulary
- *              self-salt, Sec. 5.2).  In place, one read and one write per logit.
+ *              vocabulary: derive the seed r from the row's previous token (or
+ *              window of tokens; and, for self-salt, from v), draw x = CBRNG(v, r),
+ *              and add delta to the logit when x < gamma (Sec. 2.2, Eq. 1 and
+ *              Eq. 2; full-vocabulary self-salt, Sec. 5.2).  In place, one read and
+ *              one write per logit.
+ *   watermark_argmax     greedy decoding fused with the watermark: the index of
+ *              the largest watermarked logit per row, the logits read once.
+ *   watermark_candidates the watermark on caller-given candidate ids only (the
+ *              top-k self-salt scheme of Sec. 4).
+ *   green_mask the green lists as bit sets (a parity and debugging aid).
  *   detect     For every sequence: count the positions whose token is green
- *              under the seed of the token before it (O(1) per token, Sec. 2.2)
+ *              under the seed of the token(s) before it (O(1) per token, Sec. 2.2)
  *              and return the count W and z = (W - T gamma)/sqrt(T gamma (1-gamma))
- *              with T = L - 1 (Sec. 3).
+ *              with T = L - 1 (Sec. 3); detect_window and detect_ex for windows,
+ *              per-sequence lengths and repeated n-grams.
  *
  * Definitions fixed by this library where the paper leaves them open:
  *   CBRNG(v, r)   the v-th 32-bit output of the Philox4x32-10 stream keyed by r:
@@ -30,7 +37,9 @@
  *
  * Conventions shared by every entry point:
  *   - Buffers belong to the caller.  Device pointers are HIP device (or managed)
- *     memory; the library allocates nothing, on host or device (App. E, memory).
+ *     memory of the current device; they are not checked (a host pointer makes
+ *     the kernel fault).  The library allocates nothing, on host or device
+ *     (App. E, memory).
  *   - Work is enqueued on `stream` (a hipStream_t; NULL = the null stream) and the
  *     call returns without synchronising the host.  Functions hold no global
  *     mutable state and are reentrant.

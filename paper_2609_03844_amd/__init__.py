@@ -138,6 +138,22 @@ def _key(key: int) -> int:
     return int(key) & 0xFFFFFFFFFFFFFFFF
 
 
+def _on_device(**tensors) -> None:
+    """Every tensor argument must live on the current HIP device: the kernels
+    dereference the pointers, and a host or peer pointer would fault the GPU."""
+    dev = None
+    for name, t in tensors.items():
+        if t is None:
+            continue
+        if not t.is_cuda:
+            raise ValueError(f"{name} must be on the current HIP device, got {t.device}")
+        if dev is None:
+            dev = torch.cuda.current_device()
+        if t.device.index != dev:
+            raise ValueError(f"{name} must be on the current HIP device (cuda:{dev}), "
+                             f"got {t.device}")
+
+
 def _window(context: torch.Tensor, B: int):
     """[B] (the previous token) or [B, h] (the h tokens before the step) -> (tensor, h)."""
     if context.dtype != torch.int32:
@@ -176,9 +192,11 @@ def watermark(logits: torch.Tensor, prev_tokens: torch.Tensor, key: int, gamma: 
         raise ValueError("logits must have unit stride along the vocabulary")
     context, width = _window(prev_tokens, B)
     row_stride = logits.stride(0) if B > 1 else max(V, logits.stride(0))
+    seed_kind = _seeding(seeding)
+    _on_device(logits=logits, prev_tokens=context)
     _check(_lib.sbw_watermark_window(logits.data_ptr(), dtype, B, V, row_stride,
                                      context.data_ptr(), width, _key(key), float(gamma),
-                                     float(delta), _seeding(seeding), _stream(stream)))
+                                     float(delta), seed_kind, _stream(stream)))
     return logits
 
 
@@ -204,6 +222,7 @@ def watermark_candidates(logits: torch.Tensor, prev_tokens: torch.Tensor,
         raise ValueError("candidates must be contiguous int32 [B, k]")
     context, width = _window(prev_tokens, B)
     row_stride = logits.stride(0) if B > 1 else max(V, logits.stride(0))
+    _on_device(logits=logits, prev_tokens=context, candidates=candidates)
     _check(_lib.sbw_watermark_candidates(logits.data_ptr(), dtype, B, V, row_stride,
                                          candidates.data_ptr(), candidates.shape[1],
                                          context.data_ptr(), width, _key(key), float(gamma),
@@ -249,6 +268,8 @@ def watermark_argmax(logits: torch.Tensor, prev_tokens: torch.Tensor, key: int, 
                                or not values.is_contiguous()):
         raise ValueError("values must be contiguous float32 [B]")
     row_stride = logits.stride(0) if B > 1 else max(V, logits.stride(0))
+    _on_device(logits=logits, prev_tokens=context, tokens=tokens, values=values,
+               workspace=workspace)
     _check(_lib.sbw_watermark_argmax(logits.data_ptr(), dtype, B, V, row_stride,
                                      context.data_ptr(), width, _key(key), float(gamma),
                                      float(delta), _seeding(seeding), tokens.data_ptr(),
@@ -275,6 +296,7 @@ def green_mask(prev_tokens: torch.Tensor, V: int, key: int, gamma: float, seedin
         out = torch.empty((B, words), dtype=torch.int32, device=prev_tokens.device)
     elif out.shape != (B, words) or out.dtype != torch.int32 or not out.is_contiguous():
         raise ValueError("out must be contiguous int32 [B, ceil(V/32)]")
+    _on_device(prev_tokens=context, out=out)
     _check(_lib.sbw_green_mask_window(out.data_ptr(), B, int(V), context.data_ptr(), width,
                                       _key(key), float(gamma), _seeding(seeding),
                                       _stream(stream)))
@@ -301,6 +323,7 @@ def detect(tokens: torch.Tensor, key: int, gamma: float, seeding="context",
     if z.shape != (N,) or z.dtype != torch.float64 or not z.is_contiguous():
         raise ValueError("z must be contiguous float64 [N]")
     row_stride = tokens.stride(0) if N > 1 else max(L, tokens.stride(0))
+    _on_device(tokens=tokens, counts=counts, z=z)
     _check(_lib.sbw_detect_window(tokens.data_ptr() if L > 0 else None, N, L, row_stride,
                                   int(width), _key(key), float(gamma), _seeding(seeding),
                                   counts.data_ptr(), z.data_ptr(), _stream(stream)))
@@ -332,6 +355,7 @@ def detect_ex(tokens: torch.Tensor, key: int, gamma: float, seeding="context", w
         if t.shape != (N,) or t.dtype != dt or not t.is_contiguous():
             raise ValueError(f"{name} must be contiguous {dt} [N]")
     row_stride = tokens.stride(0) if N > 1 else max(L, tokens.stride(0))
+    _on_device(tokens=tokens, lengths=lengths, counts=counts, scored=scored, z=z)
     _check(_lib.sbw_detect_ex(tokens.data_ptr(), N, L, row_stride,
                               lengths.data_ptr() if lengths is not None else None, int(width),
                               _key(key), float(gamma), _seeding(seeding),

@@ -319,3 +319,25 @@ def test_detect_ex_rejects_bad_arguments(lib):
     if not _gpu_visible():
         assert dx(lib, flags=1, L=4097, stride=4097) == NO_DEVICE
         assert dx(lib, lengths=DUMMY, scored=DUMMY) == NO_DEVICE
+
+
+def test_binding_rejects_tensors_off_the_device(sbw):
+    # a host pointer would reach a kernel: the binding refuses before any HIP call
+    import torch
+    x = torch.zeros(2, 8)
+    prev = torch.zeros(2, dtype=torch.int32)
+    with pytest.raises(ValueError, match="current HIP device"):
+        sbw.watermark(x, prev, KEY, 0.25, 2.0)
+    with pytest.raises(ValueError, match="current HIP device"):
+        sbw.watermark_candidates(x, prev, torch.zeros(2, 3, dtype=torch.int32), KEY, 0.25, 2.0)
+    with pytest.raises(ValueError, match="current HIP device"):
+        sbw.watermark_argmax(x, prev, KEY, 0.25, 2.0, tokens=torch.zeros(2, dtype=torch.int32),
+                             values=torch.zeros(2), workspace=torch.zeros(4, dtype=torch.int64))
+    with pytest.raises(ValueError, match="current HIP device"):
+        sbw.green_mask(prev, 8, KEY, 0.25, out=torch.zeros(2, 1, dtype=torch.int32))
+    tok = torch.zeros(2, 5, dtype=torch.int32)
+    with pytest.raises(ValueError, match="current HIP device"):
+        sbw.detect(tok, KEY, 0.25, counts=torch.zeros(2, dtype=torch.int32),
+                   z=torch.zeros(2, dtype=torch.float64))
+    with pytest.raises(ValueError, match="current HIP device"):
+        sbw.detect_ex(tok, KEY, 0.25)
