@@ -834,11 +834,18 @@ detect_kernel(const int32_t* __restrict__ tokens, int64_t N, int64_t L, int64_t 
 }
 
 // Detection with each distinct (width+1)-gram scored once.  One workgroup per
-// sequence and an insert-only hash set of positions in LDS (linear probing, at most
-// half full): a lane claims an empty slot with a compare-and-swap, or meets a slot
-// holding an equal n-gram and stops there, so exactly one position of every
-// distinct n-gram is claimed and scored, whatever the interleaving.
-constexpr uint32_t kMaxUniqueSlots = 8192;   // 32 KB of LDS: up to 4096 scored positions
+// sequence: the sequence is staged in LDS, next to an insert-only hash set of
+// positions (linear probing; a quarter full, half for the longest texts).  A slot
+// holds the position in its low 13 bits and 19 bits of the n-gram's hash above them.
+// A lane claims an empty slot with a compare-and-swap, or meets a slot holding an
+// equal n-gram and stops there, so exactly one position of every distinct n-gram is
+// claimed and scored, whatever the interleaving; the tokens are compared only when
+// the hash bits agree.
+constexpr uint32_t kMaxUniqueSlots = 8192;   // 32 KB of LDS (+ up to 16 KB of tokens): 4096 positions
+constexpr uint32_t kSlotPosBits = 13;        // positions < 8192 (L <= 4096 + kMaxWidth)
+constexpr int32_t kEmptySlot = -1;           // never a slot value: no position is 8191
+static_assert(kMaxUniqueSlots / 2 + kMaxWidth < (1u << kSlotPosBits) - 1u,
+              "every position fits the slot's position bits and differs from 8191");
 
 __device__ __forceinline__ uint32_t ngram_hash(const int32_t* seq, int64_t i, int width) {
   uint32_t h = 0x9E3779B9u;
@@ -855,28 +862,41 @@ __device__ __forceinline__ bool same_ngram(const int32_t* seq, int64_t a, int64_
   return same;
 }
 
+#ifndef SBW_UNIQUE_BLOCK
+#define SBW_UNIQUE_BLOCK 256  // threads per sequence of the repeat-rule detect
+#endif
+constexpr int kUniqueBlock = SBW_UNIQUE_BLOCK;
+
 template <int kSeeding, int kW>
-__global__ void __launch_bounds__(kThreads)
+__global__ void __launch_bounds__(kUniqueBlock)
 detect_unique_kernel(const int32_t* __restrict__ tokens, int64_t N, int64_t L, int64_t row_stride,
                      int width, uint64_t key, uint32_t tm1, double gamma, uint32_t slots,
                      DetectIO io) {
-  extern __shared__ int32_t table[];   // `slots` entries, a power of two
+  extern __shared__ int32_t smem[];
+  int32_t* table = smem;           // `slots` entries, a power of two
+  int32_t* seq = smem + slots;     // the sequence's tokens (up to L)
   __shared__ uint32_t sums[2];
   for (int64_t n = blockIdx.x; n < N; n += gridDim.x) {
-    const int32_t* seq = tokens + n * row_stride;
+    const int32_t* src = tokens + n * row_stride;
     const int64_t len = sequence_length(io.lengths, n, L);
-    for (uint32_t sl = threadIdx.x; sl < slots; sl += kThreads) table[sl] = -1;
-    if (threadIdx.x < 2) sums[threadIdx.x] = 0u;
+    for (int64_t t = threadIdx.x; t < len; t += kUniqueBlock) seq[t] = src[t];
+    for (uint32_t sl = threadIdx.x; sl < slots; sl += kUniqueBlock) table[sl] = kEmptySlot;
+    if (kUniqueBlock > kWave && threadIdx.x < 2) sums[threadIdx.x] = 0u;
     __syncthreads();
     uint32_t trials = 0u, green = 0u;
-    for (int64_t i = width + threadIdx.x; i < len; i += kThreads) {
-      uint32_t slot = ngram_hash(seq, i, width) & (slots - 1u);
+    for (int64_t i = width + threadIdx.x; i < len; i += kUniqueBlock) {
+      const uint32_t h = ngram_hash(seq, i, width);
+      const uint32_t fp = h >> kSlotPosBits;
+      const int32_t mine = static_cast<int32_t>((fp << kSlotPosBits) | static_cast<uint32_t>(i));
+      uint32_t slot = h & (slots - 1u);
       bool claimed = false;
       // at most `slots` probes; the set never fills, so a lane stops long before
       for (uint32_t probe = 0; probe < slots; ++probe) {
-        const int32_t held = atomicCAS(&table[slot], -1, static_cast<int32_t>(i));
-        if (held == -1) { claimed = true; break; }
-        if (same_ngram(seq, held, i, width)) break;
+        const int32_t held = atomicCAS(&table[slot], kEmptySlot, mine);
+        if (held == kEmptySlot) { claimed = true; break; }
+        if ((static_cast<uint32_t>(held) >> kSlotPosBits) == fp &&
+            same_ngram(seq, static_cast<int64_t>(static_cast<uint32_t>(held) & ((1u << kSlotPosBits) - 1u)), i, width))
+          break;
         slot = (slot + 1u) & (slots - 1u);
       }
       if (claimed) {
@@ -894,13 +914,17 @@ detect_unique_kernel(const int32_t* __restrict__ tokens, int64_t N, int64_t L, i
       trials += __shfl_xor(trials, off, 64);
       green += __shfl_xor(green, off, 64);
     }
-    if (threadIdx.x % 64 == 0) {
-      atomicAdd(&sums[0], trials);
-      atomicAdd(&sums[1], green);
+    if constexpr (kUniqueBlock == kWave) {
+      if (threadIdx.x == 0) detect_store(io, n, green, trials, gamma);
+    } else {
+      if (threadIdx.x % 64 == 0) {
+        atomicAdd(&sums[0], trials);
+        atomicAdd(&sums[1], green);
+      }
+      __syncthreads();
+      if (threadIdx.x == 0) detect_store(io, n, sums[1], sums[0], gamma);
     }
-    __syncthreads();
-    if (threadIdx.x == 0) detect_store(io, n, sums[1], sums[0], gamma);
-    __syncthreads();  // table and sums are reset for the next sequence
+    __syncthreads();  // the table (and sums) are reset for the next sequence
   }
 }
 
@@ -1108,9 +1132,10 @@ template <int kSeeding, int kW>
 void launch_detect_unique(int64_t N, hipStream_t st, const int32_t* tokens, int64_t L,
                           int64_t row_stride, int width, uint64_t key, uint32_t tm1, double gamma,
                           uint32_t slots, const DetectIO& io) {
+  const size_t lds = (static_cast<size_t>(slots) + static_cast<size_t>(L)) * sizeof(int32_t);
   hipLaunchKernelGGL((detect_unique_kernel<kSeeding, kW>), dim3(static_cast<uint32_t>(grid_for(N))),
-                     dim3(kThreads), slots * sizeof(int32_t), st, tokens, N, L, row_stride, width,
-                     key, tm1, gamma, slots, io);
+                     dim3(kUniqueBlock), lds, st, tokens, N, L, row_stride, width, key, tm1, gamma,
+                     slots, io);
 }
 
 // Every detect entry point: validation, then one launch.
@@ -1141,8 +1166,9 @@ sbw_status_t detect_impl(const int32_t* tokens, int64_t N, int64_t L, int64_t ro
   const DetectIO io{lengths, green_counts, scored, z};
   const bool ctx = seeding == SBW_SEED_CONTEXT;
   if (unique) {
-    uint32_t slots = 64u;   // a power of two, at least twice the scored positions
-    while (slots < 2 * positions) slots *= 2u;
+    // a power of two, four times the scored positions where it fits, at least twice
+    uint32_t slots = 64u;
+    while (slots < 4 * positions && slots < kMaxUniqueSlots) slots *= 2u;
     if (w == 1) {
       if (ctx) launch_detect_unique<kContext, 1>(N, st, tokens, L, row_stride, w, key, tm1, gamma, slots, io);
       else launch_detect_unique<kSelfSalt, 1>(N, st, tokens, L, row_stride, w, key, tm1, gamma, slots, io);
