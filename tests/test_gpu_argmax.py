@@ -126,11 +126,14 @@ def test_argmax_graph_replay(env):
         assert_argmax_equal((tokens.cpu().numpy(), values.cpu().numpy()), expect, f"replay {replay}")
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("seeding", ["context", "self_salt"])
-def test_argmax_c4_full_size(env, seeding):
+def test_argmax_c4_full_size(env, seeding, dtype):
     c = workloads.C4
     x, prev = workloads.watermark_inputs("c4")
-    say(f"argmax c4 {seeding}")
+    if dtype == "bf16":
+        x = workloads.f32_to_bf16_bits(x)
+    say(f"argmax c4 {seeding} {dtype}")
     got = run_argmax(env, x, prev, KEY, c["gamma"], c["delta"], seeding)
     expect = oracle.watermark_argmax(x, prev, KEY, c["gamma"], c["delta"], seeding)
     assert_argmax_equal(got, expect, f"c4 {seeding}")
