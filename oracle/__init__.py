@@ -85,6 +85,12 @@ def _declare(l: ctypes.CDLL) -> ctypes.CDLL:
         "oracle_watermark_argmax_bf16_w": (None, [P, i64, i64, i64, P, i64, u64, f64, f32, i32, P, P]),
         "oracle_watermark_candidates_f32_w": (None, [P, i64, i64, i64, P, i64, P, i64, u64, f64, f32, i32]),
         "oracle_detect_ex": (None, [P, i64, i64, i64, P, i64, u64, f64, i32, i32, P, P, P]),
+        "oracle_sample_log": (f32, [f32]),
+        "oracle_gumbel": (f32, [u32, u64]),
+        "oracle_sample_log_many": (None, [P, i64, P]),
+        "oracle_gumbel_many": (None, [P, P, i64, P]),
+        "oracle_watermark_sample_f32_w": (None, [P, i64, i64, i64, P, i64, u64, f64, f32, i32, P, f32, P, P]),
+        "oracle_watermark_sample_bf16_w": (None, [P, i64, i64, i64, P, i64, u64, f64, f32, i32, P, f32, P, P]),
         "oracle_watermark_candidates_bf16_w": (None, [P, i64, i64, i64, P, i64, P, i64, u64, f64, f32, i32]),
     }
     for name, (res, args) in sig.items():
@@ -358,3 +364,44 @@ def detect_ex(tokens: np.ndarray, width: int, key: int, gamma: float, seeding="c
                            key, float(gamma), _seeding(seeding), int(bool(ignore_repeated)),
                            _ptr(counts), _ptr(scored), _ptr(z))
     return counts, scored, z
+
+
+def sample_log(x) -> np.ndarray:
+    """The sampler's fp32 logarithm, elementwise (finite normal x > 0)."""
+    a = np.ascontiguousarray(x, dtype=np.float32)
+    out = np.empty_like(a)
+    lib().oracle_sample_log_many(_ptr(a), a.size, _ptr(out))
+    return out
+
+
+def gumbel_many(v, seed) -> np.ndarray:
+    """Gumbel noise G(v, seed) = -log(-log(u)), u from CBRNG(v, seed)."""
+    v = np.ascontiguousarray(v, dtype=np.uint32)
+    s = np.ascontiguousarray(np.broadcast_to(np.asarray(seed, dtype=np.uint64), v.shape))
+    out = np.empty(v.shape, dtype=np.float32)
+    lib().oracle_gumbel_many(_ptr(v), _ptr(s), v.size, _ptr(out))
+    return out
+
+
+def watermark_sample(logits: np.ndarray, context, key: int, gamma: float, delta: float,
+                     seeding, seeds, inv_temperature: float = 1.0):
+    """Gumbel-max draw from softmax(watermarked logits * inv_temperature), one per row:
+    (tokens int32 [B], scores float32 [B]); seeds uint64 [B] drive the noise.  Ties,
+    NaN and signed zeros follow watermark_argmax."""
+    x = np.ascontiguousarray(logits)
+    B, V = x.shape
+    c = _context(context, B)
+    sd = np.ascontiguousarray(seeds, dtype=np.uint64)
+    if sd.shape != (B,):
+        raise ValueError("seeds must be uint64 [B]")
+    tokens = np.empty(B, dtype=np.int32)
+    scores = np.empty(B, dtype=np.float32)
+    if x.dtype == np.float32:
+        fn = lib().oracle_watermark_sample_f32_w
+    elif x.dtype == np.uint16:
+        fn = lib().oracle_watermark_sample_bf16_w
+    else:
+        raise TypeError("logits must be float32 or uint16 (bf16 bits)")
+    fn(_ptr(x), B, V, V, _ptr(c), c.shape[1], key, float(gamma), float(delta), _seeding(seeding),
+       _ptr(sd), float(inv_temperature), _ptr(tokens), _ptr(scores))
+    return tokens, scores

@@ -575,3 +575,97 @@ void oracle_detect_ex(const int32_t *tokens, int64_t N, int64_t L, int64_t row_s
         z[n] = oracle_z_score(green, T, gamma);
     }
 }
+
+/* ------------------------------------------------------------------------- */
+/* Sampling from the watermarked distribution by the Gumbel-max trick: the    */
+/* token argmax_v (l'_v / T + G_v) with G_v i.i.d. standard Gumbel is a draw  */
+/* from softmax(l' / T), l' the watermarked logits of Eq. 2.  G_v is derived  */
+/* from a caller-given seed per row through the same counter-based stream as  */
+/* the watermark: u = ((CBRNG(v, seed) >> 9) + 1/2) * 2^-23, exact in fp32   */
+/* and strictly inside (0, 1), G = -log(-log(u)).                             */
+/*                                                                            */
+/* The logarithm is computed from fp32 adds, multiplies and one divide, each  */
+/* rounded once, in a fixed order, so every IEEE-754 implementation returns   */
+/* the same bits: x = 2^e m with m in [sqrt(1/2), sqrt(2)), s = (m-1)/(m+1),  */
+/* log m = 2 (s + s^3/3 + s^5/5 + s^7/7 + s^9/9) (the atanh series; |s| <=    */
+/* 0.172, so the next term is below 2^-30), log x = e ln 2 + log m.  Valid    */
+/* for finite normal x > 0, which is all it is given here.                    */
+/* ------------------------------------------------------------------------- */
+
+float oracle_sample_log(float x)
+{
+    uint32_t b = bits_from_f32(x);
+    int e = (int)((b >> 23) & 0xFFu) - 127;
+    float m = f32_from_bits((b & 0x007FFFFFu) | 0x3F800000u);    /* [1, 2) */
+    if (m > 1.41421356f) {       /* to [sqrt(1/2), sqrt(2)): halving is exact */
+        m = m * 0.5f;
+        e = e + 1;
+    }
+    float s = (m - 1.0f) / (m + 1.0f);
+    float s2 = s * s;
+    float poly = 1.0f / 9.0f;
+    poly = 1.0f / 7.0f + s2 * poly;
+    poly = 1.0f / 5.0f + s2 * poly;
+    poly = 1.0f / 3.0f + s2 * poly;
+    poly = s + (s * s2) * poly;
+    return (float)e * 0.693147180559945309f + 2.0f * poly;
+}
+
+float oracle_gumbel(uint32_t v, uint64_t seed)
+{
+    uint32_t x = oracle_cbrng(v, seed);
+    float u = ((float)(x >> 9) + 0.5f) * 1.1920928955078125e-7f;   /* 2^-23 */
+    return -oracle_sample_log(-oracle_sample_log(u));
+}
+
+void oracle_watermark_sample_f32_w(const float *logits, int64_t B, int64_t V, int64_t row_stride,
+                                   const int32_t *context, int64_t width, uint64_t key,
+                                   double gamma, float delta, int seeding, const uint64_t *seeds,
+                                   float inv_temperature, int32_t *tokens, float *scores)
+{
+    uint64_t threshold = oracle_threshold(gamma);
+    for (int64_t b = 0; b < B; ++b) {
+        float best = 0.0f; int64_t best_v = -1; int best_nan = 0;
+        for (int64_t v = 0; v < V; ++v) {
+            float l = logits[b * row_stride + v];
+            if (oracle_is_green_w(key, context + b * width, width, (uint32_t)v, threshold, seeding))
+                l = oracle_bias_f32(l, delta);
+            float score = l * inv_temperature + oracle_gumbel((uint32_t)v, seeds[b]);
+            argmax_update(score, v, &best, &best_v, &best_nan);
+        }
+        tokens[b] = (int32_t)best_v;
+        scores[b] = best;
+    }
+}
+
+void oracle_watermark_sample_bf16_w(const uint16_t *logits, int64_t B, int64_t V,
+                                    int64_t row_stride, const int32_t *context, int64_t width,
+                                    uint64_t key, double gamma, float delta, int seeding,
+                                    const uint64_t *seeds, float inv_temperature, int32_t *tokens,
+                                    float *scores)
+{
+    uint64_t threshold = oracle_threshold(gamma);
+    for (int64_t b = 0; b < B; ++b) {
+        float best = 0.0f; int64_t best_v = -1; int best_nan = 0;
+        for (int64_t v = 0; v < V; ++v) {
+            uint16_t l = logits[b * row_stride + v];
+            if (oracle_is_green_w(key, context + b * width, width, (uint32_t)v, threshold, seeding))
+                l = oracle_bias_bf16(l, delta);
+            float score = f32_from_bits((uint32_t)l << 16) * inv_temperature +
+                          oracle_gumbel((uint32_t)v, seeds[b]);
+            argmax_update(score, v, &best, &best_v, &best_nan);
+        }
+        tokens[b] = (int32_t)best_v;
+        scores[b] = best;
+    }
+}
+
+void oracle_sample_log_many(const float *x, int64_t n, float *out)
+{
+    for (int64_t i = 0; i < n; ++i) out[i] = oracle_sample_log(x[i]);
+}
+
+void oracle_gumbel_many(const uint32_t *v, const uint64_t *seed, int64_t n, float *out)
+{
+    for (int64_t i = 0; i < n; ++i) out[i] = oracle_gumbel(v[i], seed[i]);
+}
