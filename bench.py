@@ -225,6 +225,24 @@ def other_configs(torch, sbw, dev, steps, c5_tokens):
     res["c4_watermark_argmax"] = fused
     del bufs
 
+    # sampling fused with the watermark on the c4 batch: one Gumbel-max draw per row
+    c = workloads.C4
+    x, prev = workloads.watermark_inputs("c4")
+    bufs, p = rotating(x), torch.from_numpy(prev).to(dev)
+    n = c["B"] * c["V"]
+    tokens = torch.empty(c["B"], dtype=torch.int32, device=dev)
+    scores = torch.empty(c["B"], dtype=torch.float32, device=dev)
+    ws = torch.empty(sbw.argmax_workspace_size(c["B"], c["V"]), dtype=torch.int64, device=dev)
+    seeds = torch.arange(1, c["B"] + 1, dtype=torch.int64, device=dev)
+    sampled = {}
+    for seeding in ("context", "self_salt"):
+        us = _mean_us(torch, lambda i, s=seeding: sbw.watermark_sample(
+            bufs[i % len(bufs)], p, key, c["gamma"], c["delta"], seeds, s, 1.0, tokens=tokens,
+            scores=scores, workspace=ws), steps)
+        sampled[seeding] = {"us": us, "gelem_per_s": n / us / 1e3}
+    res["c4_watermark_sample"] = sampled
+    del bufs
+
     # SBW-ss on the c4 batch: the self-salt watermark (width 4) on the top-40 ids only
     c = workloads.C4
     x, _ = workloads.watermark_inputs("c4")

@@ -12,6 +12,7 @@
  *              one write per logit.
  *   watermark_argmax     greedy decoding fused with the watermark: the index of
  *              the largest watermarked logit per row, the logits read once.
+ *   watermark_sample     sampling fused with the watermark (Gumbel-max).
  *   watermark_candidates the watermark on caller-given candidate ids only (the
  *              top-k self-salt scheme of Sec. 4).
  *   green_mask the green lists as bit sets (a parity and debugging aid).
@@ -259,6 +260,34 @@ sbw_status_t sbw_watermark_argmax(const void *logits, sbw_dtype_t dtype, int64_t
                                   uint64_t key, double gamma, float delta, sbw_seeding_t seeding,
                                   int32_t *tokens, float *values, uint64_t *workspace,
                                   void *stream);
+
+/*
+ * sbw_watermark_sample -- sampling fused with the watermark: for every row, one draw
+ * from softmax(l' * inv_temperature), l' the watermarked logits (Eq. 2), by the
+ * Gumbel-max trick: the token maximising l'_v * inv_temperature + G_v, with the
+ * noise G_v = -log(-log(u_v)), u_v = ((CBRNG(v, seeds[b]) >> 9) + 1/2) * 2^-23 (the
+ * watermark's counter-based stream keyed by the row's seed).  The logarithm is the
+ * atanh series on the reduced mantissa in fp32 adds, multiplies and one divide, in a
+ * fixed order, so the draw is reproducible bit for bit (a decoding epilogue of the
+ * logits processor, Sec. 5.1; the paper leaves sampling to the serving stack).
+ *
+ *   logits, dtype, B, V, row_stride, context, width, key, gamma, delta, seeding
+ *                as for sbw_watermark_argmax (logits only read).
+ *   seeds        device, [B] uint64: the noise seed of each row; draws with equal
+ *                seeds and inputs are equal.
+ *   inv_temperature  1/T, finite and > 0 (else SBW_ERR_INVALID_ARG).
+ *   tokens       device, [B] int32, written: the drawn token (ties and NaN as for
+ *                sbw_watermark_argmax; a NaN logit always wins).
+ *   scores       device, [B] float, written (may be NULL): the winning score
+ *                l'_v * inv_temperature + G_v.
+ *   workspace    as for sbw_watermark_argmax, same size.
+ * Enqueues two kernels on `stream` and no memset (graph-capturable).
+ */
+sbw_status_t sbw_watermark_sample(const void *logits, sbw_dtype_t dtype, int64_t B, int64_t V,
+                                  int64_t row_stride, const int32_t *context, int64_t width,
+                                  uint64_t key, double gamma, float delta, sbw_seeding_t seeding,
+                                  const uint64_t *seeds, float inv_temperature, int32_t *tokens,
+                                  float *scores, uint64_t *workspace, void *stream);
 
 /* Workspace size, in uint64 elements, that sbw_watermark_argmax needs for B rows of
  * V logits: B * ceil(V / 2048) (0 when B or V is not positive). */

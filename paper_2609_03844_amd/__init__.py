@@ -43,6 +43,7 @@ _STATUS = {
 EXPORTED = ("sbw_watermark", "sbw_green_mask", "sbw_detect", "sbw_watermark_window",
             "sbw_green_mask_window", "sbw_detect_window", "sbw_watermark_argmax",
             "sbw_watermark_argmax_workspace", "sbw_watermark_candidates", "sbw_detect_ex",
+            "sbw_watermark_sample",
             "sbw_strerror", "sbw_last_hip_error", "sbw_version")
 DETECT_IGNORE_REPEATED = 1
 MAX_UNIQUE_POSITIONS = 4096
@@ -83,6 +84,9 @@ def _load() -> ctypes.CDLL:
     lib.sbw_watermark_argmax.restype = i32
     lib.sbw_watermark_argmax.argtypes = [P, i32, i64, i64, i64, P, i64, u64, f64, f32, i32, P, P,
                                          P, P]
+    lib.sbw_watermark_sample.restype = i32
+    lib.sbw_watermark_sample.argtypes = [P, i32, i64, i64, i64, P, i64, u64, f64, f32, i32, P, f32,
+                                         P, P, P, P]
     lib.sbw_detect_ex.restype = i32
     lib.sbw_detect_ex.argtypes = [P, i64, i64, i64, P, i64, u64, f64, i32, ctypes.c_uint32, P, P,
                                   P, P]
@@ -276,6 +280,57 @@ def watermark_argmax(logits: torch.Tensor, prev_tokens: torch.Tensor, key: int, 
                                      values.data_ptr() if values is not None else None,
                                      workspace.data_ptr(), _stream(stream)))
     return tokens, values
+
+
+def watermark_sample(logits: torch.Tensor, prev_tokens: torch.Tensor, key: int, gamma: float,
+                     delta: float, seeds: torch.Tensor, seeding="context",
+                     inv_temperature: float = 1.0, tokens: torch.Tensor | None = None,
+                     scores: torch.Tensor | None = None, workspace: torch.Tensor | None = None,
+                     with_scores: bool = True, stream=None):
+    """One draw per row from softmax(watermarked logits * inv_temperature), fused
+    (Gumbel-max with noise from seeds, uint64 [B] as an int64 tensor).  Returns (tokens
+    int32 [B], scores float32 [B] or None); the workspace is as for watermark_argmax."""
+    if logits.dim() != 2:
+        raise ValueError("logits must be [B, V]")
+    if logits.dtype == torch.float32:
+        dtype = F32
+    elif logits.dtype == torch.bfloat16:
+        dtype = BF16
+    else:
+        raise TypeError("logits must be float32 or bfloat16")
+    B, V = logits.shape
+    if B > 0 and V > 0 and logits.stride(1) != 1:
+        raise ValueError("logits must have unit stride along the vocabulary")
+    if seeds.shape != (B,) or seeds.dtype not in (torch.int64, torch.uint64) or not seeds.is_contiguous():
+        raise ValueError("seeds must be contiguous 64-bit integers [B]")
+    context, width = _window(prev_tokens, B)
+    dev = logits.device
+    if tokens is None:
+        tokens = torch.empty(B, dtype=torch.int32, device=dev)
+    if scores is None and with_scores:
+        scores = torch.empty(B, dtype=torch.float32, device=dev)
+    need = argmax_workspace_size(B, V)
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.int64, device=dev)
+    if tokens.shape != (B,) or tokens.dtype != torch.int32 or not tokens.is_contiguous():
+        raise ValueError("tokens must be contiguous int32 [B]")
+    if (workspace.dtype != torch.int64 or not workspace.is_contiguous()
+            or workspace.numel() < need):
+        raise ValueError(f"workspace must be contiguous int64 with >= {need} elements")
+    if scores is not None and (scores.shape != (B,) or scores.dtype != torch.float32
+                               or not scores.is_contiguous()):
+        raise ValueError("scores must be contiguous float32 [B]")
+    row_stride = logits.stride(0) if B > 1 else max(V, logits.stride(0))
+    seed_kind = _seeding(seeding)
+    _on_device(logits=logits, prev_tokens=context, seeds=seeds, tokens=tokens, scores=scores,
+               workspace=workspace)
+    _check(_lib.sbw_watermark_sample(logits.data_ptr(), dtype, B, V, row_stride,
+                                     context.data_ptr(), width, _key(key), float(gamma),
+                                     float(delta), seed_kind, seeds.data_ptr(),
+                                     float(inv_temperature), tokens.data_ptr(),
+                                     scores.data_ptr() if scores is not None else None,
+                                     workspace.data_ptr(), _stream(stream)))
+    return tokens, scores
 
 
 def argmax_workspace_size(B: int, V: int) -> int:

@@ -18,10 +18,12 @@ HIPCC_FLAGS = [
     "-std=c++17",
     "-fPIC",
     "-shared",
-    # bit-exact arithmetic: no FMA contraction, no fast-math, fp32 denormals kept
+    # bit-exact arithmetic: no FMA contraction, no fast-math, fp32 denormals kept,
+    # IEEE-rounded fp32 divide (the sampler's logarithm divides once)
     "-ffp-contract=off",
     "-fno-fast-math",
     "-fno-gpu-flush-denormals-to-zero",
+    "-fhip-fp32-correctly-rounded-divide-sqrt",
     # packed fp32 VALU ops stay off
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-Wall",

@@ -144,4 +144,39 @@ __device__ __forceinline__ uint16_t bias_bf16(uint16_t l, float delta, bool gree
   return static_cast<uint16_t>(bias_bf16x2(l, delta, green, false));
 }
 
+// ---------------------------------------------------------------------------
+// Gumbel noise for sampling.  u = ((x >> 9) + 1/2) * 2^-23 (exact, inside (0, 1))
+// from a 32-bit draw x, G = -log(-log u).  The logarithm takes x = 2^e m with m in
+// [sqrt(1/2), sqrt(2)), s = (m-1)/(m+1), log m = 2 (s + s^3/3 + s^5/5 + s^7/7 + s^9/9)
+// (the atanh series) and e ln 2 + log m: fp32 adds, multiplies and one IEEE divide
+// in a fixed order, with contraction off, so the result is the same bits on any
+// IEEE-754 implementation.  Finite normal arguments only (all it is given).
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ float sample_log(float x) {
+  const uint32_t b = __float_as_uint(x);
+  int e = static_cast<int>((b >> 23) & 0xFFu) - 127;
+  float m = __uint_as_float((b & 0x007FFFFFu) | 0x3F800000u);
+  if (m > 1.41421356f) {
+    m = m * 0.5f;
+    e = e + 1;
+  }
+  const float s = (m - 1.0f) / (m + 1.0f);
+  const float s2 = s * s;
+  float poly = 1.0f / 9.0f;
+  poly = 1.0f / 7.0f + s2 * poly;
+  poly = 1.0f / 5.0f + s2 * poly;
+  poly = 1.0f / 3.0f + s2 * poly;
+  poly = s + (s * s2) * poly;
+  return static_cast<float>(e) * 0.693147180559945309f + 2.0f * poly;
+}
+
+__device__ __forceinline__ float gumbel_of(uint32_t x) {
+  const float u = (static_cast<float>(x >> 9) + 0.5f) * 1.1920928955078125e-7f;  // 2^-23
+  return -sample_log(-sample_log(u));
+}
+
+// Bounds of gumbel_of over all 2^23 values of u: (-2.81, 16.64), taken loosely.
+constexpr float kGumbelLo = -3.0f;
+constexpr float kGumbelHi = 17.0f;
+
 }  // namespace sbw

@@ -518,19 +518,85 @@ __device__ __forceinline__ void green_values(u32x4 o, float delta, float (&x)[8]
   }
 }
 
-template <typename VecT, int kW>
+// What a pass maximises: the watermarked logit (greedy decoding), or, for sampling,
+// that logit times 1/T plus the token's Gumbel noise (the Gumbel-max trick).  The
+// bounds transform the skip test's logit bounds the same way, with the noise's
+// range; both are non-decreasing in the logit, so the test stays exact.
+template <bool kSample>
+struct Score {
+  uint64_t seed;    // sampling: the row's noise seed
+  float inv_t;      // sampling: 1 / temperature
+  __device__ __forceinline__ float of(float l, uint32_t v) const {
+    if constexpr (kSample) return l * inv_t + gumbel_of(cbrng(v, seed));
+    return l;
+  }
+  __device__ __forceinline__ float upper(float l) const {
+    if constexpr (kSample) return l * inv_t + kGumbelHi;
+    return l;
+  }
+  __device__ __forceinline__ float lower(float l) const {
+    if constexpr (kSample) return l * inv_t + kGumbelLo;
+    return l;
+  }
+};
+
+template <bool kSample, typename VecT, int kW>
 __device__ __forceinline__ void scan_self_salt(LaneBest& b, VecT o, uint32_t j, const RowSeed<kW>& rs,
-                                               uint32_t tm1, int none_green, float delta, float lb) {
+                                               uint32_t tm1, int none_green, float delta, float lb,
+                                               const Score<kSample>& sc) {
   constexpr int kE = std::is_same<VecT, f32x4>::value ? 4 : 8;
   float x[kE], gv[kE];
   green_values(o, delta, x, gv);
 #pragma unroll
   for (int e = 0; e < kE; ++e) {
-    if (!(static_cast<bool>(static_cast<int>(x[e] < lb) & static_cast<int>(gv[e] < lb)))) {
+    if (!(static_cast<bool>(static_cast<int>(sc.upper(x[e]) < lb) &
+                            static_cast<int>(sc.upper(gv[e]) < lb)))) {
       const uint32_t v = j * kE + e;
       const bool g = !none_green && is_green(draw<kSelfSalt>(rs, v), tm1);
-      consider(b, g ? gv[e] : x[e], v);
+      consider(b, sc.of(g ? gv[e] : x[e], v), v);
     }
+  }
+}
+
+// Sampling under context seeding: whether any element may reach lb, and the scores
+// of a watermarked vector with one noise block per 4 tokens (the same counter
+// layout as the watermark's).
+template <typename VecT>
+__device__ __forceinline__ bool may_reach_sample(VecT o, float delta, float lb,
+                                                 const Score<true>& sc) {
+  constexpr int kE = std::is_same<VecT, f32x4>::value ? 4 : 8;
+  float x[kE], gv[kE];
+  green_values(o, delta, x, gv);
+  int below = 1;
+#pragma unroll
+  for (int e = 0; e < kE; ++e)
+    below &= static_cast<int>(sc.upper(x[e]) < lb) & static_cast<int>(sc.upper(gv[e]) < lb);
+  return !below;
+}
+
+__device__ __forceinline__ void consider_sample(LaneBest& b, f32x4 wm, uint32_t j,
+                                                const Score<true>& sc) {
+  const Block n = philox_block(j, key_of(sc.seed));
+  const uint32_t v = j * 4u;
+  consider(b, wm.x * sc.inv_t + gumbel_of(n.w0), v);
+  consider(b, wm.y * sc.inv_t + gumbel_of(n.w1), v + 1u);
+  consider(b, wm.z * sc.inv_t + gumbel_of(n.w2), v + 2u);
+  consider(b, wm.w * sc.inv_t + gumbel_of(n.w3), v + 3u);
+}
+
+__device__ __forceinline__ void consider_sample(LaneBest& b, u32x4 wm, uint32_t j,
+                                                const Score<true>& sc) {
+  const Key k = key_of(sc.seed);
+  const Block n0 = philox_block(2u * j, k);
+  const Block n1 = philox_block(2u * j + 1u, k);
+  const uint32_t x[8] = {n0.w0, n0.w1, n0.w2, n0.w3, n1.w0, n1.w1, n1.w2, n1.w3};
+  const uint32_t w[4] = {wm.x, wm.y, wm.z, wm.w};
+  const uint32_t v = j * 8u;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    consider(b, __uint_as_float(w[q] << 16) * sc.inv_t + gumbel_of(x[2 * q]), v + 2u * q);
+    consider(b, __uint_as_float(w[q] & 0xFFFF0000u) * sc.inv_t + gumbel_of(x[2 * q + 1]),
+             v + 2u * q + 1u);
   }
 }
 
@@ -540,11 +606,12 @@ __device__ __forceinline__ void scan_self_salt(LaneBest& b, VecT o, uint32_t j, 
 // updates its running argmax only for the vectors that may reach lb, in increasing
 // index order (self-salt: the elements that may).  The skipped elements cannot be
 // the segment's maximum, so the partial is the same as that of a full scan.
-template <typename T, int kSeeding, int kN, int kW>
+template <typename T, int kSeeding, int kN, int kW, bool kSample>
 __global__ void __launch_bounds__(kThreads)
 argmax_vec_kernel(const T* __restrict__ logits, int64_t row_stride, uint32_t V, int64_t B,
                   const int32_t* __restrict__ context, int width, uint64_t key, uint32_t tm1,
-                  int none_green, float delta, uint32_t segments, uint64_t* __restrict__ partials) {
+                  int none_green, float delta, const uint64_t* __restrict__ seeds, float inv_t,
+                  uint32_t segments, uint64_t* __restrict__ partials) {
   using VecT = typename std::conditional<sizeof(T) == 4, f32x4, u32x4>::type;
   __shared__ uint64_t lds_key[kThreads / 64], lds_part[kThreads / 64];
   constexpr uint32_t kPer = 16u / sizeof(T);
@@ -581,17 +648,23 @@ argmax_vec_kernel(const T* __restrict__ logits, int64_t row_stride, uint32_t V, 
     }
 #pragma unroll
     for (int off = 32; off >= 1; off >>= 1) m = fmaxf(m, __shfl_xor(m, off, 64));
-    const float lb = reach_bound(m, delta, T{});
+    const Score<kSample> sc{kSample ? seeds[row] : 0u, inv_t};
+    const float lb = sc.lower(reach_bound(m, delta, T{}));
     const RowSeed<kW> rs = row_seed<kSeeding, kW>(key, context + row * width, width);
     LaneBest lb_lane = lane_best_init();
 #pragma unroll
     for (int n = 0; n < kN; ++n) {
       const uint32_t j = seg_first + n * kThreads + threadIdx.x;
       if (!(whole || j < full)) continue;
-      if constexpr (kSeeding == kSelfSalt)
-        scan_self_salt(lb_lane, buf[n], j, rs, tm1, none_green, delta, lb);
-      else if (may_reach(buf[n], dplus, delta, lb))
+      if constexpr (kSeeding == kSelfSalt) {
+        scan_self_salt(lb_lane, buf[n], j, rs, tm1, none_green, delta, lb, sc);
+      } else if constexpr (kSample) {
+        if (may_reach_sample(buf[n], delta, lb, sc))
+          consider_sample(lb_lane, none_green ? buf[n] : bias_vec_context(buf[n], j, rs.seed, tm1, delta),
+                          j, sc);
+      } else if (may_reach(buf[n], dplus, delta, lb)) {
         consider_vec(lb_lane, none_green ? buf[n] : bias_vec_context(buf[n], j, rs.seed, tm1, delta), j);
+      }
     }
     // The row's partial last vector, element by element, by lane 0 of the segment
     // that holds it (never skipped).
@@ -599,7 +672,7 @@ argmax_vec_kernel(const T* __restrict__ logits, int64_t row_stride, uint32_t V, 
       for (uint32_t e = 0; e < tail; ++e) {
         const uint32_t v = full * kPer + e;
         const bool g = !none_green && is_green(draw<kSeeding>(rs, v), tm1);
-        consider(lb_lane, widen(bias_elem(row_ptr[v], delta, g)), v);
+        consider(lb_lane, sc.of(widen(bias_elem(row_ptr[v], delta, g)), v), v);
       }
     }
     block_argmax_store(lb_lane, partials + row * segments + blockIdx.x, lds_key, lds_part);
@@ -608,22 +681,24 @@ argmax_vec_kernel(const T* __restrict__ logits, int64_t row_stride, uint32_t V, 
 
 // Rows that are not 16-byte aligned: one element per thread per step, a segment of
 // kArgmaxSegElems elements per workgroup.
-template <typename T, int kSeeding, int kW>
+template <typename T, int kSeeding, int kW, bool kSample>
 __global__ void __launch_bounds__(kThreads)
 argmax_elem_kernel(const T* __restrict__ logits, int64_t row_stride, uint32_t V, int64_t B,
                    const int32_t* __restrict__ context, int width, uint64_t key, uint32_t tm1,
-                   int none_green, float delta, uint32_t segments, uint64_t* __restrict__ partials) {
+                   int none_green, float delta, const uint64_t* __restrict__ seeds, float inv_t,
+                   uint32_t segments, uint64_t* __restrict__ partials) {
   __shared__ uint64_t lds_key[kThreads / 64], lds_part[kThreads / 64];
   const uint64_t seg_first = static_cast<uint64_t>(blockIdx.x) * kArgmaxSegElems;
   for (int64_t row = blockIdx.y; row < B; row += gridDim.y) {
     const RowSeed<kW> rs = row_seed<kSeeding, kW>(key, context + row * width, width);
+    const Score<kSample> sc{kSample ? seeds[row] : 0u, inv_t};
     LaneBest lb = lane_best_init();
     for (int s = 0; s < kElemSegSteps; ++s) {
       const uint64_t v64 = seg_first + static_cast<uint64_t>(s) * kThreads + threadIdx.x;
       if (v64 < V) {
         const uint32_t v = static_cast<uint32_t>(v64);
         const bool g = !none_green && is_green(draw<kSeeding>(rs, v), tm1);
-        consider(lb, widen(bias_elem(logits[row * row_stride + v], delta, g)), v);
+        consider(lb, sc.of(widen(bias_elem(logits[row * row_stride + v], delta, g)), v), v);
       }
     }
     block_argmax_store(lb, partials + row * segments + blockIdx.x, lds_key, lds_part);
@@ -1067,11 +1142,17 @@ static_assert(vec_segment_elems<float>(SBW_ARGMAX_VECS_CONTEXT) >= kArgmaxSegEle
                   vec_segment_elems<float>(SBW_ARGMAX_VECS_SELF_SALT) >= kArgmaxSegElems,
               "vector segments must not outnumber element segments");
 
-template <typename T, int kSeeding, int kW>
+// The per-row noise seeds and 1/T of a sampling pass (unused by greedy decoding).
+struct SampleArgs {
+  const uint64_t* seeds;
+  float inv_t;
+};
+
+template <typename T, int kSeeding, int kW, bool kSample>
 void launch_argmax(const void* logits, int64_t B, uint32_t V, int64_t row_stride,
                    const int32_t* context, int width, uint64_t key, uint32_t tm1, int none,
-                   float delta, bool aligned, int32_t* tokens, float* values, uint64_t* partials,
-                   hipStream_t stream) {
+                   float delta, const SampleArgs& sa, bool aligned, int32_t* tokens, float* values,
+                   uint64_t* partials, hipStream_t stream) {
   const T* p = static_cast<const T*>(logits);
   const uint32_t rows = static_cast<uint32_t>(B < kMaxGridY ? B : kMaxGridY);
   uint32_t segments;
@@ -1079,35 +1160,37 @@ void launch_argmax(const void* logits, int64_t B, uint32_t V, int64_t row_stride
     constexpr int kN = argmax_vecs_for<kSeeding>();
     const uint64_t seg = vec_segment_elems<T>(kN);
     segments = static_cast<uint32_t>((static_cast<uint64_t>(V) + seg - 1) / seg);
-    hipLaunchKernelGGL((argmax_vec_kernel<T, kSeeding, kN, kW>), dim3(segments, rows),
+    hipLaunchKernelGGL((argmax_vec_kernel<T, kSeeding, kN, kW, kSample>), dim3(segments, rows),
                        dim3(kThreads), 0, stream, p, row_stride, V, B, context, width, key, tm1,
-                       none, delta, segments, partials);
+                       none, delta, sa.seeds, sa.inv_t, segments, partials);
   } else {
     segments = static_cast<uint32_t>((static_cast<uint64_t>(V) + kArgmaxSegElems - 1) /
                                      kArgmaxSegElems);
-    hipLaunchKernelGGL((argmax_elem_kernel<T, kSeeding, kW>), dim3(segments, rows), dim3(kThreads),
-                       0, stream, p, row_stride, V, B, context, width, key, tm1, none, delta,
-                       segments, partials);
+    hipLaunchKernelGGL((argmax_elem_kernel<T, kSeeding, kW, kSample>), dim3(segments, rows),
+                       dim3(kThreads), 0, stream, p, row_stride, V, B, context, width, key, tm1,
+                       none, delta, sa.seeds, sa.inv_t, segments, partials);
   }
   const int64_t row_blocks = grid_for((B + kThreads / 64 - 1) / (kThreads / 64));
   hipLaunchKernelGGL(argmax_finish_kernel, dim3(row_blocks), dim3(kThreads), 0, stream, partials,
                      segments, B, tokens, values);
 }
 
-template <typename T>
+template <typename T, bool kSample>
 void dispatch_argmax(const void* logits, int64_t B, uint32_t V, int64_t row_stride,
                      const int32_t* context, int width, uint64_t key, uint32_t tm1, int none,
-                     float delta, sbw_seeding_t seeding, bool aligned, int32_t* tokens,
-                     float* values, uint64_t* best, hipStream_t st) {
+                     float delta, const SampleArgs& sa, sbw_seeding_t seeding, bool aligned,
+                     int32_t* tokens, float* values, uint64_t* partials, hipStream_t st) {
   if (seeding == SBW_SEED_CONTEXT)
-    launch_argmax<T, kContext, kMaxWidth>(logits, B, V, row_stride, context, width, key, tm1,
-                                          none, delta, aligned, tokens, values, best, st);
+    launch_argmax<T, kContext, kMaxWidth, kSample>(logits, B, V, row_stride, context, width, key,
+                                                   tm1, none, delta, sa, aligned, tokens, values,
+                                                   partials, st);
   else if (width == 1)
-    launch_argmax<T, kSelfSalt, 1>(logits, B, V, row_stride, context, width, key, tm1, none,
-                                   delta, aligned, tokens, values, best, st);
+    launch_argmax<T, kSelfSalt, 1, kSample>(logits, B, V, row_stride, context, width, key, tm1,
+                                            none, delta, sa, aligned, tokens, values, partials, st);
   else
-    launch_argmax<T, kSelfSalt, kMaxWidth>(logits, B, V, row_stride, context, width, key, tm1,
-                                           none, delta, aligned, tokens, values, best, st);
+    launch_argmax<T, kSelfSalt, kMaxWidth, kSample>(logits, B, V, row_stride, context, width, key,
+                                                    tm1, none, delta, sa, aligned, tokens, values,
+                                                    partials, st);
 }
 
 template <int kSeeding, int kW>
@@ -1186,6 +1269,48 @@ sbw_status_t detect_impl(const int32_t* tokens, int64_t N, int64_t L, int64_t ro
     if (ctx) launch_detect<kContext, kMaxWidth>(positions, blocks, st, tokens, N, L, row_stride, w, key, tm1, gamma, io);
     else launch_detect<kSelfSalt, kMaxWidth>(positions, blocks, st, tokens, N, L, row_stride, w, key, tm1, gamma, io);
   }
+  return after_launch();
+}
+
+// Greedy decoding and sampling: validation, then the segment pass and the read-out.
+template <bool kSample>
+sbw_status_t decode_impl(const void* logits, sbw_dtype_t dtype, int64_t B, int64_t V,
+                         int64_t row_stride, const int32_t* context, int64_t width, uint64_t key,
+                         double gamma, float delta, sbw_seeding_t seeding, const SampleArgs& sa,
+                         int32_t* tokens, float* values, uint64_t* workspace, void* stream) {
+  if (B < 0 || V < 0 || row_stride < V) return SBW_ERR_INVALID_ARG;
+  sbw_status_t s = check_width(width);
+  if (s != SBW_OK) return s;
+  if (dtype != SBW_F32 && dtype != SBW_BF16) return SBW_ERR_UNSUPPORTED;
+  if (!valid_seeding(seeding)) return SBW_ERR_UNSUPPORTED;
+  if (!(gamma >= 0.0 && gamma <= 1.0)) return SBW_ERR_GAMMA;
+  if (!isfinite(delta)) return SBW_ERR_DELTA;
+  if (V >= (int64_t{1} << 32)) return SBW_ERR_UNSUPPORTED;
+  if (B == 0) return SBW_OK;
+  if (V == 0) return SBW_ERR_INVALID_ARG;  // no token to choose
+  if (logits == nullptr || context == nullptr || tokens == nullptr || workspace == nullptr)
+    return SBW_ERR_INVALID_ARG;
+  if (B > INT64_MAX / 4 / row_stride) return SBW_ERR_UNSUPPORTED;
+  s = check_device();
+  if (s != SBW_OK) return s;
+
+  // gamma == 0: nothing is green, every logit (and the value returned) is unchanged.
+  const uint64_t T = threshold_of(gamma);
+  const int none = T == 0 ? 1 : 0;
+  const uint32_t tm1 = none ? 0u : static_cast<uint32_t>(T - 1);
+  const float d = delta;
+  const size_t esize = dtype == SBW_F32 ? 4 : 2;
+  const bool aligned = (reinterpret_cast<uintptr_t>(logits) % 16 == 0) &&
+                       ((static_cast<uint64_t>(row_stride) * esize) % 16 == 0);
+  const uint32_t v32 = static_cast<uint32_t>(V);
+  const int w = static_cast<int>(width);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if (dtype == SBW_F32)
+    dispatch_argmax<float, kSample>(logits, B, v32, row_stride, context, w, key, tm1, none, d, sa,
+                                    seeding, aligned, tokens, values, workspace, st);
+  else
+    dispatch_argmax<uint16_t, kSample>(logits, B, v32, row_stride, context, w, key, tm1, none, d,
+                                       sa, seeding, aligned, tokens, values, workspace, st);
   return after_launch();
 }
 
@@ -1279,41 +1404,20 @@ sbw_status_t sbw_watermark_argmax(const void* logits, sbw_dtype_t dtype, int64_t
                                   uint64_t key, double gamma, float delta, sbw_seeding_t seeding,
                                   int32_t* tokens, float* values, uint64_t* workspace,
                                   void* stream) {
-  if (B < 0 || V < 0 || row_stride < V) return SBW_ERR_INVALID_ARG;
-  sbw_status_t s = check_width(width);
-  if (s != SBW_OK) return s;
-  if (dtype != SBW_F32 && dtype != SBW_BF16) return SBW_ERR_UNSUPPORTED;
-  if (!valid_seeding(seeding)) return SBW_ERR_UNSUPPORTED;
-  if (!(gamma >= 0.0 && gamma <= 1.0)) return SBW_ERR_GAMMA;
-  if (!isfinite(delta)) return SBW_ERR_DELTA;
-  if (V >= (int64_t{1} << 32)) return SBW_ERR_UNSUPPORTED;
-  if (B == 0) return SBW_OK;
-  if (V == 0) return SBW_ERR_INVALID_ARG;  // no token to choose
-  if (logits == nullptr || context == nullptr || tokens == nullptr || workspace == nullptr)
-    return SBW_ERR_INVALID_ARG;
-  if (B > INT64_MAX / 4 / row_stride) return SBW_ERR_UNSUPPORTED;
-  s = check_device();
-  if (s != SBW_OK) return s;
+  return decode_impl<false>(logits, dtype, B, V, row_stride, context, width, key, gamma, delta,
+                            seeding, SampleArgs{nullptr, 1.0f}, tokens, values, workspace, stream);
+}
 
-  // gamma == 0: nothing is green, every logit (and the value returned) is unchanged.
-  const uint64_t T = threshold_of(gamma);
-  const int none = T == 0 ? 1 : 0;
-  const uint32_t tm1 = none ? 0u : static_cast<uint32_t>(T - 1);
-  const float d = delta;
-  const size_t esize = dtype == SBW_F32 ? 4 : 2;
-  const bool aligned = (reinterpret_cast<uintptr_t>(logits) % 16 == 0) &&
-                       ((static_cast<uint64_t>(row_stride) * esize) % 16 == 0);
-  const uint32_t v32 = static_cast<uint32_t>(V);
-  const int w = static_cast<int>(width);
-  uint64_t* best = workspace;
-  hipStream_t st = static_cast<hipStream_t>(stream);
-  if (dtype == SBW_F32)
-    dispatch_argmax<float>(logits, B, v32, row_stride, context, w, key, tm1, none, d, seeding,
-                           aligned, tokens, values, best, st);
-  else
-    dispatch_argmax<uint16_t>(logits, B, v32, row_stride, context, w, key, tm1, none, d, seeding,
-                              aligned, tokens, values, best, st);
-  return after_launch();
+sbw_status_t sbw_watermark_sample(const void* logits, sbw_dtype_t dtype, int64_t B, int64_t V,
+                                  int64_t row_stride, const int32_t* context, int64_t width,
+                                  uint64_t key, double gamma, float delta, sbw_seeding_t seeding,
+                                  const uint64_t* seeds, float inv_temperature, int32_t* tokens,
+                                  float* scores, uint64_t* workspace, void* stream) {
+  if (!(isfinite(inv_temperature) && inv_temperature > 0.0f)) return SBW_ERR_INVALID_ARG;
+  if (B > 0 && V > 0 && seeds == nullptr) return SBW_ERR_INVALID_ARG;
+  return decode_impl<true>(logits, dtype, B, V, row_stride, context, width, key, gamma, delta,
+                           seeding, SampleArgs{seeds, inv_temperature}, tokens, scores, workspace,
+                           stream);
 }
 
 int64_t sbw_watermark_argmax_workspace(int64_t B, int64_t V) {

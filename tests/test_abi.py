@@ -40,7 +40,7 @@ def test_header_declares_the_boundary():
                            "sbw_green_mask_window", "sbw_last_hip_error", "sbw_strerror",
                            "sbw_version", "sbw_watermark", "sbw_watermark_argmax",
                            "sbw_watermark_argmax_workspace", "sbw_watermark_candidates",
-                           "sbw_watermark_window"]
+                           "sbw_watermark_sample", "sbw_watermark_window"]
 
 
 def test_library_exports_every_declared_symbol(sbw, lib):
@@ -341,3 +341,23 @@ def test_binding_rejects_tensors_off_the_device(sbw):
                    z=torch.zeros(2, dtype=torch.float64))
     with pytest.raises(ValueError, match="current HIP device"):
         sbw.detect_ex(tok, KEY, 0.25)
+
+
+def ws_(lib, logits=DUMMY, dtype=0, B=2, V=8, stride=8, context=DUMMY, width=1, gamma=0.25,
+        delta=2.0, seeding=0, seeds=DUMMY, inv_t=1.0, tokens=DUMMY, scores=DUMMY, workspace=DUMMY):
+    return lib.sbw_watermark_sample(logits, dtype, B, V, stride, context, width, KEY, gamma, delta,
+                                    seeding, seeds, inv_t, tokens, scores, workspace, None)
+
+
+def test_sample_rejects_bad_arguments(lib):
+    for inv_t in (0.0, -1.0, math.inf, math.nan):
+        assert ws_(lib, inv_t=inv_t) == INVALID, inv_t
+    for name in ("logits", "context", "seeds", "tokens", "workspace"):
+        assert ws_(lib, **{name: NULL}) == INVALID, name
+    assert ws_(lib, V=0, stride=0) == INVALID
+    assert ws_(lib, gamma=2.0) == GAMMA
+    assert ws_(lib, delta=math.inf) == DELTA
+    assert ws_(lib, seeding=7) == UNSUPPORTED
+    assert ws_(lib, B=0, seeds=NULL) == OK
+    if not _gpu_visible():
+        assert ws_(lib, scores=NULL) == NO_DEVICE
