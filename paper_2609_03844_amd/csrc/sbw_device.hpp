@@ -70,6 +70,49 @@ __device__ __forceinline__ uint32_t block_word(const Block& b, uint32_t i) {
   return (i & 2u) ? hi : lo;
 }
 
+// A copy of a wave-uniform key that the optimiser cannot see through.  Without it,
+// the 20 round keys of a stream drawn in a long unrolled loop are computed once and
+// kept live, which exhausts the scalar registers and spills them to vector lanes;
+// from the copy they are derived again, by scalar adds, next to their use.
+__device__ __forceinline__ Key opaque_key(Key k) {
+  asm volatile("" : "+s"(k.lo), "+s"(k.hi));
+  return k;
+}
+
+// The ten round keys of a Philox key, for a stream drawn many times with one key.
+// Held in vector registers (opaque to the optimiser), the rounds then take them as
+// operands instead of deriving them again with scalar adds for every block.
+struct RoundKeys {
+  uint32_t k0[10], k1[10];
+};
+
+__device__ __forceinline__ RoundKeys vector_round_keys(Key k) {
+  RoundKeys rk;
+#pragma unroll
+  for (int r = 0; r < 10; ++r) {
+    rk.k0[r] = k.lo + static_cast<uint32_t>(r) * kPhiloxWeyl0;
+    rk.k1[r] = k.hi + static_cast<uint32_t>(r) * kPhiloxWeyl1;
+    asm volatile("" : "+v"(rk.k0[r]), "+v"(rk.k1[r]));
+  }
+  return rk;
+}
+
+__device__ __forceinline__ Block philox_block(uint32_t c0, const RoundKeys& rk) {
+  uint32_t x0 = c0, x1 = 0u, x2 = 0u, x3 = 0u;
+#pragma unroll
+  for (int round = 0; round < 10; ++round) {
+    const uint64_t pa = wide_mul(kPhiloxMulA, x0);
+    const uint64_t pb = wide_mul(kPhiloxMulB, x2);
+    const uint32_t y0 = round == 0 ? rk.k0[0] : xor3(static_cast<uint32_t>(pb >> 32), x1, rk.k0[round]);
+    const uint32_t y1 = static_cast<uint32_t>(pb);
+    const uint32_t y2 = round == 0 ? static_cast<uint32_t>(pa >> 32) ^ rk.k1[0]
+                                   : xor3(static_cast<uint32_t>(pa >> 32), x3, rk.k1[round]);
+    const uint32_t y3 = static_cast<uint32_t>(pa);
+    x0 = y0; x1 = y1; x2 = y2; x3 = y3;
+  }
+  return Block{x0, x1, x2, x3};
+}
+
 // CBRNG(v, r): position v of the Philox stream keyed by r (Sec. 2.2).
 __device__ __forceinline__ uint32_t cbrng(uint32_t v, uint64_t r) {
   return block_word(philox_block(v >> 2, key_of(r)), v & 3u);
@@ -178,5 +221,28 @@ __device__ __forceinline__ float gumbel_of(uint32_t x) {
 // Bounds of gumbel_of over all 2^23 values of u: (-2.81, 16.64), taken loosely.
 constexpr float kGumbelLo = -3.0f;
 constexpr float kGumbelHi = 17.0f;
+
+// Bounds of gumbel_of from the leading one bits of the draw, for passes that skip
+// tokens whose noise cannot lift them to the best score.  With c the number of
+// leading ones of x, capped at 23, q = 1 - u = n 2^-24 for an odd n whose top bit
+// is bit 23 - c, so q lies in [2^-(c+1), 2^-c) (q = 2^-24 when c = 23).
+//  * Above: t = -log(1 - q) > q, so G = -log t < -log q <= (c + 1) ln 2.
+//  * Below, for c >= 2: G increases with u, so it exceeds its value at
+//    u = 1 - 2^-c, -log(-log(1 - 2^-c)) = c ln 2 - e(c) with e(2) = 0.1404 and e
+//    falling toward 0 as c grows; so G > gumbel_upper(c) - (ln 2 + margin + 0.1404).
+// The upper bound takes one fma; both hold, with room for the rounding of the fp32
+// logarithm, for every one of the 2^23 values of u.
+constexpr float kLn2f = 0.693147182f;                    // ln 2 rounded up
+constexpr float kGumbelMargin = 0.0009765625f;           // 2^-10
+constexpr float kGumbelUpperOffset = kLn2f + kGumbelMargin;
+constexpr float kGumbelGap = 0.8442f;                    // gumbel_upper(c) - G for c >= 2
+
+// c as a float.  ~x | 2^8 has at most 23 leading zeros, so no cap is needed.
+__device__ __forceinline__ float noise_ones(uint32_t x) {
+  return static_cast<float>(__builtin_clz(~x | 0x100u));
+}
+__device__ __forceinline__ float gumbel_upper(float c) {
+  return __builtin_fmaf(c, kLn2f, kGumbelUpperOffset);
+}
 
 }  // namespace sbw

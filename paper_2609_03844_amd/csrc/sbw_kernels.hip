@@ -358,6 +358,17 @@ watermark_elem_kernel(T* __restrict__ logits, int64_t row_stride, uint32_t V, in
 #ifndef SBW_ARGMAX_VECS_SELF_SALT
 #define SBW_ARGMAX_VECS_SELF_SALT 8
 #endif
+#ifndef SBW_SAMPLE_VECS_F32
+#define SBW_SAMPLE_VECS_F32 8
+#endif
+#ifndef SBW_SAMPLE_VECS_BF16
+#define SBW_SAMPLE_VECS_BF16 4
+#endif
+// Sub-batches of that many vectors per lane in a sampling segment: they share one
+// candidate queue per wave and one read-out.
+#ifndef SBW_SAMPLE_SUBS
+#define SBW_SAMPLE_SUBS 1
+#endif
 constexpr int kElemSegSteps = 8;                                // element kernel
 constexpr int64_t kArgmaxSegElems = kThreads * kElemSegSteps;   // element-kernel segment
 
@@ -388,6 +399,19 @@ __device__ __forceinline__ void consider(LaneBest& b, float x, uint32_t i) {
   // Bitwise, not short-circuit, operators keep the update branch-free.
   const bool take = static_cast<bool>(static_cast<int>(!b.any) | static_cast<int>(x > b.v) |
                                       (static_cast<int>(x != x) & static_cast<int>(b.v == b.v)));
+  b.v = take ? x : b.v;
+  b.i = take ? i : b.i;
+  b.any = true;
+}
+
+// The same argmax for a lane that sees its indices in any order: equal values and
+// NaNs go to the smaller index.
+__device__ __forceinline__ void consider_any_order(LaneBest& b, float x, uint32_t i) {
+  const int xn = static_cast<int>(x != x), bn = static_cast<int>(b.v != b.v);
+  const int first = static_cast<int>(i < b.i);
+  const bool take = static_cast<bool>(static_cast<int>(!b.any) | static_cast<int>(x > b.v) |
+                                      (static_cast<int>(x == b.v) & first) |
+                                      (xn & ((1 - bn) | first)));
   b.v = take ? x : b.v;
   b.i = take ? i : b.i;
   b.any = true;
@@ -519,9 +543,7 @@ __device__ __forceinline__ void green_values(u32x4 o, float delta, float (&x)[8]
 }
 
 // What a pass maximises: the watermarked logit (greedy decoding), or, for sampling,
-// that logit times 1/T plus the token's Gumbel noise (the Gumbel-max trick).  The
-// bounds transform the skip test's logit bounds the same way, with the noise's
-// range; both are non-decreasing in the logit, so the test stays exact.
+// that logit times 1/T plus the token's Gumbel noise (the Gumbel-max trick).
 template <bool kSample>
 struct Score {
   uint64_t seed;    // sampling: the row's noise seed
@@ -530,73 +552,21 @@ struct Score {
     if constexpr (kSample) return l * inv_t + gumbel_of(cbrng(v, seed));
     return l;
   }
-  __device__ __forceinline__ float upper(float l) const {
-    if constexpr (kSample) return l * inv_t + kGumbelHi;
-    return l;
-  }
-  __device__ __forceinline__ float lower(float l) const {
-    if constexpr (kSample) return l * inv_t + kGumbelLo;
-    return l;
-  }
 };
 
-template <bool kSample, typename VecT, int kW>
+template <typename VecT, int kW>
 __device__ __forceinline__ void scan_self_salt(LaneBest& b, VecT o, uint32_t j, const RowSeed<kW>& rs,
-                                               uint32_t tm1, int none_green, float delta, float lb,
-                                               const Score<kSample>& sc) {
+                                               uint32_t tm1, int none_green, float delta, float lb) {
   constexpr int kE = std::is_same<VecT, f32x4>::value ? 4 : 8;
   float x[kE], gv[kE];
   green_values(o, delta, x, gv);
 #pragma unroll
   for (int e = 0; e < kE; ++e) {
-    if (!(static_cast<bool>(static_cast<int>(sc.upper(x[e]) < lb) &
-                            static_cast<int>(sc.upper(gv[e]) < lb)))) {
+    if (!(static_cast<bool>(static_cast<int>(x[e] < lb) & static_cast<int>(gv[e] < lb)))) {
       const uint32_t v = j * kE + e;
       const bool g = !none_green && is_green(draw<kSelfSalt>(rs, v), tm1);
-      consider(b, sc.of(g ? gv[e] : x[e], v), v);
+      consider(b, g ? gv[e] : x[e], v);
     }
-  }
-}
-
-// Sampling under context seeding: whether any element may reach lb, and the scores
-// of a watermarked vector with one noise block per 4 tokens (the same counter
-// layout as the watermark's).
-template <typename VecT>
-__device__ __forceinline__ bool may_reach_sample(VecT o, float delta, float lb,
-                                                 const Score<true>& sc) {
-  constexpr int kE = std::is_same<VecT, f32x4>::value ? 4 : 8;
-  float x[kE], gv[kE];
-  green_values(o, delta, x, gv);
-  int below = 1;
-#pragma unroll
-  for (int e = 0; e < kE; ++e)
-    below &= static_cast<int>(sc.upper(x[e]) < lb) & static_cast<int>(sc.upper(gv[e]) < lb);
-  return !below;
-}
-
-__device__ __forceinline__ void consider_sample(LaneBest& b, f32x4 wm, uint32_t j,
-                                                const Score<true>& sc) {
-  const Block n = philox_block(j, key_of(sc.seed));
-  const uint32_t v = j * 4u;
-  consider(b, wm.x * sc.inv_t + gumbel_of(n.w0), v);
-  consider(b, wm.y * sc.inv_t + gumbel_of(n.w1), v + 1u);
-  consider(b, wm.z * sc.inv_t + gumbel_of(n.w2), v + 2u);
-  consider(b, wm.w * sc.inv_t + gumbel_of(n.w3), v + 3u);
-}
-
-__device__ __forceinline__ void consider_sample(LaneBest& b, u32x4 wm, uint32_t j,
-                                                const Score<true>& sc) {
-  const Key k = key_of(sc.seed);
-  const Block n0 = philox_block(2u * j, k);
-  const Block n1 = philox_block(2u * j + 1u, k);
-  const uint32_t x[8] = {n0.w0, n0.w1, n0.w2, n0.w3, n1.w0, n1.w1, n1.w2, n1.w3};
-  const uint32_t w[4] = {wm.x, wm.y, wm.z, wm.w};
-  const uint32_t v = j * 8u;
-#pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    consider(b, __uint_as_float(w[q] << 16) * sc.inv_t + gumbel_of(x[2 * q]), v + 2u * q);
-    consider(b, __uint_as_float(w[q] & 0xFFFF0000u) * sc.inv_t + gumbel_of(x[2 * q + 1]),
-             v + 2u * q + 1u);
   }
 }
 
@@ -606,12 +576,11 @@ __device__ __forceinline__ void consider_sample(LaneBest& b, u32x4 wm, uint32_t 
 // updates its running argmax only for the vectors that may reach lb, in increasing
 // index order (self-salt: the elements that may).  The skipped elements cannot be
 // the segment's maximum, so the partial is the same as that of a full scan.
-template <typename T, int kSeeding, int kN, int kW, bool kSample>
+template <typename T, int kSeeding, int kN, int kW>
 __global__ void __launch_bounds__(kThreads)
 argmax_vec_kernel(const T* __restrict__ logits, int64_t row_stride, uint32_t V, int64_t B,
                   const int32_t* __restrict__ context, int width, uint64_t key, uint32_t tm1,
-                  int none_green, float delta, const uint64_t* __restrict__ seeds, float inv_t,
-                  uint32_t segments, uint64_t* __restrict__ partials) {
+                  int none_green, float delta, uint32_t segments, uint64_t* __restrict__ partials) {
   using VecT = typename std::conditional<sizeof(T) == 4, f32x4, u32x4>::type;
   __shared__ uint64_t lds_key[kThreads / 64], lds_part[kThreads / 64];
   constexpr uint32_t kPer = 16u / sizeof(T);
@@ -648,8 +617,7 @@ argmax_vec_kernel(const T* __restrict__ logits, int64_t row_stride, uint32_t V, 
     }
 #pragma unroll
     for (int off = 32; off >= 1; off >>= 1) m = fmaxf(m, __shfl_xor(m, off, 64));
-    const Score<kSample> sc{kSample ? seeds[row] : 0u, inv_t};
-    const float lb = sc.lower(reach_bound(m, delta, T{}));
+    const float lb = reach_bound(m, delta, T{});
     const RowSeed<kW> rs = row_seed<kSeeding, kW>(key, context + row * width, width);
     LaneBest lb_lane = lane_best_init();
 #pragma unroll
@@ -657,11 +625,7 @@ argmax_vec_kernel(const T* __restrict__ logits, int64_t row_stride, uint32_t V, 
       const uint32_t j = seg_first + n * kThreads + threadIdx.x;
       if (!(whole || j < full)) continue;
       if constexpr (kSeeding == kSelfSalt) {
-        scan_self_salt(lb_lane, buf[n], j, rs, tm1, none_green, delta, lb, sc);
-      } else if constexpr (kSample) {
-        if (may_reach_sample(buf[n], delta, lb, sc))
-          consider_sample(lb_lane, none_green ? buf[n] : bias_vec_context(buf[n], j, rs.seed, tm1, delta),
-                          j, sc);
+        scan_self_salt(lb_lane, buf[n], j, rs, tm1, none_green, delta, lb);
       } else if (may_reach(buf[n], dplus, delta, lb)) {
         consider_vec(lb_lane, none_green ? buf[n] : bias_vec_context(buf[n], j, rs.seed, tm1, delta), j);
       }
@@ -672,10 +636,292 @@ argmax_vec_kernel(const T* __restrict__ logits, int64_t row_stride, uint32_t V, 
       for (uint32_t e = 0; e < tail; ++e) {
         const uint32_t v = full * kPer + e;
         const bool g = !none_green && is_green(draw<kSeeding>(rs, v), tm1);
-        consider(lb_lane, sc.of(widen(bias_elem(row_ptr[v], delta, g)), v), v);
+        consider(lb_lane, widen(bias_elem(row_ptr[v], delta, g)), v);
       }
     }
     block_argmax_store(lb_lane, partials + row * segments + blockIdx.x, lds_key, lds_part);
+  }
+}
+
+// Each token's larger candidate logit, max(x, bias(x)), times 1/T.  fp32: bias(x)
+// is x + delta rounded, so the larger one is x + max(delta, 0) (x + 0 only turns -0
+// into +0).  bf16: bias rounds to bf16, so both candidates are formed.
+__device__ __forceinline__ void upper_logits(f32x4 o, float, float dplus, float inv_t, float (&phi)[4]) {
+  phi[0] = (o.x + dplus) * inv_t;
+  phi[1] = (o.y + dplus) * inv_t;
+  phi[2] = (o.z + dplus) * inv_t;
+  phi[3] = (o.w + dplus) * inv_t;
+}
+__device__ __forceinline__ void upper_logits(u32x4 o, float delta, float, float inv_t, float (&phi)[8]) {
+  float x[8], gv[8];
+  green_values(o, delta, x, gv);
+#pragma unroll
+  for (int e = 0; e < 8; ++e) phi[e] = (delta >= 0.0f ? gv[e] : x[e]) * inv_t;
+}
+
+// Largest raw logit of a vector folded into m.  v_max3_f32 on the raw values: the
+// compiler's fmaxf would first canonicalise every loaded value.  A signalling NaN
+// may make m NaN, which only turns the skip test built on m off.
+__device__ __forceinline__ float max3_raw(float a, float b, float c) {
+  float r;
+  asm("v_max3_f32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
+  return r;
+}
+__device__ __forceinline__ float fold_max(f32x4 o, float m) {
+  return max3_raw(max3_raw(m, o.x, o.y), o.z, o.w);
+}
+__device__ __forceinline__ float fold_max(u32x4 o, float m) {
+  const uint32_t w[4] = {o.x, o.y, o.z, o.w};
+#pragma unroll
+  for (int q = 0; q < 4; ++q) m = max3_raw(m, __uint_as_float(w[q] << 16), __uint_as_float(w[q] & 0xFFFF0000u));
+  return m;
+}
+
+// Largest value over the wave, by DPP moves on order-preserving integer keys (no
+// index arithmetic or LDS round trips): within quads, half rows and rows, then row
+// broadcasts carry the maximum to lane 63.  A NaN lane may make the result NaN,
+// which makes every bound test above keep its token.
+template <int kCtrl, int kRowMask>
+__device__ __forceinline__ int dpp_max_step(int k) {
+  return max(k, __builtin_amdgcn_update_dpp(static_cast<int>(0x80000000u), k, kCtrl, kRowMask, 0xF, false));
+}
+__device__ __forceinline__ float wave_max(float v) {
+  int k = __float_as_int(v);
+  k ^= (k >> 31) & 0x7FFFFFFF;
+  k = dpp_max_step<0xB1, 0xF>(k);    // quad_perm [1,0,3,2]
+  k = dpp_max_step<0x4E, 0xF>(k);    // quad_perm [2,3,0,1]
+  k = dpp_max_step<0x141, 0xF>(k);   // row_half_mirror
+  k = dpp_max_step<0x140, 0xF>(k);   // row_mirror
+  k = dpp_max_step<0x142, 0xA>(k);   // row_bcast:15 into rows 1 and 3
+  k = dpp_max_step<0x143, 0xC>(k);   // row_bcast:31 into rows 2 and 3
+  k = __builtin_amdgcn_readlane(k, 63);
+  return __int_as_float(k ^ ((k >> 31) & 0x7FFFFFFF));
+}
+
+// The raw bits of element e of a vector (fp32 bits, or bf16 bits in the low half).
+__device__ __forceinline__ uint32_t raw_elem(f32x4 o, int e) {
+  const float w[4] = {o.x, o.y, o.z, o.w};
+  return __float_as_uint(w[e]);
+}
+__device__ __forceinline__ uint32_t raw_elem(u32x4 o, int e) {
+  const uint32_t w[4] = {o.x, o.y, o.z, o.w};
+  return (e & 1) ? (w[e >> 1] >> 16) : (w[e >> 1] & 0xFFFFu);
+}
+__device__ __forceinline__ float from_raw(uint32_t r, float) { return __uint_as_float(r); }
+__device__ __forceinline__ uint16_t from_raw(uint32_t r, uint16_t) { return static_cast<uint16_t>(r); }
+
+// The noise draws of vector j: 4 tokens (fp32) or 8 (bf16), one block per 4 tokens
+// as CBRNG lays them out.
+__device__ __forceinline__ void noise_words(uint32_t j, const RoundKeys& k, uint32_t (&x)[4]) {
+  const Block n = philox_block(j, k);
+  x[0] = n.w0; x[1] = n.w1; x[2] = n.w2; x[3] = n.w3;
+}
+__device__ __forceinline__ void noise_words(uint32_t j, const RoundKeys& k, uint32_t (&x)[8]) {
+  const Block n0 = philox_block(2u * j, k);
+  const Block n1 = philox_block(2u * j + 1u, k);
+  x[0] = n0.w0; x[1] = n0.w1; x[2] = n0.w2; x[3] = n0.w3;
+  x[4] = n1.w0; x[5] = n1.w1; x[6] = n1.w2; x[7] = n1.w3;
+}
+
+// Appends a lane's token to the wave's queue at its rank among the lanes in mask.
+__device__ __forceinline__ void enqueue(uint32_t* q_v, uint32_t* q_raw, uint32_t queued, uint64_t mask,
+                                        uint32_t v, uint32_t raw) {
+  const uint32_t pos = queued + __builtin_amdgcn_mbcnt_hi(static_cast<uint32_t>(mask >> 32),
+                                                          __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(mask), 0u));
+  q_v[pos] = v;
+  q_raw[pos] = raw;
+}
+
+// Scores the queued tokens of a wave, 64 at a time, one per lane: colour, bias, noise.
+template <typename T, int kSeeding, int kW>
+__device__ __forceinline__ void score_queue(LaneBest& b, const uint32_t* q_v, const uint32_t* q_raw,
+                                            uint32_t queued, const RowSeed<kW>& rs, uint32_t tm1,
+                                            int none_green, float delta, const Score<true>& sc) {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  for (uint32_t i = threadIdx.x % 64u; i < queued; i += 64u) {
+    const uint32_t v = q_v[i];
+    const T raw = from_raw(q_raw[i], T{});
+    uint32_t x;
+    if constexpr (kSeeding == kContext)
+      x = block_word(philox_block(v >> 2, opaque_key(key_of(rs.seed))), v & 3u);
+    else
+      x = draw<kSelfSalt>(rs, v);
+    const bool g = !none_green && is_green(x, tm1);
+    const float l = widen(bias_elem(raw, delta, g));
+    const float noise = gumbel_of(block_word(philox_block(v >> 2, opaque_key(key_of(sc.seed))), v & 3u));
+    consider_any_order(b, l * sc.inv_t + noise, v);
+  }
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// Sampling, vector path.  A segment is kSub sub-batches laid out like the segments
+// of argmax_vec_kernel.  Every token's noise must be drawn, but its exact value (two
+// logarithms) and the token's colour only matter for the few tokens that may still
+// reach the wave's best score.  Per sub-batch:
+//  1. the wave's largest logit m gives a lower bound lb of the best score (with the
+//     noise's overall minimum); a vector none of whose tokens reaches lb even with
+//     the noise's overall maximum draws no noise;
+//  2. the other vectors draw their noise; each token's score is bounded from above
+//     and below by the bounds of its noise (gumbel_upper, kGumbelGap) and of its
+//     logit (the larger and the smaller of x and bias(x)); lb rises to the largest
+//     lower bound of the wave;
+//  3. the tokens whose upper bound reaches lb join the wave's queue in LDS; a queue
+//     that would overflow, and the last one, is scored exactly, one token per lane.
+// lb only rises over the sub-batches.  A token left out scores below lb, which some
+// token of the wave's share attains, so the partial equals that of a full scan.  The bounds follow from monotone fp32
+// rounding: the score is (l * 1/T) + G with both steps rounded and 1/T > 0.  Lanes
+// see tokens out of index order, so their running argmax breaks ties by index.
+template <typename T, int kSeeding, int kN, int kSub, int kW>
+__global__ void __launch_bounds__(kThreads)
+sample_vec_kernel(const T* __restrict__ logits, int64_t row_stride, uint32_t V, int64_t B,
+                  const int32_t* __restrict__ context, int width, uint64_t key, uint32_t tm1,
+                  int none_green, float delta, const uint64_t* __restrict__ seeds, float inv_t,
+                  uint32_t segments, uint64_t* __restrict__ partials) {
+  using VecT = typename std::conditional<sizeof(T) == 4, f32x4, u32x4>::type;
+  constexpr int kE = sizeof(T) == 4 ? 4 : 8;         // tokens per vector
+  __shared__ uint64_t lds_key[kThreads / 64], lds_part[kThreads / 64];
+  // Per wave: token ids, then raw logits.  The queue is scored whenever it holds more
+  // than 64 tokens before a vector is queued, so it never holds more than 64 plus one
+  // vector's worth (kE tokens in each of 64 lanes).
+  constexpr uint32_t kQueueCap = 64u + 64u * kE;
+  __shared__ uint32_t lds_queue[(kThreads / 64) * 2 * kQueueCap];
+  uint32_t* q_v = lds_queue + (threadIdx.x / 64u) * 2u * kQueueCap;
+  uint32_t* q_raw = q_v + kQueueCap;
+  constexpr uint32_t kPer = 16u / sizeof(T);
+  constexpr uint32_t kSubVecs = kThreads * kN;       // vectors per sub-batch
+  const uint32_t full = V / kPer;
+  const uint32_t tail = V % kPer;
+  const uint32_t seg_base = blockIdx.x * (kSubVecs * kSub);
+  for (int64_t row = blockIdx.y; row < B; row += gridDim.y) {
+    const T* row_ptr = logits + row * row_stride;
+    const VecT* vec = reinterpret_cast<const VecT*>(row_ptr);
+    const Score<true> sc{seeds[row], inv_t};
+    const RoundKeys nk = vector_round_keys(key_of(sc.seed));
+    const RowSeed<kW> rs = row_seed<kSeeding, kW>(key, context + row * width, width);
+    const float dt = fabsf(delta) * inv_t;
+    const float dplus = delta > 0.0f ? delta : 0.0f;
+    LaneBest best = lane_best_init();
+    float lb = -INFINITY;           // the best score is at least lb (the same in every lane)
+    uint32_t queued = 0;            // tokens in the wave's queue (the same in every lane)
+    // Sub-batch `sub` into registers; the next one is loaded while this one is scored.
+    auto load_sub = [&](VecT (&buf)[kN], int sub) {
+      // Opaque to the optimiser, so that no Philox work is hoisted out of the loops.
+      uint32_t sub_first = seg_base + static_cast<uint32_t>(sub) * kSubVecs;
+      asm volatile("" : "+s"(sub_first));
+      if (sub_first + kSubVecs <= full) {
+#pragma unroll
+        for (int n = 0; n < kN; ++n) buf[n] = stream_load(vec + sub_first + n * kThreads + threadIdx.x);
+      } else {
+#pragma unroll
+        for (int n = 0; n < kN; ++n) {
+          const uint32_t j = sub_first + n * kThreads + threadIdx.x;
+          buf[n] = VecT{};
+          if (j < full) buf[n] = stream_load(vec + j);
+        }
+      }
+    };
+    auto process_sub = [&](const VecT (&buf)[kN], int sub) {
+      uint32_t sub_first = seg_base + static_cast<uint32_t>(sub) * kSubVecs;
+      asm volatile("" : "+s"(sub_first));
+      const bool whole = sub_first + kSubVecs <= full;
+      float m = -INFINITY;
+#pragma unroll
+      for (int n = 0; n < kN; ++n)
+        if (whole || sub_first + n * kThreads + threadIdx.x < full) m = fold_max(buf[n], m);
+      const float lb0 = fmaxf(lb, reach_bound(wave_max(m), delta, T{}) * inv_t + kGumbelLo);
+      float hi[kN][kE];
+      float top = -INFINITY;    // the lane's largest hi among tokens whose draw has c >= 2
+#pragma unroll
+      for (int n = 0; n < kN; ++n) {
+        const uint32_t j = sub_first + n * kThreads + threadIdx.x;
+        float phi[kE];
+        upper_logits(buf[n], delta, dplus, inv_t, phi);
+        float vmax = -INFINITY;   // NaN-propagating: a NaN token is always kept
+#pragma unroll
+        for (int e = 0; e < kE; ++e) vmax = __builtin_elementwise_maximum(vmax, phi[e]);
+        const bool reach = (whole || j < full) && !(vmax + kGumbelHi < lb0);
+#pragma unroll
+        for (int e = 0; e < kE; ++e) hi[n][e] = -INFINITY;
+        if (reach) {
+          uint32_t nw[kE];
+          noise_words(j, nk, nw);
+#pragma unroll
+          for (int e = 0; e < kE; ++e) {
+            const float c = noise_ones(nw[e]);
+            hi[n][e] = phi[e] + gumbel_upper(c);
+            top = fmaxf(top, c >= 2.0f ? hi[n][e] : -INFINITY);
+          }
+        }
+      }
+      // A token with c >= 2 and upper bound hi scores at least hi - gap - d: its noise
+      // is at least gumbel_upper(c) - kGumbelGap, and its two candidate logits times
+      // 1/T differ by at most |delta|/T plus roundings (of the bias, to 8 significant
+      // bits for bf16, and of the products), which the relative term covers, as it
+      // covers the rounding of this subtraction.  An infinite top gives no bound.
+      {
+        constexpr float kRel = sizeof(T) == 4 ? 0x1p-18f : 0x1p-7f;
+        const float slack = kGumbelGap + dt + kRel * (fabsf(top) + 18.0f + dt);
+        const float lb_lane = top < INFINITY ? top - slack : -INFINITY;
+        lb = fmaxf(lb0, wave_max(lb_lane));
+      }
+
+      // Queue the tokens whose upper bound reaches lb.  The counters are the same in
+      // every lane.
+#pragma unroll
+      for (int n = 0; n < kN; ++n) {
+        if (queued > 64u) {
+          score_queue<T, kSeeding>(best, q_v, q_raw, queued, rs, tm1, none_green, delta, sc);
+          queued = 0;
+          lb = fmaxf(lb, wave_max(best.any ? best.v : -INFINITY));
+        }
+        const uint32_t j = sub_first + n * kThreads + threadIdx.x;
+        if (whole) {
+#pragma unroll
+          for (int e = 0; e < kE; ++e) {
+            const bool reaches = !(hi[n][e] < lb);
+            const uint64_t mask = __ballot(reaches);
+            if (reaches) enqueue(q_v, q_raw, queued, mask, j * kE + e, raw_elem(buf[n], e));
+            queued = __builtin_amdgcn_readfirstlane(queued + static_cast<uint32_t>(__popcll(mask)));
+          }
+        } else {
+          const bool valid = j < full;
+          const uint64_t valid_mask = __ballot(valid);
+#pragma unroll
+          for (int e = 0; e < kE; ++e) {
+            const bool reaches = !(hi[n][e] < lb);
+            const uint64_t mask = __ballot(reaches) & valid_mask;
+            if (valid && reaches) enqueue(q_v, q_raw, queued, mask, j * kE + e, raw_elem(buf[n], e));
+            queued = __builtin_amdgcn_readfirstlane(queued + static_cast<uint32_t>(__popcll(mask)));
+          }
+        }
+      }
+    };
+    VecT buf0[kN], buf1[kN];
+    load_sub(buf0, 0);
+    for (int sub = 0; sub < kSub; sub += 2) {
+      if (sub + 1 < kSub) load_sub(buf1, sub + 1);
+      process_sub(buf0, sub);
+      if (sub + 1 < kSub) {
+        if (sub + 2 < kSub) load_sub(buf0, sub + 2);
+        process_sub(buf1, sub + 1);
+      }
+    }
+    if (queued != 0u)
+      score_queue<T, kSeeding>(best, q_v, q_raw, queued, rs, tm1, none_green, delta, sc);
+    // The row's partial last vector, element by element, by lane 0 of the segment
+    // that holds it.
+    if (tail != 0u && threadIdx.x == 0 && full >= seg_base && full - seg_base < kSubVecs * kSub) {
+      for (uint32_t e = 0; e < tail; ++e) {
+        const uint32_t v = full * kPer + e;
+        const bool g = !none_green && is_green(draw<kSeeding>(rs, v), tm1);
+        consider_any_order(best, sc.of(widen(bias_elem(row_ptr[v], delta, g)), v), v);
+      }
+    }
+    block_argmax_store(best, partials + row * segments + blockIdx.x, lds_key, lds_part);
   }
 }
 
@@ -1137,9 +1383,16 @@ constexpr int argmax_vecs_for() {
 }
 template <typename T>
 constexpr uint64_t vec_segment_elems(int kN) { return (16u / sizeof(T)) * kThreads * kN; }
+// Sampling holds a bound per token in registers: fewer vectors per lane for bf16.
+template <typename T>
+constexpr int sample_vecs_for() {
+  return sizeof(T) == 4 ? SBW_SAMPLE_VECS_F32 : SBW_SAMPLE_VECS_BF16;
+}
 // The workspace is sized for the element path; vector segments must be at least as long.
 static_assert(vec_segment_elems<float>(SBW_ARGMAX_VECS_CONTEXT) >= kArgmaxSegElems &&
-                  vec_segment_elems<float>(SBW_ARGMAX_VECS_SELF_SALT) >= kArgmaxSegElems,
+                  vec_segment_elems<float>(SBW_ARGMAX_VECS_SELF_SALT) >= kArgmaxSegElems &&
+                  vec_segment_elems<float>(SBW_SAMPLE_VECS_F32) >= kArgmaxSegElems &&
+                  vec_segment_elems<uint16_t>(SBW_SAMPLE_VECS_BF16) >= kArgmaxSegElems,
               "vector segments must not outnumber element segments");
 
 // The per-row noise seeds and 1/T of a sampling pass (unused by greedy decoding).
@@ -1156,13 +1409,20 @@ void launch_argmax(const void* logits, int64_t B, uint32_t V, int64_t row_stride
   const T* p = static_cast<const T*>(logits);
   const uint32_t rows = static_cast<uint32_t>(B < kMaxGridY ? B : kMaxGridY);
   uint32_t segments;
-  if (aligned) {
+  if (aligned && kSample) {
+    constexpr int kN = sample_vecs_for<T>();
+    const uint64_t seg = vec_segment_elems<T>(kN) * SBW_SAMPLE_SUBS;
+    segments = static_cast<uint32_t>((static_cast<uint64_t>(V) + seg - 1) / seg);
+    hipLaunchKernelGGL((sample_vec_kernel<T, kSeeding, kN, SBW_SAMPLE_SUBS, kW>), dim3(segments, rows),
+                       dim3(kThreads), 0, stream, p, row_stride, V, B, context, width, key, tm1,
+                       none, delta, sa.seeds, sa.inv_t, segments, partials);
+  } else if (aligned) {
     constexpr int kN = argmax_vecs_for<kSeeding>();
     const uint64_t seg = vec_segment_elems<T>(kN);
     segments = static_cast<uint32_t>((static_cast<uint64_t>(V) + seg - 1) / seg);
-    hipLaunchKernelGGL((argmax_vec_kernel<T, kSeeding, kN, kW, kSample>), dim3(segments, rows),
+    hipLaunchKernelGGL((argmax_vec_kernel<T, kSeeding, kN, kW>), dim3(segments, rows),
                        dim3(kThreads), 0, stream, p, row_stride, V, B, context, width, key, tm1,
-                       none, delta, sa.seeds, sa.inv_t, segments, partials);
+                       none, delta, segments, partials);
   } else {
     segments = static_cast<uint32_t>((static_cast<uint64_t>(V) + kArgmaxSegElems - 1) /
                                      kArgmaxSegElems);

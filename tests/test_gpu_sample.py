@@ -149,3 +149,36 @@ def test_sample_c4_full_size(env, seeding, dtype):
     assert_argmax_equal(got, expect, f"c4 {seeding} {dtype}")
     green = oracle.is_green_many(KEY, prev, expect[0], c["gamma"], seeding)
     assert green.mean() > 0.5          # the watermark shows in the draws
+
+
+def queue_rows(rng, V, dtype):
+    """Rows where many tokens reach the best score's bound, so a wave's candidate
+    queue fills and is scored in several rounds, with ties spread over lanes, waves
+    and segments: all +inf, all -inf, all NaN, equal huge logits (the noise rounds
+    away, every one of them ties) among small ones, and a row of equal logits."""
+    rows = [np.full(V, np.inf, dtype=np.float32), np.full(V, -np.inf, dtype=np.float32),
+            np.full(V, np.nan, dtype=np.float32)]
+    r = (0.1 * rng.standard_normal(V)).astype(np.float32)
+    r[rng.choice(V, 300, replace=False)] = 1e9
+    rows.append(r)
+    r = np.full(V, -5.0, dtype=np.float32); r[V - 3] = np.nan; r[V // 2:V // 2 + 2000] = 1e9
+    rows.append(r)
+    rows.append(np.full(V, 0.5, dtype=np.float32))
+    x = np.stack(rows)
+    return workloads.f32_to_bf16_bits(x) if dtype == "bf16" else x
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("seeding", ["context", "self_salt"])
+@pytest.mark.parametrize("V", [20000, 40001])
+def test_sample_queue_rounds(env, dtype, seeding, V):
+    rng = np.random.default_rng(450 + V)
+    x = queue_rows(rng, V, dtype)
+    B = x.shape[0]
+    ctx = workloads.context_tokens(B, 1, V, rng)[:, 0].copy()
+    seeds = seeds_for(rng, B)
+    for gamma, delta, inv_t in [(0.25, 2.0, 1.0), (0.5, -1.0, 1e-30), (1.0, 0.5, 1e30)]:
+        say(f"sample queue rounds {dtype} {seeding} V={V} gamma={gamma} inv_t={inv_t}")
+        assert_argmax_equal(run_sample(env, x, ctx, seeds, WIDE, gamma, delta, seeding, inv_t),
+                            oracle.watermark_sample(x, ctx, WIDE, gamma, delta, seeding, seeds, inv_t),
+                            f"{dtype}/{seeding}/{V}/{gamma}/{inv_t}")
