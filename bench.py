@@ -239,7 +239,8 @@ def other_configs(torch, sbw, dev, steps, c5_tokens):
         us = _mean_us(torch, lambda i, s=seeding: sbw.watermark_sample(
             bufs[i % len(bufs)], p, key, c["gamma"], c["delta"], seeds, s, 1.0, tokens=tokens,
             scores=scores, workspace=ws), steps)
-        sampled[seeding] = {"us": us, "gelem_per_s": n / us / 1e3}
+        sampled[seeding] = {"us": us, "gelem_per_s": n / us / 1e3, "hbm_gbps": 4 * n / us / 1e3,
+                            "hbm_frac": 4 * n / us / 1e3 / HBM_PEAK_GBPS}
     res["c4_watermark_sample"] = sampled
     del bufs
 
@@ -514,13 +515,14 @@ def main():
         del bufs
         torch.cuda.empty_cache()
         out["configs"] = other_configs(torch, sbw, dev, args.steps, toks)
-        # The fused argmax pass runs at one shape only, so its name alone keys it.
+        # The fused argmax and sampling passes run at one shape only, so the name keys them.
         traffic_cfg = measured_traffic(PROFILE_CONFIGS)
-        for seeding, code in (("context", 0), ("self_salt", 1)):
-            hits = [v for k, v in traffic_cfg.items()
-                    if k.startswith(f"sbw::argmax_vec_kernel<float, {code},")]
-            out["configs"]["c4_watermark_argmax"][seeding]["traffic"] = (
-                hits[0] if len(hits) == 1 else None)
+        for cfg, kernel in (("c4_watermark_argmax", "argmax_vec_kernel"),
+                            ("c4_watermark_sample", "sample_vec_kernel")):
+            for seeding, code in (("context", 0), ("self_salt", 1)):
+                hits = [v for k, v in traffic_cfg.items()
+                        if k.startswith(f"sbw::{kernel}<float, {code},")]
+                out["configs"][cfg][seeding]["traffic"] = hits[0] if len(hits) == 1 else None
         out["paper_table"] = paper_table(torch, sbw, dev)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(x, prev, toks["self_salt"], args.cpu_seconds)
