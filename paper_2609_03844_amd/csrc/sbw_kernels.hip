@@ -40,12 +40,30 @@ namespace {
 #define SBW_CONTEXT_UNROLL 2   // 16-byte vectors per lane, context seeding (HBM-bound)
 #endif
 #ifndef SBW_SELF_SALT_UNROLL
-#define SBW_SELF_SALT_UNROLL 2 // 16-byte vectors per lane, self-salt (Philox-bound)
+#define SBW_SELF_SALT_UNROLL 2 // 16-byte vectors per lane, self-salt fp32 (Philox-bound)
+#endif
+#ifndef SBW_SELF_SALT_UNROLL_BF16
+#define SBW_SELF_SALT_UNROLL_BF16 1
 #endif
 // Self-salt rows per workgroup (sharing the candidate terms) are chosen per launch,
 // for width 1 only (with a wider window the window terms dominate and sharing does
 // not pay): the most rows, up to 4 for fp32 and 2 for bf16 (register pressure), that
 // still leave SBW_SELF_SALT_MIN_GROUPS workgroups.
+// A self-salt workgroup may also take several row groups (at most ..._GROUP_ITERS,
+// while SBW_SELF_SALT_MIN_GROUPS workgroups remain), computing the candidate terms
+// once, and load the next group while drawing the current one (..._PREFETCH).
+#ifndef SBW_SELF_SALT_GROUP_ITERS
+#define SBW_SELF_SALT_GROUP_ITERS 1
+#endif
+#ifndef SBW_SELF_SALT_PREFETCH
+#define SBW_SELF_SALT_PREFETCH 0
+#endif
+#ifndef SBW_SELF_SALT_GROUP_ITERS_BF16
+#define SBW_SELF_SALT_GROUP_ITERS_BF16 4
+#endif
+#ifndef SBW_SELF_SALT_PREFETCH_BF16
+#define SBW_SELF_SALT_PREFETCH_BF16 1
+#endif
 #ifndef SBW_SELF_SALT_MIN_GROUPS
 #define SBW_SELF_SALT_MIN_GROUPS 2048
 #endif
@@ -267,10 +285,12 @@ __device__ __forceinline__ u32x4 bias_vec_terms(u32x4 raw, uint32_t j, const Can
   return u32x4{out[0], out[1], out[2], out[3]};
 }
 
-// Grid: x = tile of kThreads * kU vectors of a row, y = group of kRows rows
-// (grid-stride over groups beyond 65535).  All rows' loads are issued first; the
-// candidate terms are computed while they are in flight.
-template <typename T, int kU, int kW, int kRows>
+// Grid: x = tile of kThreads * kU vectors of a row, y = a slot that takes groups of
+// kRows rows y, y + gridDim.y, ...  The candidate terms depend on the columns only, so
+// a workgroup computes them once, while its first group's loads are in flight, and
+// uses them for every group it takes.  With kPrefetch the next group's logits are
+// loaded while the current group is drawn.
+template <typename T, int kU, int kW, int kRows, bool kPrefetch>
 __global__ void __launch_bounds__(kThreads)
 watermark_ss_rows_kernel(T* __restrict__ logits, int64_t row_stride, uint32_t V, int64_t B,
                          const int32_t* __restrict__ context, int width, uint64_t key, uint32_t tm1,
@@ -282,13 +302,11 @@ watermark_ss_rows_kernel(T* __restrict__ logits, int64_t row_stride, uint32_t V,
   const uint32_t first = blockIdx.x * (kThreads * kU);
   const bool whole = first + kThreads * kU <= full;
   const int64_t groups = (B + kRows - 1) / kRows;
-  for (int64_t g = blockIdx.y; g < groups; g += gridDim.y) {
+  auto load_group = [&](VecT (&buf)[kRows][kU], int64_t g) {
     const int64_t row0 = g * kRows;
-    const int nrows = static_cast<int>(B - row0 < kRows ? B - row0 : kRows);
-    VecT buf[kRows][kU];
 #pragma unroll
     for (int r = 0; r < kRows; ++r) {
-      if (r < nrows) {
+      if (row0 + r < B) {
         const VecT* vec = reinterpret_cast<const VecT*>(logits + (row0 + r) * row_stride);
 #pragma unroll
         for (int u = 0; u < kU; ++u) {
@@ -297,15 +315,13 @@ watermark_ss_rows_kernel(T* __restrict__ logits, int64_t row_stride, uint32_t V,
         }
       }
     }
-    CandTerm ct[kU][kPer];
-#pragma unroll
-    for (int u = 0; u < kU; ++u)
-#pragma unroll
-      for (uint32_t e = 0; e < kPer; ++e)
-        ct[u][e] = cand_term(key, (first + u * kThreads + threadIdx.x) * kPer + e);
+  };
+  CandTerm ct[kU][kPer];
+  auto draw_group = [&](const VecT (&buf)[kRows][kU], int64_t g) {
+    const int64_t row0 = g * kRows;
 #pragma unroll
     for (int r = 0; r < kRows; ++r) {
-      if (r < nrows) {
+      if (row0 + r < B) {
         const int64_t row = row0 + r;
         T* row_ptr = logits + row * row_stride;
         VecT* vec = reinterpret_cast<VecT*>(row_ptr);
@@ -322,6 +338,36 @@ watermark_ss_rows_kernel(T* __restrict__ logits, int64_t row_stride, uint32_t V,
             bias_one<T, kSelfSalt>(row_ptr, full * kPer + e, rs, tm1, delta);
         }
       }
+    }
+  };
+  int64_t g = blockIdx.y;
+  if (g >= groups) return;
+  VecT buf0[kRows][kU];
+  load_group(buf0, g);
+#pragma unroll
+  for (int u = 0; u < kU; ++u)
+#pragma unroll
+    for (uint32_t e = 0; e < kPer; ++e)
+      ct[u][e] = cand_term(key, (first + u * kThreads + threadIdx.x) * kPer + e);
+  if constexpr (!kPrefetch) {
+    for (;;) {
+      draw_group(buf0, g);
+      g += gridDim.y;
+      if (g >= groups) break;
+      load_group(buf0, g);
+    }
+  } else {
+    VecT buf1[kRows][kU];
+    for (;;) {
+      const int64_t g1 = g + gridDim.y;
+      if (g1 < groups) load_group(buf1, g1);
+      draw_group(buf0, g);
+      if (g1 >= groups) break;
+      const int64_t g2 = g1 + gridDim.y;
+      if (g2 < groups) load_group(buf0, g2);
+      draw_group(buf1, g1);
+      if (g2 >= groups) break;
+      g = g2;
     }
   }
 }
@@ -1292,11 +1338,15 @@ sbw_status_t check_width(int64_t width) {
   return SBW_OK;
 }
 
-// Vectors per lane.  Two in flight per lane measured best for both seedings on
-// MI355X: the context pass reaches ~80 % of HBM peak (one per lane: ~75 %), and the
-// self-salt pass gets two independent sets of Philox chains per lane.
-template <int kSeeding>
-constexpr int unroll_for() { return kSeeding == kContext ? SBW_CONTEXT_UNROLL : SBW_SELF_SALT_UNROLL; }
+// Vectors per lane.  Two in flight per lane measured best for the context pass (~80 %
+// of HBM peak; one per lane: ~75 %) and for fp32 self-salt (two independent sets of
+// Philox chains per lane); bf16 self-salt does best with one (8 tokens) per lane and
+// row groups that load their successor while drawing.
+template <int kSeeding, typename T>
+constexpr int unroll_for() {
+  return kSeeding == kContext ? SBW_CONTEXT_UNROLL
+                              : (sizeof(T) == 4 ? SBW_SELF_SALT_UNROLL : SBW_SELF_SALT_UNROLL_BF16);
+}
 
 template <typename T, int kSeeding, int kW>
 void launch_watermark(void* logits, int64_t B, uint32_t V, int64_t row_stride,
@@ -1305,7 +1355,7 @@ void launch_watermark(void* logits, int64_t B, uint32_t V, int64_t row_stride,
   T* p = static_cast<T*>(logits);
   const uint32_t rows = static_cast<uint32_t>(B < kMaxGridY ? B : kMaxGridY);
   if (aligned) {
-    constexpr int kU = unroll_for<kSeeding>();
+    constexpr int kU = unroll_for<kSeeding, T>();
     constexpr uint32_t kPer = 16u / sizeof(T);
     const uint64_t vectors = (static_cast<uint64_t>(V) + kPer - 1) / kPer;
     const uint32_t tiles = static_cast<uint32_t>((vectors + kThreads * kU - 1) / (kThreads * kU));
@@ -1317,17 +1367,26 @@ void launch_watermark(void* logits, int64_t B, uint32_t V, int64_t row_stride,
                                      ? 2
                                      : 1;
       const int64_t groups = (B + rows_per_group - 1) / rows_per_group;
-      const dim3 grid(tiles, static_cast<uint32_t>(groups < kMaxGridY ? groups : kMaxGridY));
+      // Each workgroup takes up to kIters groups while that still leaves
+      // SBW_SELF_SALT_MIN_GROUPS workgroups.
+      int64_t slots = groups;
+      constexpr int kIters = sizeof(T) == 4 ? SBW_SELF_SALT_GROUP_ITERS : SBW_SELF_SALT_GROUP_ITERS_BF16;
+      for (int it = kIters; it > 1; --it) {
+        const int64_t s2 = (groups + it - 1) / it;
+        if (s2 * tiles >= int64_t{SBW_SELF_SALT_MIN_GROUPS}) { slots = s2; break; }
+      }
+      const dim3 grid(tiles, static_cast<uint32_t>(slots < kMaxGridY ? slots : kMaxGridY));
+      constexpr bool kPf = (sizeof(T) == 4 ? SBW_SELF_SALT_PREFETCH : SBW_SELF_SALT_PREFETCH_BF16) != 0;
       if (kMaxRows == 4 && rows_per_group == 4)
-        hipLaunchKernelGGL((watermark_ss_rows_kernel<T, kU, kW, (kMaxRows > 2 ? kMaxRows : 1)>),
+        hipLaunchKernelGGL((watermark_ss_rows_kernel<T, kU, kW, (kMaxRows > 2 ? kMaxRows : 1), kPf>),
                            grid, dim3(kThreads), 0, stream, p, row_stride, V, B, context, width,
                            key, tm1, delta);
       else if (kMaxRows >= 2 && rows_per_group == 2)
-        hipLaunchKernelGGL((watermark_ss_rows_kernel<T, kU, kW, (kMaxRows >= 2 ? 2 : 1)>), grid,
+        hipLaunchKernelGGL((watermark_ss_rows_kernel<T, kU, kW, (kMaxRows >= 2 ? 2 : 1), kPf>), grid,
                            dim3(kThreads), 0, stream, p, row_stride, V, B, context, width, key, tm1,
                            delta);
       else
-        hipLaunchKernelGGL((watermark_ss_rows_kernel<T, kU, kW, 1>), grid, dim3(kThreads), 0,
+        hipLaunchKernelGGL((watermark_ss_rows_kernel<T, kU, kW, 1, kPf>), grid, dim3(kThreads), 0,
                            stream, p, row_stride, V, B, context, width, key, tm1, delta);
     } else {
       hipLaunchKernelGGL((watermark_vec_kernel<T, kU, kW>), dim3(tiles, rows),
