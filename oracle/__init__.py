@@ -89,6 +89,7 @@ def _declare(l: ctypes.CDLL) -> ctypes.CDLL:
         "oracle_gumbel": (f32, [u32, u64]),
         "oracle_sample_log_many": (None, [P, i64, P]),
         "oracle_gumbel_many": (None, [P, P, i64, P]),
+        "oracle_gumbel_of_draws": (None, [P, i64, P]),
         "oracle_watermark_sample_f32_w": (None, [P, i64, i64, i64, P, i64, u64, f64, f32, i32, P, f32, P, P]),
         "oracle_watermark_sample_bf16_w": (None, [P, i64, i64, i64, P, i64, u64, f64, f32, i32, P, f32, P, P]),
         "oracle_watermark_candidates_bf16_w": (None, [P, i64, i64, i64, P, i64, P, i64, u64, f64, f32, i32]),
@@ -380,6 +381,14 @@ def gumbel_many(v, seed) -> np.ndarray:
     s = np.ascontiguousarray(np.broadcast_to(np.asarray(seed, dtype=np.uint64), v.shape))
     out = np.empty(v.shape, dtype=np.float32)
     lib().oracle_gumbel_many(_ptr(v), _ptr(s), v.size, _ptr(out))
+    return out
+
+
+def gumbel_of_draws(x) -> np.ndarray:
+    """The noise G = -log(-log u) of raw 32-bit draws x, u = ((x >> 9) + 1/2) * 2^-23."""
+    x = np.ascontiguousarray(x, dtype=np.uint32)
+    out = np.empty(x.shape, dtype=np.float32)
+    lib().oracle_gumbel_of_draws(_ptr(x), x.size, _ptr(out))
     return out
 
 

@@ -611,11 +611,15 @@ float oracle_sample_log(float x)
     return (float)e * 0.693147180559945309f + 2.0f * poly;
 }
 
-float oracle_gumbel(uint32_t v, uint64_t seed)
+float oracle_gumbel_of_draw(uint32_t x)
 {
-    uint32_t x = oracle_cbrng(v, seed);
     float u = ((float)(x >> 9) + 0.5f) * 1.1920928955078125e-7f;   /* 2^-23 */
     return -oracle_sample_log(-oracle_sample_log(u));
+}
+
+float oracle_gumbel(uint32_t v, uint64_t seed)
+{
+    return oracle_gumbel_of_draw(oracle_cbrng(v, seed));
 }
 
 void oracle_watermark_sample_f32_w(const float *logits, int64_t B, int64_t V, int64_t row_stride,
@@ -668,4 +672,9 @@ void oracle_sample_log_many(const float *x, int64_t n, float *out)
 void oracle_gumbel_many(const uint32_t *v, const uint64_t *seed, int64_t n, float *out)
 {
     for (int64_t i = 0; i < n; ++i) out[i] = oracle_gumbel(v[i], seed[i]);
+}
+
+void oracle_gumbel_of_draws(const uint32_t *x, int64_t n, float *out)
+{
+    for (int64_t i = 0; i < n; ++i) out[i] = oracle_gumbel_of_draw(x[i]);
 }
