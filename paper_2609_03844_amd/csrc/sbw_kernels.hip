@@ -778,7 +778,24 @@ __device__ __forceinline__ void enqueue(uint32_t* q_v, uint32_t* q_raw, uint32_t
   q_raw[pos] = raw;
 }
 
-// Scores the queued tokens of a wave, 64 at a time, one per lane: colour, bias, noise.
+// The exact score of one queued token: colour, bias, noise.
+template <typename T, int kSeeding, int kW>
+__device__ __forceinline__ void score_entry(LaneBest& b, uint32_t v, uint32_t raw_bits,
+                                            const RowSeed<kW>& rs, uint32_t tm1, int none_green,
+                                            float delta, const Score<true>& sc) {
+  const T raw = from_raw(raw_bits, T{});
+  uint32_t x;
+  if constexpr (kSeeding == kContext)
+    x = block_word(philox_block(v >> 2, opaque_key(key_of(rs.seed))), v & 3u);
+  else
+    x = draw<kSelfSalt>(rs, v);
+  const bool g = !none_green && is_green(x, tm1);
+  const float l = widen(bias_elem(raw, delta, g));
+  const float noise = gumbel_of(block_word(philox_block(v >> 2, opaque_key(key_of(sc.seed))), v & 3u));
+  consider_any_order(b, l * sc.inv_t + noise, v);
+}
+
+// Scores the queued tokens of a wave, 64 at a time, one per lane.
 template <typename T, int kSeeding, int kW>
 __device__ __forceinline__ void score_queue(LaneBest& b, const uint32_t* q_v, const uint32_t* q_raw,
                                             uint32_t queued, const RowSeed<kW>& rs, uint32_t tm1,
@@ -786,19 +803,8 @@ __device__ __forceinline__ void score_queue(LaneBest& b, const uint32_t* q_v, co
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
   __builtin_amdgcn_wave_barrier();
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-  for (uint32_t i = threadIdx.x % 64u; i < queued; i += 64u) {
-    const uint32_t v = q_v[i];
-    const T raw = from_raw(q_raw[i], T{});
-    uint32_t x;
-    if constexpr (kSeeding == kContext)
-      x = block_word(philox_block(v >> 2, opaque_key(key_of(rs.seed))), v & 3u);
-    else
-      x = draw<kSelfSalt>(rs, v);
-    const bool g = !none_green && is_green(x, tm1);
-    const float l = widen(bias_elem(raw, delta, g));
-    const float noise = gumbel_of(block_word(philox_block(v >> 2, opaque_key(key_of(sc.seed))), v & 3u));
-    consider_any_order(b, l * sc.inv_t + noise, v);
-  }
+  for (uint32_t i = threadIdx.x % 64u; i < queued; i += 64u)
+    score_entry<T, kSeeding>(b, q_v[i], q_raw[i], rs, tm1, none_green, delta, sc);
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
   __builtin_amdgcn_wave_barrier();
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
@@ -835,6 +841,7 @@ sample_vec_kernel(const T* __restrict__ logits, int64_t row_stride, uint32_t V, 
   // vector's worth (kE tokens in each of 64 lanes).
   constexpr uint32_t kQueueCap = 64u + 64u * kE;
   __shared__ uint32_t lds_queue[(kThreads / 64) * 2 * kQueueCap];
+  __shared__ uint32_t lds_count[kThreads / 64];
   uint32_t* q_v = lds_queue + (threadIdx.x / 64u) * 2u * kQueueCap;
   uint32_t* q_raw = q_v + kQueueCap;
   constexpr uint32_t kPer = 16u / sizeof(T);
@@ -956,8 +963,27 @@ sample_vec_kernel(const T* __restrict__ logits, int64_t row_stride, uint32_t V, 
         process_sub(buf1, sub + 1);
       }
     }
-    if (queued != 0u)
-      score_queue<T, kSeeding>(best, q_v, q_raw, queued, rs, tm1, none_green, delta, sc);
+    // What is left in the four queues is scored together: entry i of their
+    // concatenation goes to lane i % 64 of wave (i / 64) % 4, so a workgroup's few
+    // candidates take one wave's pass instead of four.
+    {
+      const uint32_t lane = threadIdx.x % 64u, wave = threadIdx.x / 64u;
+      if (lane == 0u) lds_count[wave] = queued;
+      __syncthreads();
+      uint32_t start[kThreads / 64 + 1];
+      start[0] = 0u;
+#pragma unroll
+      for (int w = 0; w < kThreads / 64; ++w) start[w + 1] = start[w] + lds_count[w];
+      const uint32_t total = start[kThreads / 64];
+      for (uint32_t i = wave * 64u + lane; i < total; i += kThreads) {
+        uint32_t w = 0;
+#pragma unroll
+        for (int k = 1; k < kThreads / 64; ++k) w += static_cast<uint32_t>(i >= start[k]);
+        const uint32_t* wq = lds_queue + w * 2u * kQueueCap;
+        const uint32_t off = i - start[w];
+        score_entry<T, kSeeding>(best, wq[off], wq[kQueueCap + off], rs, tm1, none_green, delta, sc);
+      }
+    }
     // The row's partial last vector, element by element, by lane 0 of the segment
     // that holds it.
     if (tail != 0u && threadIdx.x == 0 && full >= seg_base && full - seg_base < kSubVecs * kSub) {
