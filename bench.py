@@ -75,6 +75,9 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-configs", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--power-probe", action="store_true",
+                    help="only run the self-salt pass back to back for ~2.5 s while sampling "
+                         "the GFX clock and socket power with amd-smi; print them as JSON")
     return ap.parse_args()
 
 
@@ -352,12 +355,78 @@ def _cpu_model():
     return "unknown"
 
 
+def power_probe(torch, sbw, dev, seconds=2.5):
+    """The clock and power the sustained self-salt pass runs at: amd-smi samples
+    (read-only) taken while 200-launch graph replays of the c4 pass run back to back."""
+    import subprocess
+    import threading
+    c4, key = workloads.C4, workloads.PAPER_KEY
+    x, prev = workloads.watermark_inputs("c4")
+    bufs = [torch.from_numpy(x).to(dev) for _ in range(6)]
+    p = torch.from_numpy(prev).to(dev)
+
+    def fn(i):
+        sbw.watermark(bufs[i % 6], p, key, c4["gamma"], c4["delta"], "self_salt")
+    for i in range(5):
+        fn(i)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        for i in range(200):
+            fn(i)
+    samples, stop = [], threading.Event()
+
+    def sampler():
+        while not stop.is_set():
+            t = time.time()
+            r = subprocess.run(["amd-smi", "metric", "-g", "0", "--clock", "--power", "--json"],
+                               capture_output=True, text=True)
+            try:
+                d = json.loads(r.stdout)
+                d = d["gpu_data"][0] if "gpu_data" in d else (d[0] if isinstance(d, list) else d)
+                samples.append((t, float(d["clock"]["gfx_0"]["clk"]["value"]),
+                                float(d["power"]["socket_power"]["value"])))
+            except (ValueError, KeyError, IndexError, TypeError):
+                pass
+            time.sleep(0.05)
+    th = threading.Thread(target=sampler)
+    th.start()
+    time.sleep(1.0)
+    t0, per_launch = time.time(), []
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    while time.time() - t0 < seconds:
+        a.record()
+        g.replay()
+        b.record()
+        torch.cuda.synchronize()
+        per_launch.append(a.elapsed_time(b) / 200 * 1e3)
+    t1 = time.time()
+    stop.set()
+    th.join()
+    idle = [s for s in samples if s[0] < t0]
+    busy = [s for s in samples if t0 + 0.5 <= s[0] < t1]     # past the first clock step
+    med = lambda xs: float(np.median(xs)) if xs else None
+    return {"probe": "self-salt c4 watermark, 200-launch graph replays back to back",
+            "seconds": round(t1 - t0, 2), "replays": len(per_launch),
+            "us_per_launch_first_replay": per_launch[0], "us_per_launch_median": med(per_launch),
+            "gfx_mhz_idle_median": med([s[1] for s in idle]),
+            "gfx_mhz_busy_median": med([s[1] for s in busy]),
+            "socket_w_busy_median": med([s[2] for s in busy]), "samples_busy": len(busy)}
+
+
 def main():
     args = parse()
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU; --gpus must be 1",
                           "n_gpus": args.gpus}))
         sys.exit(2)
+    if args.power_probe:
+        import torch
+        import paper_2609_03844_amd as sbw
+        dev = torch.device("cuda:0")
+        torch.cuda.set_device(dev)
+        print(json.dumps(power_probe(torch, sbw, dev)))
+        return
 
     import torch
     import paper_2609_03844_amd as sbw
