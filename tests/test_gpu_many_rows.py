@@ -1,7 +1,7 @@
 """GPU parity when rows (or row groups) outnumber the 65535 workgroups of a grid's y
 dimension, so every row-parallel kernel runs its grid-stride loop: many short rows
 for the watermark (both seedings, the self-salt row groups), greedy decoding,
-candidates and both detection kernels."""
+sampling, candidates and both detection kernels."""
 import numpy as np
 import pytest
 
@@ -40,6 +40,15 @@ def test_argmax_and_candidates_many_rows(env, seeding):
     torch.cuda.synchronize()
     et, ev = oracle.watermark_argmax(x, ctx, WIDE, 0.5, 1.5, seeding)
     assert np.array_equal(tok.cpu().numpy(), et) and np.array_equal(val.cpu().numpy(), ev)
+    # sampling: the same rows, one noise seed per row
+    seeds = rng.integers(0, 2**63, B, dtype=np.int64).astype(np.uint64)
+    say(f"sample many rows {seeding}")
+    tok, sc = sbw.watermark_sample(_to_device(torch, dev, x), c, WIDE, 0.5, 1.5,
+                                   torch.from_numpy(seeds.view(np.int64)).to(dev), seeding, 0.9)
+    torch.cuda.synchronize()
+    et, es = oracle.watermark_sample(x, ctx, WIDE, 0.5, 1.5, seeding, seeds, 0.9)
+    assert np.array_equal(tok.cpu().numpy(), et)
+    assert np.array_equal(sc.cpu().numpy().view(np.uint32), es.view(np.uint32))
     # candidates: one workgroup per row, at most 2^20 workgroups
     B, V = 1100001, 8
     x = rng.standard_normal((B, V)).astype(np.float32)

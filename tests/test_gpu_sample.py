@@ -182,3 +182,19 @@ def test_sample_queue_rounds(env, dtype, seeding, V):
         assert_argmax_equal(run_sample(env, x, ctx, seeds, WIDE, gamma, delta, seeding, inv_t),
                             oracle.watermark_sample(x, ctx, WIDE, gamma, delta, seeding, seeds, inv_t),
                             f"{dtype}/{seeding}/{V}/{gamma}/{inv_t}")
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("seeding", ["context", "self_salt"])
+@pytest.mark.parametrize("width", [2, 8])
+def test_sample_windows(env, dtype, seeding, width):
+    """Windows of 2 and of the longest supported width, 8, on a ragged multi-segment row."""
+    rng = np.random.default_rng(460 + width)
+    B, V = 5, 30011
+    x = hard_rows(rng, B, V, dtype)
+    ctx = workloads.context_tokens(B, width, V, rng)
+    seeds = seeds_for(rng, B)
+    say(f"sample windows {dtype} {seeding} h={width}")
+    assert_argmax_equal(run_sample(env, x, ctx, seeds, WIDE, 0.25, 2.0, seeding, 1.0),
+                        oracle.watermark_sample(x, ctx, WIDE, 0.25, 2.0, seeding, seeds, 1.0),
+                        f"{dtype}/{seeding}/h={width}")
