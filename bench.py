@@ -586,11 +586,11 @@ def main():
         out["configs"] = other_configs(torch, sbw, dev, args.steps, toks)
         # The fused argmax and sampling passes run at one shape only, so the name keys them.
         traffic_cfg = measured_traffic(PROFILE_CONFIGS)
-        for cfg, kernel in (("c4_watermark_argmax", "argmax_vec_kernel"),
-                            ("c4_watermark_sample", "sample_vec_kernel")):
+        for cfg, mode in (("c4_watermark_argmax", "false"), ("c4_watermark_sample", "true")):
             for seeding, code in (("context", 0), ("self_salt", 1)):
                 hits = [v for k, v in traffic_cfg.items()
-                        if k.startswith(f"sbw::{kernel}<float, {code},")]
+                        if k.startswith(f"sbw::decode_vec_kernel<float, {code},")
+                        and k.split("@")[0].endswith(f", {mode}>")]
                 out["configs"][cfg][seeding]["traffic"] = hits[0] if len(hits) == 1 else None
         out["paper_table"] = paper_table(torch, sbw, dev)
     if not args.no_cpu_baseline:

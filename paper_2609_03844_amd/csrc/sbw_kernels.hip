@@ -395,25 +395,18 @@ watermark_elem_kernel(T* __restrict__ logits, int64_t row_stride, uint32_t V, in
 // orders the values (every NaN above +inf, -0 equal to +0), the low word is
 // ~index, so the maximum key is the largest value at its smallest index.
 // ---------------------------------------------------------------------------
-// 16-byte vectors per lane in a workgroup's segment of the fused argmax.  A longer
-// segment gives each wave a larger sample for its skip bound; every lane holds its
-// whole share in registers.
-#ifndef SBW_ARGMAX_VECS_CONTEXT
-#define SBW_ARGMAX_VECS_CONTEXT 8
+// 16-byte vectors per lane in a sub-batch of the fused decoding pass (greedy and
+// sampling), and sub-batches per workgroup segment.  A longer segment gives each wave
+// a larger sample for its bounds; every lane holds a sub-batch in registers, and bf16
+// takes fewer vectors to hold its 8-token bounds.
+#ifndef SBW_DECODE_VECS_F32
+#define SBW_DECODE_VECS_F32 8
 #endif
-#ifndef SBW_ARGMAX_VECS_SELF_SALT
-#define SBW_ARGMAX_VECS_SELF_SALT 8
+#ifndef SBW_DECODE_VECS_BF16
+#define SBW_DECODE_VECS_BF16 4
 #endif
-#ifndef SBW_SAMPLE_VECS_F32
-#define SBW_SAMPLE_VECS_F32 8
-#endif
-#ifndef SBW_SAMPLE_VECS_BF16
-#define SBW_SAMPLE_VECS_BF16 4
-#endif
-// Sub-batches of that many vectors per lane in a sampling segment: they share one
-// candidate queue per wave and one read-out.
-#ifndef SBW_SAMPLE_SUBS
-#define SBW_SAMPLE_SUBS 1
+#ifndef SBW_DECODE_SUBS
+#define SBW_DECODE_SUBS 1
 #endif
 constexpr int kElemSegSteps = 8;                                // element kernel
 constexpr int64_t kArgmaxSegElems = kThreads * kElemSegSteps;   // element-kernel segment
@@ -463,24 +456,6 @@ __device__ __forceinline__ void consider_any_order(LaneBest& b, float x, uint32_
   b.any = true;
 }
 
-__device__ __forceinline__ void consider_vec(LaneBest& b, f32x4 o, uint32_t j) {
-  const uint32_t v = j * 4u;
-  consider(b, o.x, v);
-  consider(b, o.y, v + 1u);
-  consider(b, o.z, v + 2u);
-  consider(b, o.w, v + 3u);
-}
-
-__device__ __forceinline__ void consider_vec(LaneBest& b, u32x4 o, uint32_t j) {
-  const uint32_t v = j * 8u;
-  const uint32_t w[4] = {o.x, o.y, o.z, o.w};
-#pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    consider(b, __uint_as_float(w[q] << 16), v + 2u * q);
-    consider(b, __uint_as_float(w[q] & 0xFFFF0000u), v + 2u * q + 1u);
-  }
-}
-
 __device__ __forceinline__ float widen(float x) { return x; }
 __device__ __forceinline__ float widen(uint16_t x) { return __uint_as_float(static_cast<uint32_t>(x) << 16); }
 
@@ -527,18 +502,6 @@ __device__ __forceinline__ void block_argmax_store(const LaneBest& lb, uint64_t*
 // the maximum nor tied with it: its colour need not be drawn.  A NaN compares false
 // and is always kept (it wins), so NaN logits never make the test skip anything;
 // delta is finite, so bias(x) is NaN only when x is.
-__device__ __forceinline__ float raw_max(f32x4 o) { return fmaxf(fmaxf(o.x, o.y), fmaxf(o.z, o.w)); }
-__device__ __forceinline__ float raw_max(u32x4 o) {
-  float m = __uint_as_float(o.x << 16);
-  const uint32_t w[4] = {o.x, o.y, o.z, o.w};
-#pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    m = fmaxf(m, __uint_as_float(w[q] << 16));
-    m = fmaxf(m, __uint_as_float(w[q] & 0xFFFF0000u));
-  }
-  return m;
-}
-
 // The lower bound from the largest logit m (-inf when there is none).
 __device__ __forceinline__ float reach_bound(float m, float delta, float) {
   return fminf(m, m + delta);
@@ -548,34 +511,8 @@ __device__ __forceinline__ float reach_bound(float m, float delta, uint16_t) {
   return fminf(m, widen(bias_bf16(static_cast<uint16_t>(b), delta, true)));
 }
 
-// Whether some element of the vector may end at or above lb.  fp32: with
-// dplus = max(delta, 0), x + dplus is the larger of x and bias(x) (x itself when
-// delta < 0, where x + 0 only turns -0 into +0, which compares equal).
-__device__ __forceinline__ bool may_reach(f32x4 o, float dplus, float, float lb) {
-  return !(static_cast<bool>(static_cast<int>(o.x + dplus < lb) & static_cast<int>(o.y + dplus < lb) &
-                             static_cast<int>(o.z + dplus < lb) & static_cast<int>(o.w + dplus < lb)));
-}
-__device__ __forceinline__ bool may_reach(u32x4 o, float, float delta, float lb) {
-  const uint32_t w[4] = {o.x, o.y, o.z, o.w};
-  int below = 1;
-#pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    const uint32_t g = bias_bf16x2(w[q], delta, true, true);
-    below &= static_cast<int>(__uint_as_float(w[q] << 16) < lb) &
-             static_cast<int>(__uint_as_float(w[q] & 0xFFFF0000u) < lb) &
-             static_cast<int>(__uint_as_float(g << 16) < lb) &
-             static_cast<int>(__uint_as_float(g & 0xFFFF0000u) < lb);
-  }
-  return !below;
-}
-
-// Self-salt draws one Philox block per token, so it tests and draws token by token:
-// the elements of a vector as (x, bias(x)) pairs, then only those that may reach lb.
-__device__ __forceinline__ void green_values(f32x4 o, float delta, float (&x)[4], float (&gv)[4]) {
-  x[0] = o.x; x[1] = o.y; x[2] = o.z; x[3] = o.w;
-#pragma unroll
-  for (int e = 0; e < 4; ++e) gv[e] = bias_f32(x[e], delta, true);
-}
+// The 8 bf16 elements of a vector as (x, bias(x)) pairs: each token's two candidate
+// values, widened.
 __device__ __forceinline__ void green_values(u32x4 o, float delta, float (&x)[8], float (&gv)[8]) {
   const uint32_t w[4] = {o.x, o.y, o.z, o.w};
 #pragma unroll
@@ -600,95 +537,6 @@ struct Score {
   }
 };
 
-template <typename VecT, int kW>
-__device__ __forceinline__ void scan_self_salt(LaneBest& b, VecT o, uint32_t j, const RowSeed<kW>& rs,
-                                               uint32_t tm1, int none_green, float delta, float lb) {
-  constexpr int kE = std::is_same<VecT, f32x4>::value ? 4 : 8;
-  float x[kE], gv[kE];
-  green_values(o, delta, x, gv);
-#pragma unroll
-  for (int e = 0; e < kE; ++e) {
-    if (!(static_cast<bool>(static_cast<int>(x[e] < lb) & static_cast<int>(gv[e] < lb)))) {
-      const uint32_t v = j * kE + e;
-      const bool g = !none_green && is_green(draw<kSelfSalt>(rs, v), tm1);
-      consider(b, g ? gv[e] : x[e], v);
-    }
-  }
-}
-
-// Vector path.  A segment is kThreads * kN vectors, vector n of lane t at offset
-// n * kThreads + t; every lane loads all of its kN vectors at once.  Each wave
-// then takes the largest logit of its share, derives lb, and draws colours and
-// updates its running argmax only for the vectors that may reach lb, in increasing
-// index order (self-salt: the elements that may).  The skipped elements cannot be
-// the segment's maximum, so the partial is the same as that of a full scan.
-template <typename T, int kSeeding, int kN, int kW>
-__global__ void __launch_bounds__(kThreads)
-argmax_vec_kernel(const T* __restrict__ logits, int64_t row_stride, uint32_t V, int64_t B,
-                  const int32_t* __restrict__ context, int width, uint64_t key, uint32_t tm1,
-                  int none_green, float delta, uint32_t segments, uint64_t* __restrict__ partials) {
-  using VecT = typename std::conditional<sizeof(T) == 4, f32x4, u32x4>::type;
-  __shared__ uint64_t lds_key[kThreads / 64], lds_part[kThreads / 64];
-  constexpr uint32_t kPer = 16u / sizeof(T);
-  constexpr uint32_t kSegVecs = kThreads * kN;       // vectors per segment
-  const uint32_t full = V / kPer;
-  const uint32_t tail = V % kPer;
-  const uint32_t seg_base = blockIdx.x * kSegVecs;
-  const float dplus = delta > 0.0f ? delta : 0.0f;
-  for (int64_t row = blockIdx.y; row < B; row += gridDim.y) {
-    const T* row_ptr = logits + row * row_stride;
-    const VecT* vec = reinterpret_cast<const VecT*>(row_ptr);
-    // Opaque to the optimiser: otherwise the first Philox round of every vector,
-    // which depends on the counter only, is hoisted out of the row loop and pins
-    // registers for the whole kernel.
-    uint32_t seg_first = seg_base;
-    asm volatile("" : "+s"(seg_first));
-    VecT buf[kN];
-    float m = -INFINITY;
-    const bool whole = seg_first + kSegVecs <= full;
-    if (whole) {
-#pragma unroll
-      for (int n = 0; n < kN; ++n) buf[n] = stream_load(vec + seg_first + n * kThreads + threadIdx.x);
-#pragma unroll
-      for (int n = 0; n < kN; ++n) m = fmaxf(m, raw_max(buf[n]));
-    } else {
-#pragma unroll
-      for (int n = 0; n < kN; ++n) {
-        const uint32_t j = seg_first + n * kThreads + threadIdx.x;
-        if (j < full) {
-          buf[n] = stream_load(vec + j);
-          m = fmaxf(m, raw_max(buf[n]));
-        }
-      }
-    }
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) m = fmaxf(m, __shfl_xor(m, off, 64));
-    const float lb = reach_bound(m, delta, T{});
-    const RowSeed<kW> rs = row_seed<kSeeding, kW>(key, context + row * width, width);
-    LaneBest lb_lane = lane_best_init();
-#pragma unroll
-    for (int n = 0; n < kN; ++n) {
-      const uint32_t j = seg_first + n * kThreads + threadIdx.x;
-      if (!(whole || j < full)) continue;
-      if constexpr (kSeeding == kSelfSalt) {
-        scan_self_salt(lb_lane, buf[n], j, rs, tm1, none_green, delta, lb);
-      } else if (may_reach(buf[n], dplus, delta, lb)) {
-        consider_vec(lb_lane, none_green ? buf[n] : bias_vec_context(buf[n], j, rs.seed, tm1, delta), j);
-      }
-    }
-    // The row's partial last vector, element by element, by lane 0 of the segment
-    // that holds it (never skipped).
-    if (!whole && tail != 0u && threadIdx.x == 0 && full >= seg_first && full - seg_first < kSegVecs) {
-      for (uint32_t e = 0; e < tail; ++e) {
-        const uint32_t v = full * kPer + e;
-        const bool g = !none_green && is_green(draw<kSeeding>(rs, v), tm1);
-        consider(lb_lane, widen(bias_elem(row_ptr[v], delta, g)), v);
-      }
-    }
-    block_argmax_store(lb_lane, partials + row * segments + blockIdx.x, lds_key, lds_part);
-  }
-}
-
 // Each token's larger candidate logit, max(x, bias(x)), times 1/T.  fp32: bias(x)
 // is x + delta rounded, so the larger one is x + max(delta, 0) (x + 0 only turns -0
 // into +0).  bf16: bias rounds to bf16, so both candidates are formed.
@@ -703,6 +551,20 @@ __device__ __forceinline__ void upper_logits(u32x4 o, float delta, float, float 
   green_values(o, delta, x, gv);
 #pragma unroll
   for (int e = 0; e < 8; ++e) phi[e] = (delta >= 0.0f ? gv[e] : x[e]) * inv_t;
+}
+
+// The same without the temperature (greedy decoding).
+__device__ __forceinline__ void upper_logits(f32x4 o, float, float dplus, float (&phi)[4]) {
+  phi[0] = o.x + dplus;
+  phi[1] = o.y + dplus;
+  phi[2] = o.z + dplus;
+  phi[3] = o.w + dplus;
+}
+__device__ __forceinline__ void upper_logits(u32x4 o, float delta, float, float (&phi)[8]) {
+  float x[8], gv[8];
+  green_values(o, delta, x, gv);
+#pragma unroll
+  for (int e = 0; e < 8; ++e) phi[e] = delta >= 0.0f ? gv[e] : x[e];
 }
 
 // Largest raw logit of a vector folded into m.  v_max3_f32 on the raw values: the
@@ -779,10 +641,10 @@ __device__ __forceinline__ void enqueue(uint32_t* q_v, uint32_t* q_raw, uint32_t
 }
 
 // The exact score of one queued token: colour, bias, noise.
-template <typename T, int kSeeding, int kW>
+template <typename T, int kSeeding, int kW, bool kSample>
 __device__ __forceinline__ void score_entry(LaneBest& b, uint32_t v, uint32_t raw_bits,
                                             const RowSeed<kW>& rs, uint32_t tm1, int none_green,
-                                            float delta, const Score<true>& sc) {
+                                            float delta, const Score<kSample>& sc) {
   const T raw = from_raw(raw_bits, T{});
   uint32_t x;
   if constexpr (kSeeding == kContext)
@@ -791,45 +653,52 @@ __device__ __forceinline__ void score_entry(LaneBest& b, uint32_t v, uint32_t ra
     x = draw<kSelfSalt>(rs, v);
   const bool g = !none_green && is_green(x, tm1);
   const float l = widen(bias_elem(raw, delta, g));
-  const float noise = gumbel_of(block_word(philox_block(v >> 2, opaque_key(key_of(sc.seed))), v & 3u));
-  consider_any_order(b, l * sc.inv_t + noise, v);
+  if constexpr (kSample) {
+    const float noise = gumbel_of(block_word(philox_block(v >> 2, opaque_key(key_of(sc.seed))), v & 3u));
+    consider_any_order(b, l * sc.inv_t + noise, v);
+  } else {
+    consider_any_order(b, l, v);
+  }
 }
 
 // Scores the queued tokens of a wave, 64 at a time, one per lane.
-template <typename T, int kSeeding, int kW>
+template <typename T, int kSeeding, int kW, bool kSample>
 __device__ __forceinline__ void score_queue(LaneBest& b, const uint32_t* q_v, const uint32_t* q_raw,
                                             uint32_t queued, const RowSeed<kW>& rs, uint32_t tm1,
-                                            int none_green, float delta, const Score<true>& sc) {
+                                            int none_green, float delta, const Score<kSample>& sc) {
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
   __builtin_amdgcn_wave_barrier();
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
   for (uint32_t i = threadIdx.x % 64u; i < queued; i += 64u)
-    score_entry<T, kSeeding>(b, q_v[i], q_raw[i], rs, tm1, none_green, delta, sc);
+    score_entry<T, kSeeding, kW, kSample>(b, q_v[i], q_raw[i], rs, tm1, none_green, delta, sc);
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
   __builtin_amdgcn_wave_barrier();
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-// Sampling, vector path.  A segment is kSub sub-batches laid out like the segments
-// of argmax_vec_kernel.  Every token's noise must be drawn, but its exact value (two
-// logarithms) and the token's colour only matter for the few tokens that may still
-// reach the wave's best score.  Per sub-batch:
-//  1. the wave's largest logit m gives a lower bound lb of the best score (with the
-//     noise's overall minimum); a vector none of whose tokens reaches lb even with
-//     the noise's overall maximum draws no noise;
-//  2. the other vectors draw their noise; each token's score is bounded from above
+// Fused decoding, vector path: greedy (kSample false) or Gumbel-max sampling.  A
+// segment is kSub sub-batches of kThreads * kN vectors, vector n of lane t at
+// offset n * kThreads + t; every lane loads a sub-batch at once.  The colour draw
+// (and, sampling, the exact noise with its two logarithms) matters only for the few
+// tokens that may still reach the wave's best score.  Per sub-batch:
+//  1. greedy: with m the wave's largest logit, some token ends at least at
+//     lb = min(m, bias(m)), and a token's value is at most max(x, bias(x));
+//     sampling: lb from m with the noise's overall minimum, and a vector none of
+//     whose tokens reaches lb even with the noise's overall maximum draws no noise;
+//     the other vectors draw their noise, each token's score is bounded from above
 //     and below by the bounds of its noise (gumbel_upper, kGumbelGap) and of its
-//     logit (the larger and the smaller of x and bias(x)); lb rises to the largest
-//     lower bound of the wave;
-//  3. the tokens whose upper bound reaches lb join the wave's queue in LDS; a queue
-//     that would overflow, and the last one, is scored exactly, one token per lane.
-// lb only rises over the sub-batches.  A token left out scores below lb, which some
-// token of the wave's share attains, so the partial equals that of a full scan.  The bounds follow from monotone fp32
-// rounding: the score is (l * 1/T) + G with both steps rounded and 1/T > 0.  Lanes
-// see tokens out of index order, so their running argmax breaks ties by index.
-template <typename T, int kSeeding, int kN, int kSub, int kW>
+//     logit, and lb rises to the largest lower bound of the wave;
+//  2. the tokens whose upper bound reaches lb join the wave's queue in LDS; a queue
+//     that would overflow is scored exactly, one token per lane, and at the end
+//     the four waves' queues are scored together.
+// lb only rises.  A token left out scores below lb, which some token of the wave's
+// share attains, so the partial equals that of a full scan.  The sampling bounds
+// follow from monotone fp32 rounding: the score is (l * 1/T) + G with both steps
+// rounded and 1/T > 0.  Lanes see tokens out of index order, so their running
+// argmax breaks ties by index.
+template <typename T, int kSeeding, int kN, int kSub, int kW, bool kSample>
 __global__ void __launch_bounds__(kThreads)
-sample_vec_kernel(const T* __restrict__ logits, int64_t row_stride, uint32_t V, int64_t B,
+decode_vec_kernel(const T* __restrict__ logits, int64_t row_stride, uint32_t V, int64_t B,
                   const int32_t* __restrict__ context, int width, uint64_t key, uint32_t tm1,
                   int none_green, float delta, const uint64_t* __restrict__ seeds, float inv_t,
                   uint32_t segments, uint64_t* __restrict__ partials) {
@@ -852,8 +721,12 @@ sample_vec_kernel(const T* __restrict__ logits, int64_t row_stride, uint32_t V, 
   for (int64_t row = blockIdx.y; row < B; row += gridDim.y) {
     const T* row_ptr = logits + row * row_stride;
     const VecT* vec = reinterpret_cast<const VecT*>(row_ptr);
-    const Score<true> sc{seeds[row], inv_t};
-    const RoundKeys nk = vector_round_keys(key_of(sc.seed));
+    Score<kSample> sc{0u, inv_t};
+    RoundKeys nk{};
+    if constexpr (kSample) {
+      sc.seed = seeds[row];
+      nk = vector_round_keys(key_of(sc.seed));
+    }
     const RowSeed<kW> rs = row_seed<kSeeding, kW>(key, context + row * width, width);
     const float dt = fabsf(delta) * inv_t;
     const float dplus = delta > 0.0f ? delta : 0.0f;
@@ -885,8 +758,15 @@ sample_vec_kernel(const T* __restrict__ logits, int64_t row_stride, uint32_t V, 
 #pragma unroll
       for (int n = 0; n < kN; ++n)
         if (whole || sub_first + n * kThreads + threadIdx.x < full) m = fold_max(buf[n], m);
-      const float lb0 = fmaxf(lb, reach_bound(wave_max(m), delta, T{}) * inv_t + kGumbelLo);
       float hi[kN][kE];
+      if constexpr (!kSample) {
+        // Greedy decoding: the largest logit's own value bounds the best from below,
+        // and a token's larger candidate value bounds it from above.
+        lb = fmaxf(lb, reach_bound(wave_max(m), delta, T{}));
+#pragma unroll
+        for (int n = 0; n < kN; ++n) upper_logits(buf[n], delta, dplus, hi[n]);
+      } else {
+      const float lb0 = fmaxf(lb, reach_bound(wave_max(m), delta, T{}) * inv_t + kGumbelLo);
       float top = -INFINITY;    // the lane's largest hi among tokens whose draw has c >= 2
 #pragma unroll
       for (int n = 0; n < kN; ++n) {
@@ -921,13 +801,14 @@ sample_vec_kernel(const T* __restrict__ logits, int64_t row_stride, uint32_t V, 
         const float lb_lane = top < INFINITY ? top - slack : -INFINITY;
         lb = fmaxf(lb0, wave_max(lb_lane));
       }
+      }
 
       // Queue the tokens whose upper bound reaches lb.  The counters are the same in
       // every lane.
 #pragma unroll
       for (int n = 0; n < kN; ++n) {
         if (queued > 64u) {
-          score_queue<T, kSeeding>(best, q_v, q_raw, queued, rs, tm1, none_green, delta, sc);
+          score_queue<T, kSeeding, kW, kSample>(best, q_v, q_raw, queued, rs, tm1, none_green, delta, sc);
           queued = 0;
           lb = fmaxf(lb, wave_max(best.any ? best.v : -INFINITY));
         }
@@ -981,7 +862,8 @@ sample_vec_kernel(const T* __restrict__ logits, int64_t row_stride, uint32_t V, 
         for (int k = 1; k < kThreads / 64; ++k) w += static_cast<uint32_t>(i >= start[k]);
         const uint32_t* wq = lds_queue + w * 2u * kQueueCap;
         const uint32_t off = i - start[w];
-        score_entry<T, kSeeding>(best, wq[off], wq[kQueueCap + off], rs, tm1, none_green, delta, sc);
+        score_entry<T, kSeeding, kW, kSample>(best, wq[off], wq[kQueueCap + off], rs, tm1, none_green,
+                                               delta, sc);
       }
     }
     // The row's partial last vector, element by element, by lane 0 of the segment
@@ -1461,23 +1343,16 @@ void dispatch_candidates(void* logits, int64_t B, uint32_t V, int64_t row_stride
                        p, row_stride, V, B, cand, k, context, width, key, tm1, delta);
 }
 
-// Segments per row of the fused argmax: vector path and element path.
-template <int kSeeding>
-constexpr int argmax_vecs_for() {
-  return kSeeding == kContext ? SBW_ARGMAX_VECS_CONTEXT : SBW_ARGMAX_VECS_SELF_SALT;
+// Segments per row of the fused decoding: vector path and element path.
+template <typename T>
+constexpr int decode_vecs_for() {
+  return sizeof(T) == 4 ? SBW_DECODE_VECS_F32 : SBW_DECODE_VECS_BF16;
 }
 template <typename T>
 constexpr uint64_t vec_segment_elems(int kN) { return (16u / sizeof(T)) * kThreads * kN; }
-// Sampling holds a bound per token in registers: fewer vectors per lane for bf16.
-template <typename T>
-constexpr int sample_vecs_for() {
-  return sizeof(T) == 4 ? SBW_SAMPLE_VECS_F32 : SBW_SAMPLE_VECS_BF16;
-}
 // The workspace is sized for the element path; vector segments must be at least as long.
-static_assert(vec_segment_elems<float>(SBW_ARGMAX_VECS_CONTEXT) >= kArgmaxSegElems &&
-                  vec_segment_elems<float>(SBW_ARGMAX_VECS_SELF_SALT) >= kArgmaxSegElems &&
-                  vec_segment_elems<float>(SBW_SAMPLE_VECS_F32) >= kArgmaxSegElems &&
-                  vec_segment_elems<uint16_t>(SBW_SAMPLE_VECS_BF16) >= kArgmaxSegElems,
+static_assert(vec_segment_elems<float>(SBW_DECODE_VECS_F32) >= kArgmaxSegElems &&
+                  vec_segment_elems<uint16_t>(SBW_DECODE_VECS_BF16) >= kArgmaxSegElems,
               "vector segments must not outnumber element segments");
 
 // The per-row noise seeds and 1/T of a sampling pass (unused by greedy decoding).
@@ -1494,20 +1369,13 @@ void launch_argmax(const void* logits, int64_t B, uint32_t V, int64_t row_stride
   const T* p = static_cast<const T*>(logits);
   const uint32_t rows = static_cast<uint32_t>(B < kMaxGridY ? B : kMaxGridY);
   uint32_t segments;
-  if (aligned && kSample) {
-    constexpr int kN = sample_vecs_for<T>();
-    const uint64_t seg = vec_segment_elems<T>(kN) * SBW_SAMPLE_SUBS;
+  if (aligned) {
+    constexpr int kN = decode_vecs_for<T>();
+    const uint64_t seg = vec_segment_elems<T>(kN) * SBW_DECODE_SUBS;
     segments = static_cast<uint32_t>((static_cast<uint64_t>(V) + seg - 1) / seg);
-    hipLaunchKernelGGL((sample_vec_kernel<T, kSeeding, kN, SBW_SAMPLE_SUBS, kW>), dim3(segments, rows),
-                       dim3(kThreads), 0, stream, p, row_stride, V, B, context, width, key, tm1,
-                       none, delta, sa.seeds, sa.inv_t, segments, partials);
-  } else if (aligned) {
-    constexpr int kN = argmax_vecs_for<kSeeding>();
-    const uint64_t seg = vec_segment_elems<T>(kN);
-    segments = static_cast<uint32_t>((static_cast<uint64_t>(V) + seg - 1) / seg);
-    hipLaunchKernelGGL((argmax_vec_kernel<T, kSeeding, kN, kW>), dim3(segments, rows),
-                       dim3(kThreads), 0, stream, p, row_stride, V, B, context, width, key, tm1,
-                       none, delta, segments, partials);
+    hipLaunchKernelGGL((decode_vec_kernel<T, kSeeding, kN, SBW_DECODE_SUBS, kW, kSample>),
+                       dim3(segments, rows), dim3(kThreads), 0, stream, p, row_stride, V, B, context,
+                       width, key, tm1, none, delta, sa.seeds, sa.inv_t, segments, partials);
   } else {
     segments = static_cast<uint32_t>((static_cast<uint64_t>(V) + kArgmaxSegElems - 1) /
                                      kArgmaxSegElems);
