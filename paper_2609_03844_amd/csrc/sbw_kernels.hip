@@ -468,17 +468,48 @@ __device__ __forceinline__ uint64_t partial_key(uint64_t p) {
   return arg_key(__uint_as_float(static_cast<uint32_t>(p >> 32)), static_cast<uint32_t>(p));
 }
 
+// Wave-wide maximum of 64-bit keys with their 64-bit payloads, by DPP moves (quad
+// permutes, row mirrors, then row broadcasts that carry the maximum to lane 63); no
+// index arithmetic or LDS round trips.  Lanes a move does not reach see key 0, which
+// never wins.  The result is read from lane 63 into every lane.
+template <int kCtrl, int kRowMask>
+__device__ __forceinline__ void dpp_argmax_step(uint64_t& k, uint64_t& p) {
+  const uint32_t k0 = static_cast<uint32_t>(__builtin_amdgcn_update_dpp(
+      0, static_cast<int>(static_cast<uint32_t>(k)), kCtrl, kRowMask, 0xF, false));
+  const uint32_t k1 = static_cast<uint32_t>(__builtin_amdgcn_update_dpp(
+      0, static_cast<int>(static_cast<uint32_t>(k >> 32)), kCtrl, kRowMask, 0xF, false));
+  const uint32_t p0 = static_cast<uint32_t>(__builtin_amdgcn_update_dpp(
+      0, static_cast<int>(static_cast<uint32_t>(p)), kCtrl, kRowMask, 0xF, false));
+  const uint32_t p1 = static_cast<uint32_t>(__builtin_amdgcn_update_dpp(
+      0, static_cast<int>(static_cast<uint32_t>(p >> 32)), kCtrl, kRowMask, 0xF, false));
+  const uint64_t ok = (static_cast<uint64_t>(k1) << 32) | k0;
+  if (ok > k) {
+    k = ok;
+    p = (static_cast<uint64_t>(p1) << 32) | p0;
+  }
+}
+__device__ __forceinline__ uint64_t readlane63(uint64_t x) {
+  const uint32_t lo = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(static_cast<uint32_t>(x)), 63));
+  const uint32_t hi = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(static_cast<uint32_t>(x >> 32)), 63));
+  return (static_cast<uint64_t>(hi) << 32) | lo;
+}
+__device__ __forceinline__ void wave_argmax(uint64_t& k, uint64_t& p) {
+  dpp_argmax_step<0xB1, 0xF>(k, p);    // quad_perm [1,0,3,2]
+  dpp_argmax_step<0x4E, 0xF>(k, p);    // quad_perm [2,3,0,1]
+  dpp_argmax_step<0x141, 0xF>(k, p);   // row_half_mirror
+  dpp_argmax_step<0x140, 0xF>(k, p);   // row_mirror
+  dpp_argmax_step<0x142, 0xA>(k, p);   // row_bcast:15 into rows 1 and 3
+  dpp_argmax_step<0x143, 0xC>(k, p);   // row_bcast:31 into rows 2 and 3
+  k = readlane63(k);
+  p = readlane63(p);
+}
+
 // Block-wide argmax of the lanes' running bests; thread 0 stores the partial.
 __device__ __forceinline__ void block_argmax_store(const LaneBest& lb, uint64_t* out,
                                                    uint64_t* lds_key, uint64_t* lds_part) {
   uint64_t k = lb.any ? arg_key(lb.v, lb.i) : 0u;
   uint64_t p = pack_partial(lb.v, lb.i);
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) {
-    const uint64_t ok = __shfl_xor(k, off, 64);
-    const uint64_t op = __shfl_xor(p, off, 64);
-    if (ok > k) { k = ok; p = op; }
-  }
+  wave_argmax(k, p);
   if (threadIdx.x % 64 == 0) {
     lds_key[threadIdx.x / 64] = k;
     lds_part[threadIdx.x / 64] = p;
@@ -919,12 +950,7 @@ argmax_finish_kernel(const uint64_t* __restrict__ partials, uint32_t segments, i
       const uint64_t k = partial_key(p[s]);
       if (k > bk) { bk = k; bp = p[s]; }
     }
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) {
-      const uint64_t ok = __shfl_xor(bk, off, 64);
-      const uint64_t op = __shfl_xor(bp, off, 64);
-      if (ok > bk) { bk = ok; bp = op; }
-    }
+    wave_argmax(bk, bp);
     if (lane == 0) {
       tokens[b] = static_cast<int32_t>(static_cast<uint32_t>(bp));
       if (values != nullptr) values[b] = __uint_as_float(static_cast<uint32_t>(bp >> 32));
