@@ -1743,6 +1743,6 @@ const char* sbw_strerror(sbw_status_t status) {
 
 const char* sbw_last_hip_error(void) { return hipGetErrorName(g_last_hip_error); }
 
-const char* sbw_version(void) { return "0.3.0"; }
+const char* sbw_version(void) { return "0.4.0"; }
 
 }  // extern "C"
