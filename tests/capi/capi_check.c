@@ -1,0 +1,172 @@
+/*
+ * A plain C client of libsbw: include/sbw.h compiles as C (C11), and the library
+ * links and runs with no Python or torch in the process.  Test infrastructure: it
+ * links the CPU oracle (oracle/sbw_oracle.c) to check the results.
+ *
+ *   capi_check cpu   version string, status texts, and the argument checks that
+ *                    return before any HIP call (no GPU needed).
+ *   capi_check gpu   watermark (context and self-salt, window of 4, fp32), greedy
+ *                    decoding, Gumbel-max sampling and detection on HIP device
+ *                    buffers, each compared bit for bit with the oracle (z within
+ *                    1e-6 relative).
+ *
+ * Inputs come from a xorshift64* generator seeded per case.  Prints one line per
+ * check and exits non-zero on the first mismatch.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdio.h>
+#include <stdlib.h>
+#include <string.h>
+
+#include <hip/hip_runtime_api.h>
+
+#include "sbw.h"
+
+/* The oracle's C entry points used here (oracle/sbw_oracle.c). */
+void oracle_watermark_f32_w(float *logits, int64_t B, int64_t V, int64_t row_stride,
+                            const int32_t *context, int64_t width, uint64_t key, double gamma,
+                            float delta, int seeding);
+void oracle_watermark_argmax_f32_w(const float *logits, int64_t B, int64_t V, int64_t row_stride,
+                                   const int32_t *context, int64_t width, uint64_t key,
+                                   double gamma, float delta, int seeding, int32_t *tokens,
+                                   float *values);
+void oracle_watermark_sample_f32_w(const float *logits, int64_t B, int64_t V, int64_t row_stride,
+                                   const int32_t *context, int64_t width, uint64_t key,
+                                   double gamma, float delta, int seeding, const uint64_t *seeds,
+                                   float inv_temperature, int32_t *tokens, float *scores);
+void oracle_detect_w(const int32_t *tokens, int64_t N, int64_t L, int64_t row_stride,
+                     int64_t width, uint64_t key, double gamma, int seeding,
+                     int32_t *green_counts, double *z);
+
+static uint64_t rng_state;
+static uint64_t next_u64(void)
+{
+    rng_state ^= rng_state >> 12;
+    rng_state ^= rng_state << 25;
+    rng_state ^= rng_state >> 27;
+    return rng_state * 0x2545F4914F6CDD1DULL;
+}
+static float next_logit(void) { return (float)((double)(next_u64() >> 11) * 0x1p-53 * 8.0 - 4.0); }
+
+#define CHECK(cond, ...)                                                   \
+    do {                                                                   \
+        if (!(cond)) {                                                     \
+            fprintf(stderr, "capi_check: FAILED: " __VA_ARGS__);           \
+            fprintf(stderr, "\n");                                         \
+            exit(1);                                                       \
+        }                                                                  \
+    } while (0)
+#define HIP(call) CHECK((call) == hipSuccess, "%s", #call)
+#define SBW(call) do { sbw_status_t s_ = (call); CHECK(s_ == SBW_OK, "%s -> %s", #call, sbw_strerror(s_)); } while (0)
+
+static int cpu_checks(void)
+{
+    const char *v = sbw_version();
+    CHECK(v != NULL && strlen(v) >= 5, "version");
+    CHECK(strlen(sbw_strerror(SBW_ERR_GAMMA)) > 0 && strlen(sbw_strerror((sbw_status_t)99)) > 0, "strerror");
+    float dummy = 0.0f;
+    int32_t prev = 0;
+    /* each of these fails its argument check before any HIP call */
+    CHECK(sbw_watermark(NULL, SBW_F32, 1, 1, 1, &prev, 1, 0.25, 2.0f, SBW_SEED_CONTEXT, NULL) == SBW_ERR_INVALID_ARG, "null logits");
+    CHECK(sbw_watermark(&dummy, SBW_F32, 1, 2, 1, &prev, 1, 0.25, 2.0f, SBW_SEED_CONTEXT, NULL) == SBW_ERR_INVALID_ARG, "row_stride < V");
+    CHECK(sbw_watermark(&dummy, SBW_F32, 1, 1, 1, &prev, 1, 1.5, 2.0f, SBW_SEED_CONTEXT, NULL) == SBW_ERR_GAMMA, "gamma > 1");
+    CHECK(sbw_watermark(&dummy, SBW_F32, 1, 1, 1, &prev, 1, 0.25, INFINITY, SBW_SEED_CONTEXT, NULL) == SBW_ERR_DELTA, "delta inf");
+    CHECK(sbw_watermark(&dummy, (sbw_dtype_t)7, 1, 1, 1, &prev, 1, 0.25, 2.0f, SBW_SEED_CONTEXT, NULL) == SBW_ERR_UNSUPPORTED, "dtype");
+    CHECK(sbw_watermark(&dummy, SBW_F32, 0, 1, 1, &prev, 1, 0.25, 2.0f, SBW_SEED_CONTEXT, NULL) == SBW_OK, "B = 0 is a no-op");
+    CHECK(sbw_watermark_argmax_workspace(256, 152064) == 256 * 75, "workspace size");
+    CHECK(sbw_watermark_argmax_workspace(0, 5) == 0, "workspace of nothing");
+    printf("capi cpu ok: libsbw %s\n", v);
+    return 0;
+}
+
+static int gpu_checks(void)
+{
+    const int64_t B = 8, V = 50001, W = 4, N = 16, L = 300;
+    const uint64_t key = 0x243F6A8885A308D3ULL;
+    const double gamma = 0.25;
+    const float delta = 2.0f, inv_t = 0.8f;
+    size_t nl = (size_t)(B * V);
+    float *x = malloc(nl * sizeof(float)), *expect = malloc(nl * sizeof(float)),
+          *got = malloc(nl * sizeof(float));
+    int32_t ctx[8 * 4], tok[16 * 300], etok[8], gtok[8], ecount[16], gcount[16];
+    float evals[8], gvals[8];
+    uint64_t seeds[8];
+    double ez[16], gz[16];
+    CHECK(x && expect && got, "host allocation");
+    rng_state = 0x9E3779B97F4A7C15ULL;
+    for (size_t i = 0; i < nl; ++i) x[i] = next_logit();
+    x[3 * V + 777] = NAN;                           /* a NaN row: its first NaN wins */
+    for (int i = 0; i < B * W; ++i) ctx[i] = (int32_t)(next_u64() % (uint64_t)V);
+    for (int i = 0; i < B; ++i) seeds[i] = next_u64();
+    for (int i = 0; i < N * L; ++i) tok[i] = (int32_t)(next_u64() % (uint64_t)V);
+
+    float *d_x, *d_vals;
+    int32_t *d_ctx, *d_tok, *d_tokens, *d_count;
+    uint64_t *d_seeds, *d_ws;
+    double *d_z;
+    const int64_t ws = sbw_watermark_argmax_workspace(B, V);
+    HIP(hipMalloc((void **)&d_x, nl * sizeof(float)));
+    HIP(hipMalloc((void **)&d_vals, B * sizeof(float)));
+    HIP(hipMalloc((void **)&d_ctx, sizeof ctx));
+    HIP(hipMalloc((void **)&d_tok, sizeof tok));
+    HIP(hipMalloc((void **)&d_tokens, B * sizeof(int32_t)));
+    HIP(hipMalloc((void **)&d_count, N * sizeof(int32_t)));
+    HIP(hipMalloc((void **)&d_seeds, sizeof seeds));
+    HIP(hipMalloc((void **)&d_ws, (size_t)ws * sizeof(uint64_t)));
+    HIP(hipMalloc((void **)&d_z, N * sizeof(double)));
+    HIP(hipMemcpy(d_ctx, ctx, sizeof ctx, hipMemcpyHostToDevice));
+    HIP(hipMemcpy(d_tok, tok, sizeof tok, hipMemcpyHostToDevice));
+    HIP(hipMemcpy(d_seeds, seeds, sizeof seeds, hipMemcpyHostToDevice));
+
+    for (int seeding = 0; seeding < 2; ++seeding) {
+        const sbw_seeding_t sd = (sbw_seeding_t)seeding;
+        /* greedy decoding and sampling read the unmodified logits */
+        HIP(hipMemcpy(d_x, x, nl * sizeof(float), hipMemcpyHostToDevice));
+        SBW(sbw_watermark_argmax(d_x, SBW_F32, B, V, V, d_ctx, W, key, gamma, delta, sd,
+                                 d_tokens, d_vals, d_ws, NULL));
+        HIP(hipMemcpy(gtok, d_tokens, sizeof gtok, hipMemcpyDeviceToHost));
+        HIP(hipMemcpy(gvals, d_vals, sizeof gvals, hipMemcpyDeviceToHost));
+        oracle_watermark_argmax_f32_w(x, B, V, V, ctx, W, key, gamma, delta, seeding, etok, evals);
+        CHECK(memcmp(gtok, etok, sizeof etok) == 0 && memcmp(gvals, evals, sizeof evals) == 0,
+              "argmax, seeding %d", seeding);
+        SBW(sbw_watermark_sample(d_x, SBW_F32, B, V, V, d_ctx, W, key, gamma, delta, sd, d_seeds,
+                                 inv_t, d_tokens, d_vals, d_ws, NULL));
+        HIP(hipMemcpy(gtok, d_tokens, sizeof gtok, hipMemcpyDeviceToHost));
+        HIP(hipMemcpy(gvals, d_vals, sizeof gvals, hipMemcpyDeviceToHost));
+        oracle_watermark_sample_f32_w(x, B, V, V, ctx, W, key, gamma, delta, seeding, seeds, inv_t,
+                                      etok, evals);
+        CHECK(memcmp(gtok, etok, sizeof etok) == 0 && memcmp(gvals, evals, sizeof evals) == 0,
+              "sample, seeding %d", seeding);
+        CHECK(gtok[3] == 777, "the NaN logit wins the sample");
+        /* then the watermark in place */
+        SBW(sbw_watermark_window(d_x, SBW_F32, B, V, V, d_ctx, W, key, gamma, delta, sd, NULL));
+        HIP(hipMemcpy(got, d_x, nl * sizeof(float), hipMemcpyDeviceToHost));
+        memcpy(expect, x, nl * sizeof(float));
+        oracle_watermark_f32_w(expect, B, V, V, ctx, W, key, gamma, delta, seeding);
+        CHECK(memcmp(got, expect, nl * sizeof(float)) == 0, "watermark, seeding %d", seeding);
+        /* detection */
+        SBW(sbw_detect_window(d_tok, N, L, L, W, key, gamma, sd, d_count, d_z, NULL));
+        HIP(hipMemcpy(gcount, d_count, sizeof gcount, hipMemcpyDeviceToHost));
+        HIP(hipMemcpy(gz, d_z, sizeof gz, hipMemcpyDeviceToHost));
+        oracle_detect_w(tok, N, L, L, W, key, gamma, seeding, ecount, ez);
+        CHECK(memcmp(gcount, ecount, sizeof ecount) == 0, "detect counts, seeding %d", seeding);
+        for (int i = 0; i < N; ++i)
+            CHECK(fabs(gz[i] - ez[i]) <= 1e-6 * fabs(ez[i]) + 1e-12, "detect z, seeding %d", seeding);
+        printf("capi gpu seeding %d ok\n", seeding);
+    }
+    HIP(hipFree(d_x)); HIP(hipFree(d_vals)); HIP(hipFree(d_ctx)); HIP(hipFree(d_tok));
+    HIP(hipFree(d_tokens)); HIP(hipFree(d_count)); HIP(hipFree(d_seeds)); HIP(hipFree(d_ws));
+    HIP(hipFree(d_z));
+    free(x); free(expect); free(got);
+    printf("capi gpu ok\n");
+    return 0;
+}
+
+int main(int argc, char **argv)
+{
+    if (argc == 2 && strcmp(argv[1], "cpu") == 0) return cpu_checks();
+    if (argc == 2 && strcmp(argv[1], "gpu") == 0) return gpu_checks();
+    fprintf(stderr, "usage: capi_check cpu|gpu\n");
+    return 2;
+}
