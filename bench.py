@@ -295,6 +295,22 @@ def other_configs(torch, sbw, dev, steps, c5_tokens):
         big[seeding] = {"us": us, "gelem_per_s": n / us / 1e3,
                         "hbm_gbps": 8 * n / us / 1e3, "hbm_frac": 8 * n / us / 1e3 / HBM_PEAK_GBPS}
     res["c4_B1024"] = big
+    # greedy decoding and sampling fused with the watermark at B=1024 (logits read only)
+    tokens = torch.empty(c["B_large"], dtype=torch.int32, device=dev)
+    values = torch.empty(c["B_large"], dtype=torch.float32, device=dev)
+    ws = torch.empty(sbw.argmax_workspace_size(c["B_large"], c["V"]), dtype=torch.int64, device=dev)
+    seeds = torch.arange(1, c["B_large"] + 1, dtype=torch.int64, device=dev)
+    dec = {}
+    for seeding in ("context", "self_salt"):
+        us = _mean_us(torch, lambda i, s=seeding: sbw.watermark_argmax(
+            bufs[i % len(bufs)], p, key, c["gamma"], c["delta"], s, tokens=tokens, values=values,
+            workspace=ws), max(20, steps // 4))
+        dec[f"argmax/{seeding}"] = {"us": us, "gelem_per_s": n / us / 1e3, "hbm_frac": 4 * n / us / 1e3 / HBM_PEAK_GBPS}
+        us = _mean_us(torch, lambda i, s=seeding: sbw.watermark_sample(
+            bufs[i % len(bufs)], p, key, c["gamma"], c["delta"], seeds, s, 1.0, tokens=tokens,
+            scores=values, workspace=ws), max(20, steps // 4))
+        dec[f"sample/{seeding}"] = {"us": us, "gelem_per_s": n / us / 1e3, "hbm_frac": 4 * n / us / 1e3 / HBM_PEAK_GBPS}
+    res["c4_B1024_decode"] = dec
     del bufs
     torch.cuda.empty_cache()
     return res
