@@ -247,6 +247,38 @@ def other_configs(torch, sbw, dev, steps, c5_tokens):
     res["c4_watermark_sample"] = sampled
     del bufs
 
+    # one GPU's share of the c4 vocabulary split 8 ways (a tensor-parallel LM head): B=256
+    # rows of 19008 columns holding token ids 57024..76031, through the shard entry points
+    c = workloads.C4
+    n_sh = c["V"] // 8
+    v0 = 3 * n_sh
+    x, prev = workloads.watermark_inputs("c4")
+    bufs = rotating(np.ascontiguousarray(x[:, v0:v0 + n_sh]))
+    p = torch.from_numpy(prev).to(dev)
+    n = c["B"] * n_sh
+    tokens = torch.empty(c["B"], dtype=torch.int32, device=dev)
+    values = torch.empty(c["B"], dtype=torch.float32, device=dev)
+    ws = torch.empty(sbw.argmax_workspace_size(c["B"], n_sh), dtype=torch.int64, device=dev)
+    seeds = torch.arange(1, c["B"] + 1, dtype=torch.int64, device=dev)
+    shard = {"columns": n_sh, "v_offset": v0}
+    for seeding in ("context", "self_salt"):
+        us = _mean_us(torch, lambda i, s=seeding: sbw.watermark_shard(
+            bufs[i % len(bufs)], p, v0, key, c["gamma"], c["delta"], s), steps)
+        shard[f"watermark/{seeding}"] = {"us": us, "gelem_per_s": n / us / 1e3,
+                                         "hbm_frac": 8 * n / us / 1e3 / HBM_PEAK_GBPS}
+        us = _mean_us(torch, lambda i, s=seeding: sbw.watermark_argmax_shard(
+            bufs[i % len(bufs)], p, v0, key, c["gamma"], c["delta"], s, tokens=tokens,
+            values=values, workspace=ws), steps)
+        shard[f"argmax/{seeding}"] = {"us": us, "gelem_per_s": n / us / 1e3,
+                                      "hbm_frac": 4 * n / us / 1e3 / HBM_PEAK_GBPS}
+        us = _mean_us(torch, lambda i, s=seeding: sbw.watermark_sample_shard(
+            bufs[i % len(bufs)], p, v0, key, c["gamma"], c["delta"], seeds, s, 1.0,
+            tokens=tokens, scores=values, workspace=ws), steps)
+        shard[f"sample/{seeding}"] = {"us": us, "gelem_per_s": n / us / 1e3,
+                                      "hbm_frac": 4 * n / us / 1e3 / HBM_PEAK_GBPS}
+    res["c4_tp8_shard"] = shard
+    del bufs
+
     # SBW-ss on the c4 batch: the self-salt watermark (width 4) on the top-40 ids only
     c = workloads.C4
     x, _ = workloads.watermark_inputs("c4")

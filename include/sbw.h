@@ -293,6 +293,45 @@ sbw_status_t sbw_watermark_sample(const void *logits, sbw_dtype_t dtype, int64_t
  * V logits: B * ceil(V / 2048) (0 when B or V is not positive). */
 int64_t sbw_watermark_argmax_workspace(int64_t B, int64_t V);
 
+/*
+ * Vocabulary shards.  A token's colour depends only on the row's seed and on its own
+ * id (Sec. 2.2: membership is one CBRNG draw at counter v, with no list to build), and
+ * so does its sampling noise.  A slice of the vocabulary can therefore be watermarked,
+ * and its best token found, on its own: this is what a tensor-parallel LM head holds
+ * on each device.  These calls treat column c of each row as token v_offset + c.
+ *
+ *   logits       device, [B, row_stride]: the shard's columns, V of them per row.
+ *   v_offset     global id of column 0, >= 0 (else SBW_ERR_INVALID_ARG), with
+ *                v_offset + V <= 2^32 (else SBW_ERR_UNSUPPORTED).
+ *   tokens       (argmax, sample) written as global ids, v_offset + c.
+ * Every other argument, layout and error as for the unsharded call, which is the
+ * same call with v_offset = 0.  The rows of all shards of a vocabulary, put side by
+ * side, are biased exactly as the full rows are.  For decoding, the full row's token
+ * is the shards' winner with the largest value (or score), the smallest global id
+ * among equal ones, a NaN above everything: the reduction the unsharded call makes
+ * over its own segments.  Rows whose first id is not a multiple of 4 (fp32) or 8
+ * (bf16) take the element-wise kernels, which give the same results.
+ */
+sbw_status_t sbw_watermark_shard(void *logits, sbw_dtype_t dtype, int64_t B, int64_t V,
+                                 int64_t row_stride, const int32_t *context, int64_t width,
+                                 int64_t v_offset, uint64_t key, double gamma, float delta,
+                                 sbw_seeding_t seeding, void *stream);
+
+sbw_status_t sbw_watermark_argmax_shard(const void *logits, sbw_dtype_t dtype, int64_t B,
+                                        int64_t V, int64_t row_stride, const int32_t *context,
+                                        int64_t width, int64_t v_offset, uint64_t key,
+                                        double gamma, float delta, sbw_seeding_t seeding,
+                                        int32_t *tokens, float *values, uint64_t *workspace,
+                                        void *stream);
+
+sbw_status_t sbw_watermark_sample_shard(const void *logits, sbw_dtype_t dtype, int64_t B,
+                                        int64_t V, int64_t row_stride, const int32_t *context,
+                                        int64_t width, int64_t v_offset, uint64_t key,
+                                        double gamma, float delta, sbw_seeding_t seeding,
+                                        const uint64_t *seeds, float inv_temperature,
+                                        int32_t *tokens, float *scores, uint64_t *workspace,
+                                        void *stream);
+
 /* Static description of a status code (never NULL). */
 const char *sbw_strerror(sbw_status_t status);
 

@@ -7,11 +7,16 @@ fallback: if the library is missing this module raises on import.
 
     watermark(logits, prev_tokens, key, gamma, delta, seeding="context")   in place
     watermark_argmax(logits, prev_tokens, key, gamma, delta) -> (tokens [B], values [B])
+    watermark_sample(logits, prev_tokens, key, gamma, delta, seeds) -> (tokens [B], scores [B])
     green_mask(prev_tokens, V, key, gamma, seeding="context") -> int32 [B, ceil(V/32)]
     detect(tokens, key, gamma, seeding="context") -> (counts int32 [N], z float64 [N])
 
 Tensors are torch tensors on the current HIP device; torch provides the memory
 and the stream, nothing else.
+
+The three logits calls take ``v_offset``: the logits are then one vocabulary shard,
+column c being token v_offset + c (``sbw_*_shard`` in the C ABI); ``watermark_shard``,
+``watermark_argmax_shard`` and ``watermark_sample_shard`` are the same calls.
 """
 from __future__ import annotations
 
@@ -22,8 +27,10 @@ import torch  # loads torch's HIP runtime first, so libsbw binds to the same one
 
 from ._build import LIBRARY, build  # noqa: F401  (build is re-exported)
 
-__all__ = ["watermark", "watermark_argmax", "green_mask", "detect", "SbwError", "version",
-           "library_path", "SEED_CONTEXT", "SEED_SELF_SALT"]
+__all__ = ["watermark", "watermark_argmax", "watermark_sample", "watermark_shard",
+           "watermark_argmax_shard", "watermark_sample_shard", "watermark_candidates",
+           "green_mask", "detect", "detect_ex", "SbwError", "version", "library_path",
+           "SEED_CONTEXT", "SEED_SELF_SALT"]
 
 SEED_CONTEXT = 0
 SEED_SELF_SALT = 1
@@ -43,7 +50,8 @@ _STATUS = {
 EXPORTED = ("sbw_watermark", "sbw_green_mask", "sbw_detect", "sbw_watermark_window",
             "sbw_green_mask_window", "sbw_detect_window", "sbw_watermark_argmax",
             "sbw_watermark_argmax_workspace", "sbw_watermark_candidates", "sbw_detect_ex",
-            "sbw_watermark_sample",
+            "sbw_watermark_sample", "sbw_watermark_shard", "sbw_watermark_argmax_shard",
+            "sbw_watermark_sample_shard",
             "sbw_strerror", "sbw_last_hip_error", "sbw_version")
 DETECT_IGNORE_REPEATED = 1
 MAX_UNIQUE_POSITIONS = 4096
@@ -87,6 +95,14 @@ def _load() -> ctypes.CDLL:
     lib.sbw_watermark_sample.restype = i32
     lib.sbw_watermark_sample.argtypes = [P, i32, i64, i64, i64, P, i64, u64, f64, f32, i32, P, f32,
                                          P, P, P, P]
+    lib.sbw_watermark_shard.restype = i32
+    lib.sbw_watermark_shard.argtypes = [P, i32, i64, i64, i64, P, i64, i64, u64, f64, f32, i32, P]
+    lib.sbw_watermark_argmax_shard.restype = i32
+    lib.sbw_watermark_argmax_shard.argtypes = [P, i32, i64, i64, i64, P, i64, i64, u64, f64, f32,
+                                               i32, P, P, P, P]
+    lib.sbw_watermark_sample_shard.restype = i32
+    lib.sbw_watermark_sample_shard.argtypes = [P, i32, i64, i64, i64, P, i64, i64, u64, f64, f32,
+                                               i32, P, f32, P, P, P, P]
     lib.sbw_detect_ex.restype = i32
     lib.sbw_detect_ex.argtypes = [P, i64, i64, i64, P, i64, u64, f64, i32, ctypes.c_uint32, P, P,
                                   P, P]
@@ -176,12 +192,13 @@ def _window(context: torch.Tensor, B: int):
 
 
 def watermark(logits: torch.Tensor, prev_tokens: torch.Tensor, key: int, gamma: float,
-              delta: float, seeding="context", stream=None) -> torch.Tensor:
+              delta: float, seeding="context", stream=None, v_offset: int = 0) -> torch.Tensor:
     """Adds delta to the green logits of every row, in place; returns ``logits``.
 
     logits: [B, V] float32 or bfloat16 on the GPU, unit stride along V (rows may be
     padded: stride(0) >= V).  prev_tokens: int32 [B] (the previous token of each row)
-    or int32 [B, h] (the h tokens before the step, context width h <= 8).
+    or int32 [B, h] (the h tokens before the step, context width h <= 8).  v_offset:
+    the token id of column 0 when the logits are one shard of the vocabulary.
     """
     if logits.dim() != 2:
         raise ValueError("logits must be [B, V]")
@@ -198,9 +215,14 @@ def watermark(logits: torch.Tensor, prev_tokens: torch.Tensor, key: int, gamma: 
     row_stride = logits.stride(0) if B > 1 else max(V, logits.stride(0))
     seed_kind = _seeding(seeding)
     _on_device(logits=logits, prev_tokens=context)
-    _check(_lib.sbw_watermark_window(logits.data_ptr(), dtype, B, V, row_stride,
-                                     context.data_ptr(), width, _key(key), float(gamma),
-                                     float(delta), seed_kind, _stream(stream)))
+    if v_offset == 0:
+        _check(_lib.sbw_watermark_window(logits.data_ptr(), dtype, B, V, row_stride,
+                                         context.data_ptr(), width, _key(key), float(gamma),
+                                         float(delta), seed_kind, _stream(stream)))
+    else:
+        _check(_lib.sbw_watermark_shard(logits.data_ptr(), dtype, B, V, row_stride,
+                                        context.data_ptr(), width, int(v_offset), _key(key),
+                                        float(gamma), float(delta), seed_kind, _stream(stream)))
     return logits
 
 
@@ -237,12 +259,13 @@ def watermark_candidates(logits: torch.Tensor, prev_tokens: torch.Tensor,
 def watermark_argmax(logits: torch.Tensor, prev_tokens: torch.Tensor, key: int, gamma: float,
                      delta: float, seeding="context", tokens: torch.Tensor | None = None,
                      values: torch.Tensor | None = None, workspace: torch.Tensor | None = None,
-                     with_values: bool = True, stream=None):
+                     with_values: bool = True, stream=None, v_offset: int = 0):
     """Greedy decoding of the watermarked logits in one read-only pass.
 
     Returns (tokens int32 [B], values float32 [B] or None).  ``workspace`` is an int64
     scratch tensor of at least argmax_workspace_size(B, V) elements (allocated here
-    when not given)."""
+    when not given).  With v_offset the logits are a vocabulary shard and the tokens
+    global ids."""
     if logits.dim() != 2:
         raise ValueError("logits must be [B, V]")
     if logits.dtype == torch.float32:
@@ -274,11 +297,18 @@ def watermark_argmax(logits: torch.Tensor, prev_tokens: torch.Tensor, key: int, 
     row_stride = logits.stride(0) if B > 1 else max(V, logits.stride(0))
     _on_device(logits=logits, prev_tokens=context, tokens=tokens, values=values,
                workspace=workspace)
-    _check(_lib.sbw_watermark_argmax(logits.data_ptr(), dtype, B, V, row_stride,
-                                     context.data_ptr(), width, _key(key), float(gamma),
-                                     float(delta), _seeding(seeding), tokens.data_ptr(),
-                                     values.data_ptr() if values is not None else None,
-                                     workspace.data_ptr(), _stream(stream)))
+    vptr = values.data_ptr() if values is not None else None
+    if v_offset == 0:
+        _check(_lib.sbw_watermark_argmax(logits.data_ptr(), dtype, B, V, row_stride,
+                                         context.data_ptr(), width, _key(key), float(gamma),
+                                         float(delta), _seeding(seeding), tokens.data_ptr(), vptr,
+                                         workspace.data_ptr(), _stream(stream)))
+    else:
+        _check(_lib.sbw_watermark_argmax_shard(logits.data_ptr(), dtype, B, V, row_stride,
+                                               context.data_ptr(), width, int(v_offset),
+                                               _key(key), float(gamma), float(delta),
+                                               _seeding(seeding), tokens.data_ptr(), vptr,
+                                               workspace.data_ptr(), _stream(stream)))
     return tokens, values
 
 
@@ -286,10 +316,11 @@ def watermark_sample(logits: torch.Tensor, prev_tokens: torch.Tensor, key: int, 
                      delta: float, seeds: torch.Tensor, seeding="context",
                      inv_temperature: float = 1.0, tokens: torch.Tensor | None = None,
                      scores: torch.Tensor | None = None, workspace: torch.Tensor | None = None,
-                     with_scores: bool = True, stream=None):
+                     with_scores: bool = True, stream=None, v_offset: int = 0):
     """One draw per row from softmax(watermarked logits * inv_temperature), fused
     (Gumbel-max with noise from seeds, uint64 [B] as an int64 tensor).  Returns (tokens
-    int32 [B], scores float32 [B] or None); the workspace is as for watermark_argmax."""
+    int32 [B], scores float32 [B] or None); the workspace and v_offset are as for
+    watermark_argmax."""
     if logits.dim() != 2:
         raise ValueError("logits must be [B, V]")
     if logits.dtype == torch.float32:
@@ -324,13 +355,42 @@ def watermark_sample(logits: torch.Tensor, prev_tokens: torch.Tensor, key: int, 
     seed_kind = _seeding(seeding)
     _on_device(logits=logits, prev_tokens=context, seeds=seeds, tokens=tokens, scores=scores,
                workspace=workspace)
-    _check(_lib.sbw_watermark_sample(logits.data_ptr(), dtype, B, V, row_stride,
-                                     context.data_ptr(), width, _key(key), float(gamma),
-                                     float(delta), seed_kind, seeds.data_ptr(),
-                                     float(inv_temperature), tokens.data_ptr(),
-                                     scores.data_ptr() if scores is not None else None,
-                                     workspace.data_ptr(), _stream(stream)))
+    sptr = scores.data_ptr() if scores is not None else None
+    if v_offset == 0:
+        _check(_lib.sbw_watermark_sample(logits.data_ptr(), dtype, B, V, row_stride,
+                                         context.data_ptr(), width, _key(key), float(gamma),
+                                         float(delta), seed_kind, seeds.data_ptr(),
+                                         float(inv_temperature), tokens.data_ptr(), sptr,
+                                         workspace.data_ptr(), _stream(stream)))
+    else:
+        _check(_lib.sbw_watermark_sample_shard(logits.data_ptr(), dtype, B, V, row_stride,
+                                               context.data_ptr(), width, int(v_offset),
+                                               _key(key), float(gamma), float(delta), seed_kind,
+                                               seeds.data_ptr(), float(inv_temperature),
+                                               tokens.data_ptr(), sptr, workspace.data_ptr(),
+                                               _stream(stream)))
     return tokens, scores
+
+
+def watermark_shard(logits: torch.Tensor, prev_tokens: torch.Tensor, v_offset: int, key: int,
+                    gamma: float, delta: float, seeding="context", stream=None) -> torch.Tensor:
+    """watermark() of one vocabulary shard: column c of logits is token v_offset + c."""
+    return watermark(logits, prev_tokens, key, gamma, delta, seeding, stream, v_offset=v_offset)
+
+
+def watermark_argmax_shard(logits: torch.Tensor, prev_tokens: torch.Tensor, v_offset: int,
+                           key: int, gamma: float, delta: float, seeding="context", **kw):
+    """watermark_argmax() of one vocabulary shard; the tokens are global ids."""
+    return watermark_argmax(logits, prev_tokens, key, gamma, delta, seeding, v_offset=v_offset,
+                            **kw)
+
+
+def watermark_sample_shard(logits: torch.Tensor, prev_tokens: torch.Tensor, v_offset: int,
+                           key: int, gamma: float, delta: float, seeds: torch.Tensor,
+                           seeding="context", inv_temperature: float = 1.0, **kw):
+    """watermark_sample() of one vocabulary shard; the tokens are global ids."""
+    return watermark_sample(logits, prev_tokens, key, gamma, delta, seeds, seeding,
+                            inv_temperature, v_offset=v_offset, **kw)
 
 
 def argmax_workspace_size(B: int, V: int) -> int:

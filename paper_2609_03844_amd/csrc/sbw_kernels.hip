@@ -188,10 +188,11 @@ __device__ __forceinline__ uint16_t bias_elem(uint16_t l, float d, bool g) {
   return bias_bf16(l, d, g);
 }
 
+// One token: column v of the row, token id vbase + v.
 template <typename T, int kSeeding, int kW>
 __device__ __forceinline__ void bias_one(T* row, uint32_t v, const RowSeed<kW>& rs, uint32_t tm1,
-                                         float delta) {
-  const uint32_t x = draw<kSeeding>(rs, v);
+                                         float delta, uint32_t vbase) {
+  const uint32_t x = draw<kSeeding>(rs, vbase + v);
   row[v] = bias_elem(row[v], delta, is_green(x, tm1));
 }
 
@@ -203,11 +204,12 @@ template <typename T, int kU, int kW>
 __global__ void __launch_bounds__(kThreads)
 watermark_vec_kernel(T* __restrict__ logits, int64_t row_stride, uint32_t V, int64_t B,
                      const int32_t* __restrict__ context, int width, uint64_t key, uint32_t tm1,
-                     float delta) {
+                     float delta, uint32_t vbase) {
   using VecT = typename std::conditional<sizeof(T) == 4, f32x4, u32x4>::type;
   constexpr uint32_t kPer = 16u / sizeof(T);  // elements per 16-byte vector
   const uint32_t full = V / kPer;             // complete vectors in a row
   const uint32_t tail = V % kPer;
+  const uint32_t jbase = vbase / kPer;        // vector index of the first column (vbase % 8 == 0)
   const uint32_t first = blockIdx.x * (kThreads * kU);
   for (int64_t row = blockIdx.y; row < B; row += gridDim.y) {
     T* row_ptr = logits + row * row_stride;
@@ -222,7 +224,7 @@ watermark_vec_kernel(T* __restrict__ logits, int64_t row_stride, uint32_t V, int
 #pragma unroll
       for (int u = 0; u < kU; ++u) {
         const uint32_t j = first + u * kThreads + threadIdx.x;
-        stream_store(vec + j, bias_vec_context(buf[u], j, rs.seed, tm1, delta));
+        stream_store(vec + j, bias_vec_context(buf[u], j + jbase, rs.seed, tm1, delta));
       }
     } else {
 #pragma unroll
@@ -234,14 +236,14 @@ watermark_vec_kernel(T* __restrict__ logits, int64_t row_stride, uint32_t V, int
 #pragma unroll
       for (int u = 0; u < kU; ++u) {
         const uint32_t j = first + u * kThreads + threadIdx.x;
-        if (j < full) stream_store(vec + j, bias_vec_context(buf[u], j, rs.seed, tm1, delta));
+        if (j < full) stream_store(vec + j, bias_vec_context(buf[u], j + jbase, rs.seed, tm1, delta));
       }
       // The partial vector at the end of the row, element by element, by lane 0 of
       // the tile that covers vector index `full`.
       if (tail != 0u && threadIdx.x == 0 && full >= first &&
           full - first < static_cast<uint32_t>(kThreads * kU)) {
         for (uint32_t e = 0; e < tail; ++e)
-          bias_one<T, kContext>(row_ptr, full * kPer + e, rs, tm1, delta);
+          bias_one<T, kContext>(row_ptr, full * kPer + e, rs, tm1, delta, vbase);
       }
     }
   }
@@ -294,12 +296,14 @@ template <typename T, int kU, int kW, int kRows, bool kPrefetch>
 __global__ void __launch_bounds__(kThreads)
 watermark_ss_rows_kernel(T* __restrict__ logits, int64_t row_stride, uint32_t V, int64_t B,
                          const int32_t* __restrict__ context, int width, uint64_t key, uint32_t tm1,
-                         float delta) {
+                         float delta, uint32_t vbase) {
   using VecT = typename std::conditional<sizeof(T) == 4, f32x4, u32x4>::type;
   constexpr uint32_t kPer = 16u / sizeof(T);
   const uint32_t full = V / kPer;
   const uint32_t tail = V % kPer;
   const uint32_t first = blockIdx.x * (kThreads * kU);
+  // the tile's first vector counted in token ids (vbase is a multiple of kPer)
+  const uint32_t id_first = first + vbase / kPer;
   const bool whole = first + kThreads * kU <= full;
   const int64_t groups = (B + kRows - 1) / kRows;
   auto load_group = [&](VecT (&buf)[kRows][kU], int64_t g) {
@@ -329,13 +333,15 @@ watermark_ss_rows_kernel(T* __restrict__ logits, int64_t row_stride, uint32_t V,
 #pragma unroll
         for (int u = 0; u < kU; ++u) {
           const uint32_t j = first + u * kThreads + threadIdx.x;
-          if (whole || j < full) stream_store(vec + j, bias_vec_terms(buf[r][u], j, ct[u], rs, tm1, delta));
+          if (whole || j < full)
+            stream_store(vec + j, bias_vec_terms(buf[r][u], id_first + u * kThreads + threadIdx.x,
+                                                 ct[u], rs, tm1, delta));
         }
         // the row's partial last vector, by lane 0 of the tile that covers it
         if (!whole && tail != 0u && threadIdx.x == 0 && full >= first &&
             full - first < static_cast<uint32_t>(kThreads * kU)) {
           for (uint32_t e = 0; e < tail; ++e)
-            bias_one<T, kSelfSalt>(row_ptr, full * kPer + e, rs, tm1, delta);
+            bias_one<T, kSelfSalt>(row_ptr, full * kPer + e, rs, tm1, delta, vbase);
         }
       }
     }
@@ -348,7 +354,7 @@ watermark_ss_rows_kernel(T* __restrict__ logits, int64_t row_stride, uint32_t V,
   for (int u = 0; u < kU; ++u)
 #pragma unroll
     for (uint32_t e = 0; e < kPer; ++e)
-      ct[u][e] = cand_term(key, (first + u * kThreads + threadIdx.x) * kPer + e);
+      ct[u][e] = cand_term(key, (id_first + u * kThreads + threadIdx.x) * kPer + e);
   if constexpr (!kPrefetch) {
     for (;;) {
       draw_group(buf0, g);
@@ -377,12 +383,12 @@ template <typename T, int kSeeding, int kW>
 __global__ void __launch_bounds__(kThreads)
 watermark_elem_kernel(T* __restrict__ logits, int64_t row_stride, uint32_t V, int64_t B,
                       const int32_t* __restrict__ context, int width, uint64_t key, uint32_t tm1,
-                      float delta) {
+                      float delta, uint32_t vbase) {
   const uint32_t v = blockIdx.x * kThreads + threadIdx.x;
   for (int64_t row = blockIdx.y; row < B; row += gridDim.y) {
     if (v >= V) continue;
     const RowSeed<kW> rs = row_seed<kSeeding, kW>(key, context + row * width, width);
-    bias_one<T, kSeeding>(logits + row * row_stride, v, rs, tm1, delta);
+    bias_one<T, kSeeding>(logits + row * row_stride, v, rs, tm1, delta, vbase);
   }
 }
 
@@ -732,9 +738,10 @@ __global__ void __launch_bounds__(kThreads)
 decode_vec_kernel(const T* __restrict__ logits, int64_t row_stride, uint32_t V, int64_t B,
                   const int32_t* __restrict__ context, int width, uint64_t key, uint32_t tm1,
                   int none_green, float delta, const uint64_t* __restrict__ seeds, float inv_t,
-                  uint32_t segments, uint64_t* __restrict__ partials) {
+                  uint32_t segments, uint64_t* __restrict__ partials, uint32_t vbase) {
   using VecT = typename std::conditional<sizeof(T) == 4, f32x4, u32x4>::type;
   constexpr int kE = sizeof(T) == 4 ? 4 : 8;         // tokens per vector
+  const uint32_t jbase = vbase / kE;                 // vector index of the first column
   __shared__ uint64_t lds_key[kThreads / 64], lds_part[kThreads / 64];
   // Per wave: token ids, then raw logits.  The queue is scored whenever it holds more
   // than 64 tokens before a vector is queued, so it never holds more than 64 plus one
@@ -784,6 +791,9 @@ decode_vec_kernel(const T* __restrict__ logits, int64_t row_stride, uint32_t V, 
     auto process_sub = [&](const VecT (&buf)[kN], int sub) {
       uint32_t sub_first = seg_base + static_cast<uint32_t>(sub) * kSubVecs;
       asm volatile("" : "+s"(sub_first));
+      // The same sub-batch counted in token-id vectors (the row's first id is vbase).
+      uint32_t id_first = sub_first + jbase;
+      asm volatile("" : "+s"(id_first));
       const bool whole = sub_first + kSubVecs <= full;
       float m = -INFINITY;
 #pragma unroll
@@ -812,7 +822,7 @@ decode_vec_kernel(const T* __restrict__ logits, int64_t row_stride, uint32_t V, 
         for (int e = 0; e < kE; ++e) hi[n][e] = -INFINITY;
         if (reach) {
           uint32_t nw[kE];
-          noise_words(j, nk, nw);
+          noise_words(id_first + n * kThreads + threadIdx.x, nk, nw);
 #pragma unroll
           for (int e = 0; e < kE; ++e) {
             const float c = noise_ones(nw[e]);
@@ -844,12 +854,13 @@ decode_vec_kernel(const T* __restrict__ logits, int64_t row_stride, uint32_t V, 
           lb = fmaxf(lb, wave_max(best.any ? best.v : -INFINITY));
         }
         const uint32_t j = sub_first + n * kThreads + threadIdx.x;
+        const uint32_t jid = id_first + n * kThreads + threadIdx.x;
         if (whole) {
 #pragma unroll
           for (int e = 0; e < kE; ++e) {
             const bool reaches = !(hi[n][e] < lb);
             const uint64_t mask = __ballot(reaches);
-            if (reaches) enqueue(q_v, q_raw, queued, mask, j * kE + e, raw_elem(buf[n], e));
+            if (reaches) enqueue(q_v, q_raw, queued, mask, jid * kE + e, raw_elem(buf[n], e));
             queued = __builtin_amdgcn_readfirstlane(queued + static_cast<uint32_t>(__popcll(mask)));
           }
         } else {
@@ -859,7 +870,7 @@ decode_vec_kernel(const T* __restrict__ logits, int64_t row_stride, uint32_t V, 
           for (int e = 0; e < kE; ++e) {
             const bool reaches = !(hi[n][e] < lb);
             const uint64_t mask = __ballot(reaches) & valid_mask;
-            if (valid && reaches) enqueue(q_v, q_raw, queued, mask, j * kE + e, raw_elem(buf[n], e));
+            if (valid && reaches) enqueue(q_v, q_raw, queued, mask, jid * kE + e, raw_elem(buf[n], e));
             queued = __builtin_amdgcn_readfirstlane(queued + static_cast<uint32_t>(__popcll(mask)));
           }
         }
@@ -901,9 +912,10 @@ decode_vec_kernel(const T* __restrict__ logits, int64_t row_stride, uint32_t V, 
     // that holds it.
     if (tail != 0u && threadIdx.x == 0 && full >= seg_base && full - seg_base < kSubVecs * kSub) {
       for (uint32_t e = 0; e < tail; ++e) {
-        const uint32_t v = full * kPer + e;
+        const uint32_t c = full * kPer + e;          // column; the token id is vbase + c
+        const uint32_t v = vbase + c;
         const bool g = !none_green && is_green(draw<kSeeding>(rs, v), tm1);
-        consider_any_order(best, sc.of(widen(bias_elem(row_ptr[v], delta, g)), v), v);
+        consider_any_order(best, sc.of(widen(bias_elem(row_ptr[c], delta, g)), v), v);
       }
     }
     block_argmax_store(best, partials + row * segments + blockIdx.x, lds_key, lds_part);
@@ -917,7 +929,7 @@ __global__ void __launch_bounds__(kThreads)
 argmax_elem_kernel(const T* __restrict__ logits, int64_t row_stride, uint32_t V, int64_t B,
                    const int32_t* __restrict__ context, int width, uint64_t key, uint32_t tm1,
                    int none_green, float delta, const uint64_t* __restrict__ seeds, float inv_t,
-                   uint32_t segments, uint64_t* __restrict__ partials) {
+                   uint32_t segments, uint64_t* __restrict__ partials, uint32_t vbase) {
   __shared__ uint64_t lds_key[kThreads / 64], lds_part[kThreads / 64];
   const uint64_t seg_first = static_cast<uint64_t>(blockIdx.x) * kArgmaxSegElems;
   for (int64_t row = blockIdx.y; row < B; row += gridDim.y) {
@@ -927,9 +939,10 @@ argmax_elem_kernel(const T* __restrict__ logits, int64_t row_stride, uint32_t V,
     for (int s = 0; s < kElemSegSteps; ++s) {
       const uint64_t v64 = seg_first + static_cast<uint64_t>(s) * kThreads + threadIdx.x;
       if (v64 < V) {
-        const uint32_t v = static_cast<uint32_t>(v64);
+        const uint32_t c = static_cast<uint32_t>(v64);   // column; the token id is vbase + c
+        const uint32_t v = vbase + c;
         const bool g = !none_green && is_green(draw<kSeeding>(rs, v), tm1);
-        consider(lb, sc.of(widen(bias_elem(logits[row * row_stride + v], delta, g)), v), v);
+        consider(lb, sc.of(widen(bias_elem(logits[row * row_stride + c], delta, g)), v), v);
       }
     }
     block_argmax_store(lb, partials + row * segments + blockIdx.x, lds_key, lds_part);
@@ -1285,7 +1298,7 @@ constexpr int unroll_for() {
 template <typename T, int kSeeding, int kW>
 void launch_watermark(void* logits, int64_t B, uint32_t V, int64_t row_stride,
                       const int32_t* context, int width, uint64_t key, uint32_t tm1, float delta,
-                      bool aligned, hipStream_t stream) {
+                      uint32_t vbase, bool aligned, hipStream_t stream) {
   T* p = static_cast<T*>(logits);
   const uint32_t rows = static_cast<uint32_t>(B < kMaxGridY ? B : kMaxGridY);
   if (aligned) {
@@ -1314,41 +1327,41 @@ void launch_watermark(void* logits, int64_t B, uint32_t V, int64_t row_stride,
       if (kMaxRows == 4 && rows_per_group == 4)
         hipLaunchKernelGGL((watermark_ss_rows_kernel<T, kU, kW, (kMaxRows > 2 ? kMaxRows : 1), kPf>),
                            grid, dim3(kThreads), 0, stream, p, row_stride, V, B, context, width,
-                           key, tm1, delta);
+                           key, tm1, delta, vbase);
       else if (kMaxRows >= 2 && rows_per_group == 2)
         hipLaunchKernelGGL((watermark_ss_rows_kernel<T, kU, kW, (kMaxRows >= 2 ? 2 : 1), kPf>), grid,
                            dim3(kThreads), 0, stream, p, row_stride, V, B, context, width, key, tm1,
-                           delta);
+                           delta, vbase);
       else
         hipLaunchKernelGGL((watermark_ss_rows_kernel<T, kU, kW, 1, kPf>), grid, dim3(kThreads), 0,
-                           stream, p, row_stride, V, B, context, width, key, tm1, delta);
+                           stream, p, row_stride, V, B, context, width, key, tm1, delta, vbase);
     } else {
       hipLaunchKernelGGL((watermark_vec_kernel<T, kU, kW>), dim3(tiles, rows),
                          dim3(kThreads), 0, stream, p, row_stride, V, B, context, width, key, tm1,
-                         delta);
+                         delta, vbase);
     }
   } else {
     const uint32_t tiles = static_cast<uint32_t>((static_cast<uint64_t>(V) + kThreads - 1) / kThreads);
     hipLaunchKernelGGL((watermark_elem_kernel<T, kSeeding, kW>), dim3(tiles, rows), dim3(kThreads),
-                       0, stream, p, row_stride, V, B, context, width, key, tm1, delta);
+                       0, stream, p, row_stride, V, B, context, width, key, tm1, delta, vbase);
   }
 }
 
 template <typename T>
 void dispatch_watermark(void* logits, int64_t B, uint32_t V, int64_t row_stride,
                         const int32_t* context, int width, uint64_t key, uint32_t tm1, float delta,
-                        sbw_seeding_t seeding, bool aligned, hipStream_t st) {
+                        sbw_seeding_t seeding, uint32_t vbase, bool aligned, hipStream_t st) {
   // Context seeding folds any window into one row seed; self-salt needs the window
   // per candidate, so wider windows take the kMaxWidth instantiation.
   if (seeding == SBW_SEED_CONTEXT)
     launch_watermark<T, kContext, kMaxWidth>(logits, B, V, row_stride, context, width, key, tm1,
-                                             delta, aligned, st);
+                                             delta, vbase, aligned, st);
   else if (width == 1)
     launch_watermark<T, kSelfSalt, 1>(logits, B, V, row_stride, context, width, key, tm1, delta,
-                                      aligned, st);
+                                      vbase, aligned, st);
   else
     launch_watermark<T, kSelfSalt, kMaxWidth>(logits, B, V, row_stride, context, width, key, tm1,
-                                              delta, aligned, st);
+                                              delta, vbase, aligned, st);
 }
 
 template <typename T>
@@ -1390,8 +1403,8 @@ struct SampleArgs {
 template <typename T, int kSeeding, int kW, bool kSample>
 void launch_argmax(const void* logits, int64_t B, uint32_t V, int64_t row_stride,
                    const int32_t* context, int width, uint64_t key, uint32_t tm1, int none,
-                   float delta, const SampleArgs& sa, bool aligned, int32_t* tokens, float* values,
-                   uint64_t* partials, hipStream_t stream) {
+                   float delta, const SampleArgs& sa, uint32_t vbase, bool aligned, int32_t* tokens,
+                   float* values, uint64_t* partials, hipStream_t stream) {
   const T* p = static_cast<const T*>(logits);
   const uint32_t rows = static_cast<uint32_t>(B < kMaxGridY ? B : kMaxGridY);
   uint32_t segments;
@@ -1401,13 +1414,13 @@ void launch_argmax(const void* logits, int64_t B, uint32_t V, int64_t row_stride
     segments = static_cast<uint32_t>((static_cast<uint64_t>(V) + seg - 1) / seg);
     hipLaunchKernelGGL((decode_vec_kernel<T, kSeeding, kN, SBW_DECODE_SUBS, kW, kSample>),
                        dim3(segments, rows), dim3(kThreads), 0, stream, p, row_stride, V, B, context,
-                       width, key, tm1, none, delta, sa.seeds, sa.inv_t, segments, partials);
+                       width, key, tm1, none, delta, sa.seeds, sa.inv_t, segments, partials, vbase);
   } else {
     segments = static_cast<uint32_t>((static_cast<uint64_t>(V) + kArgmaxSegElems - 1) /
                                      kArgmaxSegElems);
     hipLaunchKernelGGL((argmax_elem_kernel<T, kSeeding, kW, kSample>), dim3(segments, rows),
                        dim3(kThreads), 0, stream, p, row_stride, V, B, context, width, key, tm1,
-                       none, delta, sa.seeds, sa.inv_t, segments, partials);
+                       none, delta, sa.seeds, sa.inv_t, segments, partials, vbase);
   }
   const int64_t row_blocks = grid_for((B + kThreads / 64 - 1) / (kThreads / 64));
   hipLaunchKernelGGL(argmax_finish_kernel, dim3(row_blocks), dim3(kThreads), 0, stream, partials,
@@ -1417,19 +1430,21 @@ void launch_argmax(const void* logits, int64_t B, uint32_t V, int64_t row_stride
 template <typename T, bool kSample>
 void dispatch_argmax(const void* logits, int64_t B, uint32_t V, int64_t row_stride,
                      const int32_t* context, int width, uint64_t key, uint32_t tm1, int none,
-                     float delta, const SampleArgs& sa, sbw_seeding_t seeding, bool aligned,
-                     int32_t* tokens, float* values, uint64_t* partials, hipStream_t st) {
+                     float delta, const SampleArgs& sa, sbw_seeding_t seeding, uint32_t vbase,
+                     bool aligned, int32_t* tokens, float* values, uint64_t* partials,
+                     hipStream_t st) {
   if (seeding == SBW_SEED_CONTEXT)
     launch_argmax<T, kContext, kMaxWidth, kSample>(logits, B, V, row_stride, context, width, key,
-                                                   tm1, none, delta, sa, aligned, tokens, values,
-                                                   partials, st);
+                                                   tm1, none, delta, sa, vbase, aligned, tokens,
+                                                   values, partials, st);
   else if (width == 1)
     launch_argmax<T, kSelfSalt, 1, kSample>(logits, B, V, row_stride, context, width, key, tm1,
-                                            none, delta, sa, aligned, tokens, values, partials, st);
+                                            none, delta, sa, vbase, aligned, tokens, values,
+                                            partials, st);
   else
     launch_argmax<T, kSelfSalt, kMaxWidth, kSample>(logits, B, V, row_stride, context, width, key,
-                                                    tm1, none, delta, sa, aligned, tokens, values,
-                                                    partials, st);
+                                                    tm1, none, delta, sa, vbase, aligned, tokens,
+                                                    values, partials, st);
 }
 
 template <int kSeeding, int kW>
@@ -1511,20 +1526,37 @@ sbw_status_t detect_impl(const int32_t* tokens, int64_t N, int64_t L, int64_t ro
   return after_launch();
 }
 
+// Token ids are 32-bit: a row holds fewer than 2^32 columns (its length is a 32-bit
+// count), and a shard's last id, v_offset + V - 1, must fit.  v_offset >= 0.
+constexpr int64_t kMaxTokenIds = int64_t{1} << 32;
+bool ids_fit(int64_t V, int64_t v_offset) {
+  return V < kMaxTokenIds && v_offset <= kMaxTokenIds - V;
+}
+
+// The vector kernels load 16 bytes per lane and draw whole Philox blocks: rows must
+// start on 16 bytes, and the shard's first token id must sit at the start of a vector
+// (a multiple of 4 for fp32, of 8 for bf16).  Anything else takes the element path.
+bool vector_path_ok(const void* logits, int64_t row_stride, sbw_dtype_t dtype, uint32_t vbase) {
+  const uint32_t esize = dtype == SBW_F32 ? 4u : 2u;
+  return reinterpret_cast<uintptr_t>(logits) % 16 == 0 &&
+         (static_cast<uint64_t>(row_stride) * esize) % 16 == 0 && vbase % (16u / esize) == 0;
+}
+
 // Greedy decoding and sampling: validation, then the segment pass and the read-out.
 template <bool kSample>
 sbw_status_t decode_impl(const void* logits, sbw_dtype_t dtype, int64_t B, int64_t V,
-                         int64_t row_stride, const int32_t* context, int64_t width, uint64_t key,
-                         double gamma, float delta, sbw_seeding_t seeding, const SampleArgs& sa,
-                         int32_t* tokens, float* values, uint64_t* workspace, void* stream) {
-  if (B < 0 || V < 0 || row_stride < V) return SBW_ERR_INVALID_ARG;
+                         int64_t row_stride, const int32_t* context, int64_t width,
+                         int64_t v_offset, uint64_t key, double gamma, float delta,
+                         sbw_seeding_t seeding, const SampleArgs& sa, int32_t* tokens,
+                         float* values, uint64_t* workspace, void* stream) {
+  if (B < 0 || V < 0 || row_stride < V || v_offset < 0) return SBW_ERR_INVALID_ARG;
   sbw_status_t s = check_width(width);
   if (s != SBW_OK) return s;
   if (dtype != SBW_F32 && dtype != SBW_BF16) return SBW_ERR_UNSUPPORTED;
   if (!valid_seeding(seeding)) return SBW_ERR_UNSUPPORTED;
   if (!(gamma >= 0.0 && gamma <= 1.0)) return SBW_ERR_GAMMA;
   if (!isfinite(delta)) return SBW_ERR_DELTA;
-  if (V >= (int64_t{1} << 32)) return SBW_ERR_UNSUPPORTED;
+  if (!ids_fit(V, v_offset)) return SBW_ERR_UNSUPPORTED;
   if (B == 0) return SBW_OK;
   if (V == 0) return SBW_ERR_INVALID_ARG;  // no token to choose
   if (logits == nullptr || context == nullptr || tokens == nullptr || workspace == nullptr)
@@ -1538,18 +1570,17 @@ sbw_status_t decode_impl(const void* logits, sbw_dtype_t dtype, int64_t B, int64
   const int none = T == 0 ? 1 : 0;
   const uint32_t tm1 = none ? 0u : static_cast<uint32_t>(T - 1);
   const float d = delta;
-  const size_t esize = dtype == SBW_F32 ? 4 : 2;
-  const bool aligned = (reinterpret_cast<uintptr_t>(logits) % 16 == 0) &&
-                       ((static_cast<uint64_t>(row_stride) * esize) % 16 == 0);
+  const uint32_t vbase = static_cast<uint32_t>(v_offset);
+  const bool aligned = vector_path_ok(logits, row_stride, dtype, vbase);
   const uint32_t v32 = static_cast<uint32_t>(V);
   const int w = static_cast<int>(width);
   hipStream_t st = static_cast<hipStream_t>(stream);
   if (dtype == SBW_F32)
     dispatch_argmax<float, kSample>(logits, B, v32, row_stride, context, w, key, tm1, none, d, sa,
-                                    seeding, aligned, tokens, values, workspace, st);
+                                    seeding, vbase, aligned, tokens, values, workspace, st);
   else
     dispatch_argmax<uint16_t, kSample>(logits, B, v32, row_stride, context, w, key, tm1, none, d,
-                                       sa, seeding, aligned, tokens, values, workspace, st);
+                                       sa, seeding, vbase, aligned, tokens, values, workspace, st);
   return after_launch();
 }
 
@@ -1560,18 +1591,18 @@ using namespace sbw;
 
 extern "C" {
 
-sbw_status_t sbw_watermark_window(void* logits, sbw_dtype_t dtype, int64_t B, int64_t V,
-                                  int64_t row_stride, const int32_t* context, int64_t width,
-                                  uint64_t key, double gamma, float delta, sbw_seeding_t seeding,
-                                  void* stream) {
-  if (B < 0 || V < 0 || row_stride < V) return SBW_ERR_INVALID_ARG;
+sbw_status_t sbw_watermark_shard(void* logits, sbw_dtype_t dtype, int64_t B, int64_t V,
+                                 int64_t row_stride, const int32_t* context, int64_t width,
+                                 int64_t v_offset, uint64_t key, double gamma, float delta,
+                                 sbw_seeding_t seeding, void* stream) {
+  if (B < 0 || V < 0 || row_stride < V || v_offset < 0) return SBW_ERR_INVALID_ARG;
   sbw_status_t s = check_width(width);
   if (s != SBW_OK) return s;
   if (dtype != SBW_F32 && dtype != SBW_BF16) return SBW_ERR_UNSUPPORTED;
   if (!valid_seeding(seeding)) return SBW_ERR_UNSUPPORTED;
   if (!(gamma >= 0.0 && gamma <= 1.0)) return SBW_ERR_GAMMA;
   if (!isfinite(delta)) return SBW_ERR_DELTA;
-  if (V >= (int64_t{1} << 32)) return SBW_ERR_UNSUPPORTED;  // token ids are 32-bit
+  if (!ids_fit(V, v_offset)) return SBW_ERR_UNSUPPORTED;  // token ids are 32-bit
   if (B == 0 || V == 0) return SBW_OK;
   if (logits == nullptr || context == nullptr) return SBW_ERR_INVALID_ARG;
   if (B > INT64_MAX / 4 / row_stride) return SBW_ERR_UNSUPPORTED;
@@ -1580,20 +1611,27 @@ sbw_status_t sbw_watermark_window(void* logits, sbw_dtype_t dtype, int64_t B, in
   s = check_device();
   if (s != SBW_OK) return s;
 
-  const size_t esize = dtype == SBW_F32 ? 4 : 2;
-  const bool aligned = (reinterpret_cast<uintptr_t>(logits) % 16 == 0) &&
-                       ((static_cast<uint64_t>(row_stride) * esize) % 16 == 0);
+  const uint32_t vbase = static_cast<uint32_t>(v_offset);
+  const bool aligned = vector_path_ok(logits, row_stride, dtype, vbase);
   const uint32_t tm1 = static_cast<uint32_t>(T - 1);
   const uint32_t v32 = static_cast<uint32_t>(V);
   const int w = static_cast<int>(width);
   hipStream_t st = static_cast<hipStream_t>(stream);
   if (dtype == SBW_F32)
     dispatch_watermark<float>(logits, B, v32, row_stride, context, w, key, tm1, delta, seeding,
-                              aligned, st);
+                              vbase, aligned, st);
   else
     dispatch_watermark<uint16_t>(logits, B, v32, row_stride, context, w, key, tm1, delta, seeding,
-                                 aligned, st);
+                                 vbase, aligned, st);
   return after_launch();
+}
+
+sbw_status_t sbw_watermark_window(void* logits, sbw_dtype_t dtype, int64_t B, int64_t V,
+                                  int64_t row_stride, const int32_t* context, int64_t width,
+                                  uint64_t key, double gamma, float delta, sbw_seeding_t seeding,
+                                  void* stream) {
+  return sbw_watermark_shard(logits, dtype, B, V, row_stride, context, width, 0, key, gamma, delta,
+                             seeding, stream);
 }
 
 sbw_status_t sbw_watermark(void* logits, sbw_dtype_t dtype, int64_t B, int64_t V,
@@ -1643,8 +1681,18 @@ sbw_status_t sbw_watermark_argmax(const void* logits, sbw_dtype_t dtype, int64_t
                                   uint64_t key, double gamma, float delta, sbw_seeding_t seeding,
                                   int32_t* tokens, float* values, uint64_t* workspace,
                                   void* stream) {
-  return decode_impl<false>(logits, dtype, B, V, row_stride, context, width, key, gamma, delta,
+  return decode_impl<false>(logits, dtype, B, V, row_stride, context, width, 0, key, gamma, delta,
                             seeding, SampleArgs{nullptr, 1.0f}, tokens, values, workspace, stream);
+}
+
+sbw_status_t sbw_watermark_argmax_shard(const void* logits, sbw_dtype_t dtype, int64_t B, int64_t V,
+                                        int64_t row_stride, const int32_t* context, int64_t width,
+                                        int64_t v_offset, uint64_t key, double gamma, float delta,
+                                        sbw_seeding_t seeding, int32_t* tokens, float* values,
+                                        uint64_t* workspace, void* stream) {
+  return decode_impl<false>(logits, dtype, B, V, row_stride, context, width, v_offset, key, gamma,
+                            delta, seeding, SampleArgs{nullptr, 1.0f}, tokens, values, workspace,
+                            stream);
 }
 
 sbw_status_t sbw_watermark_sample(const void* logits, sbw_dtype_t dtype, int64_t B, int64_t V,
@@ -1652,11 +1700,22 @@ sbw_status_t sbw_watermark_sample(const void* logits, sbw_dtype_t dtype, int64_t
                                   uint64_t key, double gamma, float delta, sbw_seeding_t seeding,
                                   const uint64_t* seeds, float inv_temperature, int32_t* tokens,
                                   float* scores, uint64_t* workspace, void* stream) {
+  return sbw_watermark_sample_shard(logits, dtype, B, V, row_stride, context, width, 0, key, gamma,
+                                    delta, seeding, seeds, inv_temperature, tokens, scores,
+                                    workspace, stream);
+}
+
+sbw_status_t sbw_watermark_sample_shard(const void* logits, sbw_dtype_t dtype, int64_t B, int64_t V,
+                                        int64_t row_stride, const int32_t* context, int64_t width,
+                                        int64_t v_offset, uint64_t key, double gamma, float delta,
+                                        sbw_seeding_t seeding, const uint64_t* seeds,
+                                        float inv_temperature, int32_t* tokens, float* scores,
+                                        uint64_t* workspace, void* stream) {
   if (!(isfinite(inv_temperature) && inv_temperature > 0.0f)) return SBW_ERR_INVALID_ARG;
   if (B > 0 && V > 0 && seeds == nullptr) return SBW_ERR_INVALID_ARG;
-  return decode_impl<true>(logits, dtype, B, V, row_stride, context, width, key, gamma, delta,
-                           seeding, SampleArgs{seeds, inv_temperature}, tokens, scores, workspace,
-                           stream);
+  return decode_impl<true>(logits, dtype, B, V, row_stride, context, width, v_offset, key, gamma,
+                           delta, seeding, SampleArgs{seeds, inv_temperature}, tokens, scores,
+                           workspace, stream);
 }
 
 int64_t sbw_watermark_argmax_workspace(int64_t B, int64_t V) {
@@ -1743,6 +1802,6 @@ const char* sbw_strerror(sbw_status_t status) {
 
 const char* sbw_last_hip_error(void) { return hipGetErrorName(g_last_hip_error); }
 
-const char* sbw_version(void) { return "0.4.0"; }
+const char* sbw_version(void) { return "0.5.0"; }
 
 }  // extern "C"

@@ -39,8 +39,10 @@ def test_header_declares_the_boundary():
     assert _declared() == ["sbw_detect", "sbw_detect_ex", "sbw_detect_window", "sbw_green_mask",
                            "sbw_green_mask_window", "sbw_last_hip_error", "sbw_strerror",
                            "sbw_version", "sbw_watermark", "sbw_watermark_argmax",
-                           "sbw_watermark_argmax_workspace", "sbw_watermark_candidates",
-                           "sbw_watermark_sample", "sbw_watermark_window"]
+                           "sbw_watermark_argmax_shard", "sbw_watermark_argmax_workspace",
+                           "sbw_watermark_candidates", "sbw_watermark_sample",
+                           "sbw_watermark_sample_shard", "sbw_watermark_shard",
+                           "sbw_watermark_window"]
 
 
 def test_library_exports_every_declared_symbol(sbw, lib):
@@ -361,3 +363,49 @@ def test_sample_rejects_bad_arguments(lib):
     assert ws_(lib, B=0, seeds=NULL) == OK
     if not _gpu_visible():
         assert ws_(lib, scores=NULL) == NO_DEVICE
+
+
+def test_shard_entry_points_reject_bad_offsets(lib):
+    """v_offset >= 0 and v_offset + V <= 2^32 (token ids are 32-bit); every other check
+    is the unsharded call's."""
+    def wsh(v_offset, V=8, **kw):
+        a = dict(logits=DUMMY, B=2, stride=max(V, 8))
+        a.update(kw)
+        return lib.sbw_watermark_shard(a["logits"], 0, a["B"], V, a["stride"], DUMMY, 1, v_offset,
+                                       KEY, 0.25, 2.0, 0, None)
+
+    def ash(v_offset, V=8, **kw):
+        return lib.sbw_watermark_argmax_shard(DUMMY, 1, 2, V, max(V, 8), DUMMY, 1, v_offset, KEY,
+                                              0.25, 2.0, 1, DUMMY, DUMMY, DUMMY, None)
+
+    def ssh(v_offset, V=8, inv_t=1.0):
+        return lib.sbw_watermark_sample_shard(DUMMY, 0, 2, V, max(V, 8), DUMMY, 1, v_offset, KEY,
+                                              0.25, 2.0, 0, DUMMY, inv_t, DUMMY, DUMMY, DUMMY,
+                                              None)
+
+    for fn in (wsh, ash, ssh):
+        assert fn(-1) == INVALID
+        assert fn(-(1 << 40)) == INVALID
+        assert fn((1 << 32) - 7) == UNSUPPORTED          # last id would be 2^32
+        assert fn((1 << 32) + 1, V=0) == UNSUPPORTED
+    assert ssh(0, inv_t=0.0) == INVALID
+    assert wsh(5, B=0) == OK
+    assert wsh(1 << 32, V=0) == OK                         # an empty shard: nothing to do
+    assert ash(0, V=0) == INVALID                          # no token to choose
+    assert ssh(1 << 32, V=0) == INVALID
+    if not _gpu_visible():
+        for fn in (wsh, ash, ssh):
+            assert fn((1 << 32) - 8) == NO_DEVICE          # last id 2^32 - 1 is allowed
+            assert fn(12345) == NO_DEVICE
+
+
+def test_binding_shard_calls_validate_before_the_c_abi(sbw):
+    import torch
+    x = torch.zeros(2, 8)
+    prev = torch.zeros(2, dtype=torch.int32)
+    with pytest.raises(ValueError, match="current HIP device"):
+        sbw.watermark_shard(x, prev, 16, KEY, 0.25, 2.0)
+    with pytest.raises(ValueError, match="current HIP device"):
+        sbw.watermark_argmax_shard(x, prev, 16, KEY, 0.25, 2.0,
+                                   tokens=torch.zeros(2, dtype=torch.int32), values=torch.zeros(2),
+                                   workspace=torch.zeros(4, dtype=torch.int64))
