@@ -176,3 +176,28 @@ def test_argmax_skip_bound_edges(env, dtype, seeding):
         assert_argmax_equal(run_argmax(env, x, ctx, WIDE, gamma, delta, seeding),
                             oracle.watermark_argmax(x, ctx, WIDE, gamma, delta, seeding),
                             f"{dtype}/{seeding}/{gamma}/{delta}")
+
+
+# Launches whose grid would hold fewer than this many workgroups take the decode kernel
+# with half the vectors per lane; the bound-edge rows are run on both sides of it.
+SMALL_DECODE_GRID = 1024
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("seeding", ["context", "self_salt"])
+def test_argmax_both_launch_shapes(env, dtype, seeding):
+    """The bound-edge rows tiled to 256 rows (5 segments each: 1280 workgroups, the
+    full-width kernel) and to 8 rows (40: the half-width kernel)."""
+    rng = np.random.default_rng(93)
+    V = 40001
+    edge = bound_rows(rng, V, dtype)
+    seg = 8192
+    for B in (8, 256):
+        x = np.concatenate([edge] * (-(-B // edge.shape[0])))[:B].copy()
+        ctx = workloads.context_tokens(B, 1, V, rng)[:, 0].copy()
+        big = B * (-(-V // seg)) >= SMALL_DECODE_GRID
+        for gamma, delta in [(0.25, 2.0), (0.5, -1.0)]:
+            say(f"argmax launch shapes {dtype} {seeding} B={B} big={big} gamma={gamma}")
+            assert_argmax_equal(run_argmax(env, x, ctx, WIDE, gamma, delta, seeding),
+                                oracle.watermark_argmax(x, ctx, WIDE, gamma, delta, seeding),
+                                f"{dtype}/{seeding}/B={B}/{gamma}")

@@ -198,3 +198,23 @@ def test_sample_windows(env, dtype, seeding, width):
     assert_argmax_equal(run_sample(env, x, ctx, seeds, WIDE, 0.25, 2.0, seeding, 1.0),
                         oracle.watermark_sample(x, ctx, WIDE, 0.25, 2.0, seeding, seeds, 1.0),
                         f"{dtype}/{seeding}/h={width}")
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("seeding", ["context", "self_salt"])
+def test_sample_both_launch_shapes(env, dtype, seeding):
+    """The queue-round rows tiled to 256 rows (the full-width decode kernel: 5 segments
+    per row, 1280 workgroups) and to 8 rows (the half-width kernel for small grids)."""
+    rng = np.random.default_rng(470)
+    V = 40001
+    edge = queue_rows(rng, V, dtype)
+    for B in (8, 256):
+        x = np.concatenate([edge] * (-(-B // edge.shape[0])))[:B].copy()
+        ctx = workloads.context_tokens(B, 1, V, rng)[:, 0].copy()
+        seeds = seeds_for(rng, B)
+        for gamma, delta, inv_t in [(0.25, 2.0, 1.0), (0.5, -1.0, 0.37)]:
+            say(f"sample launch shapes {dtype} {seeding} B={B} gamma={gamma}")
+            assert_argmax_equal(run_sample(env, x, ctx, seeds, WIDE, gamma, delta, seeding, inv_t),
+                                oracle.watermark_sample(x, ctx, WIDE, gamma, delta, seeding, seeds,
+                                                        inv_t),
+                                f"{dtype}/{seeding}/B={B}/{gamma}")
