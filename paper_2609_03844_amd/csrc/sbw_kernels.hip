@@ -65,7 +65,7 @@ namespace {
 #define SBW_SELF_SALT_PREFETCH_BF16 1
 #endif
 #ifndef SBW_SELF_SALT_MIN_GROUPS
-#define SBW_SELF_SALT_MIN_GROUPS 2048
+#define SBW_SELF_SALT_MIN_GROUPS 1024  // 2048 measured 5 % slower for B * V of 5-10 M logits
 #endif
 
 constexpr int kThreads = 256;            // 4 wavefronts of 64
