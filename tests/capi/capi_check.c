@@ -74,6 +74,8 @@ static int cpu_checks(void)
     CHECK(sbw_watermark(&dummy, SBW_F32, 1, 1, 1, &prev, 1, 0.25, INFINITY, SBW_SEED_CONTEXT, NULL) == SBW_ERR_DELTA, "delta inf");
     CHECK(sbw_watermark(&dummy, (sbw_dtype_t)7, 1, 1, 1, &prev, 1, 0.25, 2.0f, SBW_SEED_CONTEXT, NULL) == SBW_ERR_UNSUPPORTED, "dtype");
     CHECK(sbw_watermark(&dummy, SBW_F32, 0, 1, 1, &prev, 1, 0.25, 2.0f, SBW_SEED_CONTEXT, NULL) == SBW_OK, "B = 0 is a no-op");
+    CHECK(sbw_watermark_shard(&dummy, SBW_F32, 1, 1, 1, &prev, 1, -1, 1, 0.25, 2.0f, SBW_SEED_CONTEXT, NULL) == SBW_ERR_INVALID_ARG, "negative v_offset");
+    CHECK(sbw_watermark_shard(&dummy, SBW_F32, 1, 2, 2, &prev, 1, (int64_t)1 << 32, 1, 0.25, 2.0f, SBW_SEED_CONTEXT, NULL) == SBW_ERR_UNSUPPORTED, "ids past 2^32");
     CHECK(sbw_watermark_argmax_workspace(256, 152064) == 256 * 75, "workspace size");
     CHECK(sbw_watermark_argmax_workspace(0, 5) == 0, "workspace of nothing");
     printf("capi cpu ok: libsbw %s\n", v);
@@ -139,6 +141,28 @@ static int gpu_checks(void)
         CHECK(memcmp(gtok, etok, sizeof etok) == 0 && memcmp(gvals, evals, sizeof evals) == 0,
               "sample, seeding %d", seeding);
         CHECK(gtok[3] == 777, "the NaN logit wins the sample");
+        /* the same draw from two vocabulary shards, [0, S) and [S, V), reduced here:
+           the larger score, the smaller id among equal ones, a NaN above all */
+        {
+            const int64_t S = 20003;
+            int32_t t0[8], t1[8];
+            float s0[8], s1[8];
+            SBW(sbw_watermark_sample_shard(d_x, SBW_F32, B, S, V, d_ctx, W, 0, key, gamma, delta, sd,
+                                           d_seeds, inv_t, d_tokens, d_vals, d_ws, NULL));
+            HIP(hipMemcpy(t0, d_tokens, sizeof t0, hipMemcpyDeviceToHost));
+            HIP(hipMemcpy(s0, d_vals, sizeof s0, hipMemcpyDeviceToHost));
+            SBW(sbw_watermark_sample_shard(d_x + S, SBW_F32, B, V - S, V, d_ctx, W, S, key, gamma,
+                                           delta, sd, d_seeds, inv_t, d_tokens, d_vals, d_ws, NULL));
+            HIP(hipMemcpy(t1, d_tokens, sizeof t1, hipMemcpyDeviceToHost));
+            HIP(hipMemcpy(s1, d_vals, sizeof s1, hipMemcpyDeviceToHost));
+            for (int b = 0; b < B; ++b) {
+                const int second = !isnan(s0[b]) && (isnan(s1[b]) || s1[b] > s0[b]);
+                const int32_t t = second ? t1[b] : t0[b];
+                const float sc = second ? s1[b] : s0[b];
+                CHECK(t == etok[b] && memcmp(&sc, &evals[b], sizeof sc) == 0,
+                      "sample from shards, row %d, seeding %d", b, seeding);
+            }
+        }
         /* then the watermark in place */
         SBW(sbw_watermark_window(d_x, SBW_F32, B, V, V, d_ctx, W, key, gamma, delta, sd, NULL));
         HIP(hipMemcpy(got, d_x, nl * sizeof(float), hipMemcpyDeviceToHost));
