@@ -9,7 +9,8 @@ A shard holds columns [a, b) of the vocabulary; column c is token a + c.  Checke
     smallest id among equal ones, NaN above all), equal the oracle's full-row decode;
   * shards whose first id is or is not a multiple of 4 (fp32) / 8 (bf16), so both the
     vector and the element kernels run, and ids up to 2^31 - 1;
-  * the 8-way split of the 152064-token vocabulary at B = 256, as views of one tensor.
+  * the 8-way split of the 152064-token vocabulary at B = 256, as views of one tensor;
+  * detection split along the text, each shard reading a halo of width tokens.
 """
 import numpy as np
 import pytest
@@ -196,3 +197,29 @@ def test_tensor_parallel_split_of_the_c4_vocabulary(env, seeding):
     torch.cuda.synchronize()
     assert_logits_equal(full.cpu().numpy(), oracle.watermark(x, prev, WIDE, gamma, delta, seeding),
                         f"tp8 {seeding}")
+
+
+@pytest.mark.parametrize("seeding", ["context", "self_salt"])
+@pytest.mark.parametrize("width", [1, 4])
+def test_detection_sharded_along_the_text(env, seeding, width):
+    """Positions [a, b) of every text scored on their own, each shard reading the width
+    tokens before a as its halo: the shards' green counts and scored positions add up
+    to the whole texts' (the oracle's), and z from the sums equals the oracle's z."""
+    torch, sbw, dev = env
+    rng = np.random.default_rng(940 + width)
+    N, L, V, gamma = 64, 1000, 128256, 0.25
+    tok = workloads.uniform_tokens(N, L, V, rng)
+    td = torch.from_numpy(tok).to(dev)
+    cuts = [width, 250, 503, 777, L]
+    counts = np.zeros(N, dtype=np.int64)
+    scored = np.zeros(N, dtype=np.int64)
+    for a, b in zip(cuts[:-1], cuts[1:]):
+        say(f"detect shard {seeding} h={width} positions [{a},{b})")
+        c, t, _ = sbw.detect_ex(td[:, a - width:b], WIDE, gamma, seeding, width=width)
+        counts += c.cpu().numpy()
+        scored += t.cpu().numpy()
+    ec, ez = oracle.detect_w(tok, width, WIDE, gamma, seeding)
+    assert np.array_equal(counts, ec)
+    assert np.all(scored == L - width)
+    z = (counts - scored * gamma) / np.sqrt(scored * gamma * (1 - gamma))
+    np.testing.assert_allclose(z, ez, rtol=1e-6, atol=1e-9)
