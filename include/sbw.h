@@ -303,7 +303,8 @@ int64_t sbw_watermark_argmax_workspace(int64_t B, int64_t V);
  *   logits       device, [B, row_stride]: the shard's columns, V of them per row.
  *   v_offset     global id of column 0, >= 0 (else SBW_ERR_INVALID_ARG), with
  *                v_offset + V <= 2^32 (else SBW_ERR_UNSUPPORTED).
- *   tokens       (argmax, sample) written as global ids, v_offset + c.
+ *   tokens       (argmax, sample) written as global ids, v_offset + c (an id of 2^31
+ *                or more comes back as its 32-bit pattern, as a negative int32).
  * Every other argument, layout and error as for the unsharded call, which is the
  * same call with v_offset = 0.  The rows of all shards of a vocabulary, put side by
  * side, are biased exactly as the full rows are.  For decoding, the full row's token
