@@ -15,6 +15,9 @@
  *   watermark_sample     sampling fused with the watermark (Gumbel-max).
  *   watermark_candidates the watermark on caller-given candidate ids only (the
  *              top-k self-salt scheme of Sec. 4).
+ *   watermark_shard, watermark_argmax_shard, watermark_sample_shard
+ *              the three logits calls on one slice of the vocabulary (a tensor-
+ *              parallel LM head), column c being token v_offset + c.
  *   green_mask the green lists as bit sets (a parity and debugging aid).
  *   detect     For every sequence: count the positions whose token is green
  *              under the seed of the token(s) before it (O(1) per token, Sec. 2.2)
