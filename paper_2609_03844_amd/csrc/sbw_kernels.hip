@@ -70,6 +70,7 @@ namespace {
 
 constexpr int kThreads = 256;            // 4 wavefronts of 64
 constexpr int kMaxWidth = 8;             // longest context window
+constexpr int kMidWidth = 4;             // self-salt watermark: windows of 2-4 (the paper's 4)
 constexpr int64_t kMaxGrid = 1ll << 20;  // blocks; grid-stride loops cover the rest
 constexpr int64_t kMaxGridY = 65535;
 
@@ -1359,6 +1360,9 @@ void dispatch_watermark(void* logits, int64_t B, uint32_t V, int64_t row_stride,
   else if (width == 1)
     launch_watermark<T, kSelfSalt, 1>(logits, B, V, row_stride, context, width, key, tm1, delta,
                                       vbase, aligned, st);
+  else if (width <= kMidWidth)
+    launch_watermark<T, kSelfSalt, kMidWidth>(logits, B, V, row_stride, context, width, key, tm1,
+                                              delta, vbase, aligned, st);
   else
     launch_watermark<T, kSelfSalt, kMaxWidth>(logits, B, V, row_stride, context, width, key, tm1,
                                               delta, vbase, aligned, st);
