@@ -70,7 +70,7 @@ namespace {
 
 constexpr int kThreads = 256;            // 4 wavefronts of 64
 constexpr int kMaxWidth = 8;             // longest context window
-constexpr int kMidWidth = 4;             // self-salt watermark: windows of 2-4 (the paper's 4)
+constexpr int kMidWidth = 4;             // windows of 2-4 (the paper's 4): own instantiations
 constexpr int64_t kMaxGrid = 1ll << 20;  // blocks; grid-stride loops cover the rest
 constexpr int64_t kMaxGridY = 65535;
 
@@ -1477,7 +1477,7 @@ void launch_detect(int64_t positions, int64_t blocks, hipStream_t st, const int3
   else if (positions <= 2 * kWave)
     hipLaunchKernelGGL((detect_kernel<kSeeding, 2, kW>), dim3(blocks), dim3(kThreads), 0, st,
                        tokens, N, L, row_stride, width, key, tm1, gamma, io);
-  else if (positions <= 4 * kWave || kW > 1)
+  else if (positions <= 4 * kWave || kW > kMidWidth)   // windows of 5-8: 4 chunks (registers)
     hipLaunchKernelGGL((detect_kernel<kSeeding, 4, kW>), dim3(blocks), dim3(kThreads), 0, st,
                        tokens, N, L, row_stride, width, key, tm1, gamma, io);
   else
@@ -1539,6 +1539,9 @@ sbw_status_t detect_impl(const int32_t* tokens, int64_t N, int64_t L, int64_t ro
   if (w == 1) {
     if (ctx) launch_detect<kContext, 1>(positions, blocks, st, tokens, N, L, row_stride, w, key, tm1, gamma, io);
     else launch_detect<kSelfSalt, 1>(positions, blocks, st, tokens, N, L, row_stride, w, key, tm1, gamma, io);
+  } else if (w <= kMidWidth) {
+    if (ctx) launch_detect<kContext, kMidWidth>(positions, blocks, st, tokens, N, L, row_stride, w, key, tm1, gamma, io);
+    else launch_detect<kSelfSalt, kMidWidth>(positions, blocks, st, tokens, N, L, row_stride, w, key, tm1, gamma, io);
   } else {
     if (ctx) launch_detect<kContext, kMaxWidth>(positions, blocks, st, tokens, N, L, row_stride, w, key, tm1, gamma, io);
     else launch_detect<kSelfSalt, kMaxWidth>(positions, blocks, st, tokens, N, L, row_stride, w, key, tm1, gamma, io);
