@@ -1381,6 +1381,9 @@ void dispatch_candidates(void* logits, int64_t B, uint32_t V, int64_t row_stride
   else if (width == 1)
     hipLaunchKernelGGL((candidates_kernel<T, kSelfSalt, 1>), grid, dim3(kThreads), 0, st, p,
                        row_stride, V, B, cand, k, context, width, key, tm1, delta);
+  else if (width <= kMidWidth)
+    hipLaunchKernelGGL((candidates_kernel<T, kSelfSalt, kMidWidth>), grid, dim3(kThreads), 0, st,
+                       p, row_stride, V, B, cand, k, context, width, key, tm1, delta);
   else
     hipLaunchKernelGGL((candidates_kernel<T, kSelfSalt, kMaxWidth>), grid, dim3(kThreads), 0, st,
                        p, row_stride, V, B, cand, k, context, width, key, tm1, delta);
@@ -1461,6 +1464,10 @@ void dispatch_argmax(const void* logits, int64_t B, uint32_t V, int64_t row_stri
     launch_argmax<T, kSelfSalt, 1, kSample>(logits, B, V, row_stride, context, width, key, tm1,
                                             none, delta, sa, vbase, aligned, tokens, values,
                                             partials, st);
+  else if (width <= kMidWidth)
+    launch_argmax<T, kSelfSalt, kMidWidth, kSample>(logits, B, V, row_stride, context, width, key,
+                                                    tm1, none, delta, sa, vbase, aligned, tokens,
+                                                    values, partials, st);
   else
     launch_argmax<T, kSelfSalt, kMaxWidth, kSample>(logits, B, V, row_stride, context, width, key,
                                                     tm1, none, delta, sa, vbase, aligned, tokens,
