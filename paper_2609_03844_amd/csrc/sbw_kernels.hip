@@ -1536,6 +1536,9 @@ sbw_status_t detect_impl(const int32_t* tokens, int64_t N, int64_t L, int64_t ro
     if (w == 1) {
       if (ctx) launch_detect_unique<kContext, 1>(N, st, tokens, L, row_stride, w, key, tm1, gamma, slots, io);
       else launch_detect_unique<kSelfSalt, 1>(N, st, tokens, L, row_stride, w, key, tm1, gamma, slots, io);
+    } else if (w <= kMidWidth) {
+      if (ctx) launch_detect_unique<kContext, kMidWidth>(N, st, tokens, L, row_stride, w, key, tm1, gamma, slots, io);
+      else launch_detect_unique<kSelfSalt, kMidWidth>(N, st, tokens, L, row_stride, w, key, tm1, gamma, slots, io);
     } else {
       if (ctx) launch_detect_unique<kContext, kMaxWidth>(N, st, tokens, L, row_stride, w, key, tm1, gamma, slots, io);
       else launch_detect_unique<kSelfSalt, kMaxWidth>(N, st, tokens, L, row_stride, w, key, tm1, gamma, slots, io);
