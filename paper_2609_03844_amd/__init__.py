@@ -21,6 +21,7 @@ column c being token v_offset + c (``sbw_*_shard`` in the C ABI); ``watermark_sh
 from __future__ import annotations
 
 import ctypes
+import functools
 import os
 
 import torch  # loads torch's HIP runtime first, so libsbw binds to the same one
@@ -148,8 +149,20 @@ def _seeding(s) -> int:
     return int(s)
 
 
+# The current device and its current stream straight from torch's C layer: building a
+# torch.cuda.Stream object per call costs about 3 us, more than a small launch.
+_raw_stream = getattr(torch._C, "_cuda_getCurrentRawStream", None)
+_get_device = getattr(torch._C, "_cuda_getDevice", None)
+
+
+def _current_device() -> int:
+    return _get_device() if _get_device is not None else torch.cuda.current_device()
+
+
 def _stream(stream) -> int:
     if stream is None:
+        if _raw_stream is not None:
+            return _raw_stream(_current_device())
         return torch.cuda.current_stream().cuda_stream
     return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
 
@@ -168,8 +181,8 @@ def _on_device(**tensors) -> None:
         if not t.is_cuda:
             raise ValueError(f"{name} must be on the current HIP device, got {t.device}")
         if dev is None:
-            dev = torch.cuda.current_device()
-        if t.device.index != dev:
+            dev = _current_device()
+        if t.get_device() != dev:
             raise ValueError(f"{name} must be on the current HIP device (cuda:{dev}), "
                              f"got {t.device}")
 
@@ -393,6 +406,7 @@ def watermark_sample_shard(logits: torch.Tensor, prev_tokens: torch.Tensor, v_of
                             inv_temperature, v_offset=v_offset, **kw)
 
 
+@functools.lru_cache(maxsize=1024)
 def argmax_workspace_size(B: int, V: int) -> int:
     """uint64 elements of scratch that watermark_argmax needs for B rows of V logits."""
     return int(_lib.sbw_watermark_argmax_workspace(int(B), int(V)))
