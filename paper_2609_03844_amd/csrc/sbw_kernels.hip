@@ -1055,6 +1055,14 @@ green_mask_kernel(uint32_t* __restrict__ bits, uint32_t V, uint32_t words_per_ro
 constexpr int kWave = 64;
 constexpr int kWavesPerBlock = kThreads / kWave;
 
+// Self-salt membership of token v after token p, from J(p) and J(v).
+__device__ __forceinline__ bool green_from_hashes(uint64_t key, uint32_t jp, uint32_t jv, uint32_t v,
+                                                  uint32_t tm1) {
+  const uint64_t self = mul_64x64(key, wide_mul(jv, jv));
+  const uint64_t t = mul_64x32(key * static_cast<uint64_t>(jp), jv);
+  return is_green(cbrng(v, t < self ? t : self), tm1);
+}
+
 // Membership of token v at a position whose window is w[0..width-1].
 template <int kSeeding, int kW>
 __device__ __forceinline__ bool window_green(uint64_t key, const uint32_t (&w)[kW], int width,
@@ -1128,18 +1136,40 @@ detect_kernel(const int32_t* __restrict__ tokens, int64_t N, int64_t L, int64_t 
         for (int k = 0; k < kW; ++k) w[c][k] = 0u;
         if (i < len) {
           v[c] = static_cast<uint32_t>(seq[i]);
+          constexpr bool kShared = kSeeding == kSelfSalt && kW == 1;   // hashes handed over
 #pragma unroll
           for (int k = 0; k < kW; ++k)
-            if (kW == 1 || k < width) w[c][k] = static_cast<uint32_t>(seq[i - width + k]);
+            if ((kW == 1 || k < width) && (!kShared || c == 0))
+              w[c][k] = static_cast<uint32_t>(seq[i - width + k]);
         }
       }
       // Independent membership chains first (instruction-level parallelism), then
       // one ballot per chunk.
       bool g[kChunk];
+      if constexpr (kSeeding == kSelfSalt && kW == 1) {
+        // Self-salt, width 1: the hash of position i's previous token is the hash of
+        // position i - 1's token, held by the lane before (lane 63 of the chunk before,
+        // for lane 0; the window token itself for the pass's first position).  A wave
+        // shift hands it over instead of hashing every token twice.
+        uint32_t jv[kChunk];
 #pragma unroll
-      for (int c = 0; c < kChunk; ++c) {
-        const int64_t i = base + c * kWave + lane;
-        g[c] = window_green<kSeeding, kW>(key, w[c], width, v[c], tm1) && i < len;
+        for (int c = 0; c < kChunk; ++c) jv[c] = jenkins32(v[c]);
+        uint32_t carry = jenkins32(w[0][0]);
+#pragma unroll
+        for (int c = 0; c < kChunk; ++c) {
+          if (c > 0) carry = __builtin_amdgcn_readlane(jv[c - 1], kWave - 1);
+          // wave_shr:1: lane t takes lane t - 1's value, lane 0 keeps `carry`
+          const uint32_t jp = static_cast<uint32_t>(__builtin_amdgcn_update_dpp(
+              static_cast<int>(carry), static_cast<int>(jv[c]), 0x138, 0xF, 0xF, false));
+          const int64_t i = base + c * kWave + lane;
+          g[c] = green_from_hashes(key, jp, jv[c], v[c], tm1) && i < len;
+        }
+      } else {
+#pragma unroll
+        for (int c = 0; c < kChunk; ++c) {
+          const int64_t i = base + c * kWave + lane;
+          g[c] = window_green<kSeeding, kW>(key, w[c], width, v[c], tm1) && i < len;
+        }
       }
 #pragma unroll
       for (int c = 0; c < kChunk; ++c) green += static_cast<uint32_t>(__popcll(__ballot(g[c])));
