@@ -224,3 +224,60 @@ def test_detection_sharded_along_the_text(env, seeding, width):
     assert np.all(scored == L - width)
     z = (counts - scored * gamma) / np.sqrt(scored * gamma * (1 - gamma))
     np.testing.assert_allclose(z, ez, rtol=1e-6, atol=1e-9)
+
+
+def test_shard_calls_replay_in_a_graph(env):
+    """Two shards watermarked and decoded inside one captured graph: every replay, with
+    eager work and the outputs clobbered in between, gives the oracle's results."""
+    torch, sbw, dev = env
+    rng = np.random.default_rng(950)
+    B, V, cut = 8, 40003, 20000
+    key, gamma, delta = WIDE, 0.25, 2.0
+    x = rng.standard_normal((B, V)).astype(np.float32)
+    prev = rng.integers(0, V, B).astype(np.int32)
+    seeds = seeds_for(rng, B)
+    src = torch.from_numpy(x).to(dev)
+    p = torch.from_numpy(prev).to(dev)
+    s_dev = torch.from_numpy(seeds.view(np.int64)).to(dev)
+    buf = torch.empty_like(src)
+    halves = [(0, cut), (cut, V)]
+    outs = [(torch.empty(B, dtype=torch.int32, device=dev), torch.empty(B, device=dev),
+             torch.empty(B, dtype=torch.int32, device=dev), torch.empty(B, device=dev))
+            for _ in halves]
+    wss = [torch.empty(sbw.argmax_workspace_size(B, b - a), dtype=torch.int64, device=dev)
+           for a, b in halves]
+
+    def work():
+        for (a, b), o, ws in zip(halves, outs, wss):
+            view = src[:, a:b]
+            sbw.watermark_argmax_shard(view, p, a, key, gamma, delta, "self_salt", tokens=o[0],
+                                       values=o[1], workspace=ws)
+            sbw.watermark_sample_shard(view, p, a, key, gamma, delta, s_dev, "self_salt",
+                                       tokens=o[2], scores=o[3], workspace=ws)
+        buf.copy_(src)
+        for a, b in halves:
+            sbw.watermark_shard(buf[:, a:b], p, a, key, gamma, delta, "self_salt")
+
+    e_wm = oracle.watermark(x, prev, key, gamma, delta, "self_salt")
+    e_am = oracle.watermark_argmax(x, prev, key, gamma, delta, "self_salt")
+    e_sm = oracle.watermark_sample(x, prev, key, gamma, delta, "self_salt", seeds, 1.0)
+    work()
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        work()
+    scratch = torch.randn(1 << 20, device=dev)
+    for replay in range(4):
+        buf.fill_(float("nan"))
+        for o in outs:
+            o[0].fill_(-1); o[1].fill_(0.0); o[2].fill_(-1); o[3].fill_(0.0)
+        scratch.mul_(1.0001)
+        torch.cuda.synchronize()
+        say(f"shard graph replay {replay}")
+        g.replay()
+        torch.cuda.synchronize()
+        assert np.array_equal(buf.cpu().numpy().view(np.uint32), e_wm.view(np.uint32)), replay
+        greedy = combine([(o[0].cpu().numpy(), o[1].cpu().numpy()) for o in outs])
+        sample = combine([(o[2].cpu().numpy(), o[3].cpu().numpy()) for o in outs])
+        assert_argmax_equal(greedy, e_am, f"greedy replay {replay}")
+        assert_argmax_equal(sample, e_sm, f"sample replay {replay}")
