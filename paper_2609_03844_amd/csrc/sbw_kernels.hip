@@ -406,6 +406,9 @@ watermark_elem_kernel(T* __restrict__ logits, int64_t row_stride, uint32_t V, in
 // sampling), and sub-batches per workgroup segment.  A longer segment gives each wave
 // a larger sample for its bounds; every lane holds a sub-batch in registers, and bf16
 // takes fewer vectors to hold its 8-token bounds.
+#ifndef SBW_DECODE_VECS_F32_GREEDY
+#define SBW_DECODE_VECS_F32_GREEDY 6   // greedy decoding, fp32 (sampling keeps 8)
+#endif
 #ifndef SBW_DECODE_VECS_F32
 #define SBW_DECODE_VECS_F32 8
 #endif
@@ -1421,8 +1424,9 @@ void dispatch_candidates(void* logits, int64_t B, uint32_t V, int64_t row_stride
 
 // Segments per row of the fused decoding: vector path and element path.
 template <typename T>
-constexpr int decode_vecs_for() {
-  return sizeof(T) == 4 ? SBW_DECODE_VECS_F32 : SBW_DECODE_VECS_BF16;
+constexpr int decode_vecs_for(bool sample) {
+  return sizeof(T) == 4 ? (sample ? SBW_DECODE_VECS_F32 : SBW_DECODE_VECS_F32_GREEDY)
+                        : SBW_DECODE_VECS_BF16;
 }
 template <typename T>
 constexpr uint64_t vec_segment_elems(int kN) { return (16u / sizeof(T)) * kThreads * kN; }
@@ -1433,6 +1437,7 @@ constexpr uint64_t vec_segment_elems(int kN) { return (16u / sizeof(T)) * kThrea
 constexpr int64_t kSmallDecodeGrid = 1024;
 // The workspace is sized for the element path; vector segments must be at least as long.
 static_assert(vec_segment_elems<float>(SBW_DECODE_VECS_F32 / 2) >= kArgmaxSegElems &&
+                  vec_segment_elems<float>(SBW_DECODE_VECS_F32_GREEDY / 2) >= kArgmaxSegElems &&
                   vec_segment_elems<uint16_t>(SBW_DECODE_VECS_BF16 / 2) >= kArgmaxSegElems,
               "vector segments must not outnumber element segments");
 
@@ -1451,7 +1456,7 @@ void launch_argmax(const void* logits, int64_t B, uint32_t V, int64_t row_stride
   const uint32_t rows = static_cast<uint32_t>(B < kMaxGridY ? B : kMaxGridY);
   uint32_t segments;
   if (aligned) {
-    constexpr int kN = decode_vecs_for<T>();
+    constexpr int kN = decode_vecs_for<T>(kSample);
     constexpr int kNs = kN / 2;
     const uint64_t seg = vec_segment_elems<T>(kN) * SBW_DECODE_SUBS;
     segments = static_cast<uint32_t>((static_cast<uint64_t>(V) + seg - 1) / seg);
