@@ -38,6 +38,16 @@ void oracle_watermark_sample_f32_w(const float *logits, int64_t B, int64_t V, in
 void oracle_detect_w(const int32_t *tokens, int64_t N, int64_t L, int64_t row_stride,
                      int64_t width, uint64_t key, double gamma, int seeding,
                      int32_t *green_counts, double *z);
+void oracle_green_mask_w(uint32_t *bits, int64_t B, int64_t V, const int32_t *context,
+                         int64_t width, uint64_t key, double gamma, int seeding);
+void oracle_watermark_candidates_f32_w(float *logits, int64_t B, int64_t V, int64_t row_stride,
+                                       const int32_t *cand, int64_t k, const int32_t *context,
+                                       int64_t width, uint64_t key, double gamma, float delta,
+                                       int seeding);
+void oracle_detect_ex(const int32_t *tokens, int64_t N, int64_t L, int64_t row_stride,
+                      const int32_t *lengths, int64_t width, uint64_t key, double gamma,
+                      int seeding, int ignore_repeated, int32_t *green_counts, int32_t *scored,
+                      double *z);
 
 static uint64_t rng_state;
 static uint64_t next_u64(void)
@@ -177,6 +187,67 @@ static int gpu_checks(void)
         CHECK(memcmp(gcount, ecount, sizeof ecount) == 0, "detect counts, seeding %d", seeding);
         for (int i = 0; i < N; ++i)
             CHECK(fabs(gz[i] - ez[i]) <= 1e-6 * fabs(ez[i]) + 1e-12, "detect z, seeding %d", seeding);
+        /* green masks */
+        {
+            const int64_t words = (V + 31) / 32;
+            uint32_t *gbits = malloc((size_t)(B * words) * sizeof(uint32_t)),
+                     *ebits = malloc((size_t)(B * words) * sizeof(uint32_t)), *d_bits;
+            CHECK(gbits && ebits, "host allocation");
+            HIP(hipMalloc((void **)&d_bits, (size_t)(B * words) * sizeof(uint32_t)));
+            SBW(sbw_green_mask_window(d_bits, B, V, d_ctx, W, key, gamma, sd, NULL));
+            HIP(hipMemcpy(gbits, d_bits, (size_t)(B * words) * sizeof(uint32_t), hipMemcpyDeviceToHost));
+            oracle_green_mask_w(ebits, B, V, ctx, W, key, gamma, seeding);
+            CHECK(memcmp(gbits, ebits, (size_t)(B * words) * sizeof(uint32_t)) == 0,
+                  "green mask, seeding %d", seeding);
+            HIP(hipFree(d_bits));
+            free(gbits); free(ebits);
+        }
+        /* the watermark on 40 candidate ids per row (one out of range, one repeated) */
+        {
+            int32_t cand[8 * 40], *d_cand;
+            for (int i = 0; i < B * 40; ++i) cand[i] = (int32_t)(next_u64() % (uint64_t)V);
+            cand[5] = (int32_t)V;
+            cand[7] = cand[6];
+            HIP(hipMalloc((void **)&d_cand, sizeof cand));
+            HIP(hipMemcpy(d_cand, cand, sizeof cand, hipMemcpyHostToDevice));
+            HIP(hipMemcpy(d_x, x, nl * sizeof(float), hipMemcpyHostToDevice));
+            SBW(sbw_watermark_candidates(d_x, SBW_F32, B, V, V, d_cand, 40, d_ctx, W, key, gamma,
+                                         delta, sd, NULL));
+            HIP(hipMemcpy(got, d_x, nl * sizeof(float), hipMemcpyDeviceToHost));
+            memcpy(expect, x, nl * sizeof(float));
+            oracle_watermark_candidates_f32_w(expect, B, V, V, cand, 40, ctx, W, key, gamma, delta,
+                                              seeding);
+            CHECK(memcmp(got, expect, nl * sizeof(float)) == 0, "candidates, seeding %d", seeding);
+            HIP(hipFree(d_cand));
+        }
+        /* detection with per-text lengths and the repeated-n-gram rule */
+        {
+            int32_t lens[16], *d_lens, gscored[16], escored[16], *d_scored;
+            for (int i = 0; i < N; ++i) lens[i] = (int32_t)(next_u64() % (uint64_t)(L + 1));
+            for (int i = 0; i < L / 2; ++i) tok[3 * L + L / 2 + i] = tok[3 * L + i];  /* repeats */
+            HIP(hipMemcpy(d_tok, tok, sizeof tok, hipMemcpyHostToDevice));
+            HIP(hipMalloc((void **)&d_lens, sizeof lens));
+            HIP(hipMalloc((void **)&d_scored, sizeof gscored));
+            HIP(hipMemcpy(d_lens, lens, sizeof lens, hipMemcpyHostToDevice));
+            for (int rule = 0; rule < 2; ++rule) {
+                SBW(sbw_detect_ex(d_tok, N, L, L, d_lens, W, key, gamma, sd,
+                                  rule ? (uint32_t)SBW_DETECT_IGNORE_REPEATED : 0u, d_count,
+                                  d_scored, d_z, NULL));
+                HIP(hipMemcpy(gcount, d_count, sizeof gcount, hipMemcpyDeviceToHost));
+                HIP(hipMemcpy(gscored, d_scored, sizeof gscored, hipMemcpyDeviceToHost));
+                HIP(hipMemcpy(gz, d_z, sizeof gz, hipMemcpyDeviceToHost));
+                oracle_detect_ex(tok, N, L, L, lens, W, key, gamma, seeding, rule, ecount, escored, ez);
+                CHECK(memcmp(gcount, ecount, sizeof ecount) == 0 &&
+                      memcmp(gscored, escored, sizeof escored) == 0,
+                      "detect_ex counts, rule %d, seeding %d", rule, seeding);
+                for (int i = 0; i < N; ++i)
+                    CHECK((isnan(gz[i]) && isnan(ez[i])) ||
+                          fabs(gz[i] - ez[i]) <= 1e-6 * fabs(ez[i]) + 1e-12,
+                          "detect_ex z, rule %d, seeding %d", rule, seeding);
+            }
+            HIP(hipFree(d_lens));
+            HIP(hipFree(d_scored));
+        }
         printf("capi gpu seeding %d ok\n", seeding);
     }
     HIP(hipFree(d_x)); HIP(hipFree(d_vals)); HIP(hipFree(d_ctx)); HIP(hipFree(d_tok));
