@@ -2,8 +2,9 @@
 
 Each case draws a shape (B, V), dtype, seeding, window width, gamma, delta, 1/T, row
 padding and an unaligned row start, then checks the watermark (bit for bit), greedy
-decoding and sampling (tokens and value bits) and detection with lengths and the
-repeat rule.  The cases are fixed by the seed, so a failure names a reproducible case.
+decoding and sampling (tokens and value bits), the row split into two vocabulary
+shards at a random column, and detection with lengths and the repeat rule.  The cases
+are fixed by the seed, so a failure names a reproducible case.
 """
 import numpy as np
 import pytest
@@ -15,7 +16,7 @@ from test_gpu_parity import WIDE, _from_device, _to_device, assert_logits_equal,
 
 pytestmark = pytest.mark.gpu
 
-CASES = 40
+CASES = 150
 
 
 def draw_case(i):
@@ -62,6 +63,16 @@ def test_random_case(env, i):
     torch.cuda.synchronize()
     assert_logits_equal(_from_device(torch, t).copy(),
                         oracle.watermark_w(x, ctx, WIDE, gamma, delta, seeding), f"case {i}")
+
+    if V > 1:                                  # the same row as two vocabulary shards
+        cut = int(rng.integers(1, V))
+        t = laid_out(env, x, pad, offset)
+        sbw.watermark_shard(t[:, :cut], c, 0, WIDE, gamma, delta, seeding)
+        sbw.watermark_shard(t[:, cut:], c, cut, WIDE, gamma, delta, seeding)
+        torch.cuda.synchronize()
+        assert_logits_equal(_from_device(torch, t).copy(),
+                            oracle.watermark_w(x, ctx, WIDE, gamma, delta, seeding),
+                            f"case {i} shards at {cut}")
 
     t = laid_out(env, x, pad, offset)
     tok, val = sbw.watermark_argmax(t, c, WIDE, gamma, delta, seeding)
