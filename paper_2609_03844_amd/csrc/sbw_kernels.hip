@@ -415,6 +415,9 @@ watermark_elem_kernel(T* __restrict__ logits, int64_t row_stride, uint32_t V, in
 #ifndef SBW_DECODE_VECS_BF16
 #define SBW_DECODE_VECS_BF16 4
 #endif
+#ifndef SBW_DECODE_VECS_BF16_SAMPLE
+#define SBW_DECODE_VECS_BF16_SAMPLE 5   // sampling, bf16 (greedy keeps 4)
+#endif
 #ifndef SBW_DECODE_SUBS
 #define SBW_DECODE_SUBS 1
 #endif
@@ -1426,19 +1429,21 @@ void dispatch_candidates(void* logits, int64_t B, uint32_t V, int64_t row_stride
 template <typename T>
 constexpr int decode_vecs_for(bool sample) {
   return sizeof(T) == 4 ? (sample ? SBW_DECODE_VECS_F32 : SBW_DECODE_VECS_F32_GREEDY)
-                        : SBW_DECODE_VECS_BF16;
+                        : (sample ? SBW_DECODE_VECS_BF16_SAMPLE : SBW_DECODE_VECS_BF16);
 }
 template <typename T>
 constexpr uint64_t vec_segment_elems(int kN) { return (16u / sizeof(T)) * kThreads * kN; }
 // Small grids: a launch of fewer workgroups than this takes half the vectors per lane
 // (twice the segments), which hides more of the load latency when the chip is not
 // full: a vocabulary shard of 19008 fp32 or bf16 logits at B = 256 gets 1280
-// workgroups instead of 768 (about 8 % faster); B = 64 rows of 152064 (1216) stay.
-constexpr int64_t kSmallDecodeGrid = 1024;
+// workgroups instead of 768 (about 8 % faster); B = 64 rows of 152064 (960-1600
+// workgroups) stay.
+constexpr int64_t kSmallDecodeGrid = 900;
 // The workspace is sized for the element path; vector segments must be at least as long.
 static_assert(vec_segment_elems<float>(SBW_DECODE_VECS_F32 / 2) >= kArgmaxSegElems &&
                   vec_segment_elems<float>(SBW_DECODE_VECS_F32_GREEDY / 2) >= kArgmaxSegElems &&
-                  vec_segment_elems<uint16_t>(SBW_DECODE_VECS_BF16 / 2) >= kArgmaxSegElems,
+                  vec_segment_elems<uint16_t>(SBW_DECODE_VECS_BF16 / 2) >= kArgmaxSegElems &&
+                  vec_segment_elems<uint16_t>(SBW_DECODE_VECS_BF16_SAMPLE / 2) >= kArgmaxSegElems,
               "vector segments must not outnumber element segments");
 
 // The per-row noise seeds and 1/T of a sampling pass (unused by greedy decoding).

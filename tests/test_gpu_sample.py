@@ -203,8 +203,8 @@ def test_sample_windows(env, dtype, seeding, width):
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("seeding", ["context", "self_salt"])
 def test_sample_both_launch_shapes(env, dtype, seeding):
-    """The queue-round rows tiled to 256 rows (the full-width decode kernel: 5 segments
-    per row, 1280 workgroups) and to 8 rows (the half-width kernel for small grids)."""
+    """The queue-round rows tiled to 256 rows (the full-width decode kernel: more than
+    900 workgroups) and to 8 rows (the half-width kernel for small grids)."""
     rng = np.random.default_rng(470)
     V = 40001
     edge = queue_rows(rng, V, dtype)
