@@ -5,19 +5,24 @@ One step = one pass of the whole hot path over one batch:
      (3*N(0,1) + 8 on 5 % of entries), gamma=0.25, delta=2, in place
   2. watermark, context seeding, same shape and parameters
   3. detect, self-salt, N=4096 x L=512 token ids over V=128256 (half null,
-     half watermarked)
+     half watermarked by the oracle's membership)
   4. detect, context seeding, the same batch shape
 The timed region runs exactly `--steps` steps: each kernel's `steps` launches are
 captured in one HIP graph and the four graphs are replayed back to back, with a
 HIP event (on the launching stream) at each group boundary; a kernel's mean launch
-duration is its group time / steps.  Logits rotate over six
-156 MB buffers, so no watermark launch is served from the 256 MB Infinity Cache
-left by the previous one: every launch reads HBM.  A separate pass after the timed
-region brackets single launches with events for p50/p95/p99 latencies.
+duration is its group time / steps.  Before it, the graphs are replayed until
+`--warm-ms` of GPU time have passed: after idle, an all-VALU pass runs up to 30 %
+slower for its first ~30 ms of load while the chip's power management settles, and
+the timed region must not sit inside that transient, whatever `--steps` is.  Logits
+rotate over six 156 MB buffers, so no watermark launch is served from the 256 MB
+Infinity Cache left by the previous one: every launch reads HBM.  A separate pass
+after the timed region brackets single launches with events for p50/p95/p99.
 
 `value` is the self-salt watermark throughput in Gelem/s (B*V / mean launch
-time), the configuration the metric names; the context-seeded launch (the
-HBM-bound one) and the detect launches are reported beside it.  All inputs are
+time), the configuration the metric names.  `roofline` is that kernel's, against
+the Philox4x32-10 roof (derived from issue slots, and measured in the same run by
+the probe library libsbw_rate.so at the clock the chip runs); `roofline.hbm_context`
+is the context-seeded launch at the same shape, the HBM-bound one.  All inputs are
 synthetic and resident in HBM before the timed region starts.
 """
 from __future__ import annotations
@@ -39,10 +44,15 @@ import workloads  # noqa: E402
 
 HBM_PEAK_GBPS = 8000.0                 # MI355X HBM3E
 CUS, LANES, CLOCK_GHZ = 256, 64, 2.4   # MI355X compute units, wave width, peak clock
-# One Philox4x32-10 block with a per-lane key needs at least 58 full-rate VALU lane-ops:
-# 20 32x32->64-bit products (v_mad_u64_u32), 20 three-input xors, 18 key-schedule adds.
-PHILOX_LANE_OPS = 58
-PHILOX_PEAK_GBLOCKS = CUS * LANES * CLOCK_GHZ / PHILOX_LANE_OPS
+# One Philox4x32-10 block with a fresh per-lane key is 58 VALU lane-ops: 18 32x32->64-bit
+# products (v_mad_u64_u32; round 0 multiplies the shared counter word), 20 three-input
+# xors (v_bitop3_b32) and 2 more xors, 18 key-schedule adds (v_add_u32).  gfx950 issues
+# one VALU instruction per lane per clock, except that two v_add_u32 can share an issue
+# slot (the probe library measures 60 of 64 lane-ops per CU-clock for products and
+# xors, 113 of 128 for adds).  So a block takes 40 + 18/2 = 49 issue slots per lane:
+PHILOX_ISSUE_SLOTS = 40 + 18 / 2
+PHILOX_PEAK_GBLOCKS = CUS * LANES * CLOCK_GHZ / PHILOX_ISSUE_SLOTS
+RATE_LIBRARY = os.path.join(ROOT, "paper_2609_03844_amd", "libsbw_rate.so")
 PROFILE = os.path.join(ROOT, "profiles", "watermark_detect_c4_c5.json")          # main step
 PROFILE_CONFIGS = os.path.join(ROOT, "profiles", "configs_c1_c4_argmax_paper_table.json")
 KERNEL_SOURCES = ("paper_2609_03844_amd/csrc/sbw_kernels.hip",
@@ -74,10 +84,12 @@ def parse():
     ap.add_argument("--latency-samples", type=int, default=50)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-configs", action="store_true")
-    ap.add_argument("--cpu-seconds", type=float, default=10.0)
-    ap.add_argument("--power-probe", action="store_true",
-                    help="only run the self-salt pass back to back for ~2.5 s while sampling "
-                         "the GFX clock and socket power with amd-smi; print them as JSON")
+    ap.add_argument("--warm-ms", type=float, default=100.0,
+                    help="GPU time of graph replays before the timed region")
+    ap.add_argument("--cpu-runs", type=int, default=10,
+                    help="timed runs of each CPU-oracle measurement (after 3 warm-up runs)")
+    ap.add_argument("--launch-only", type=int, default=0, metavar="K",
+                    help="launch every measured kernel K times eagerly and exit (for profilers)")
     return ap.parse_args()
 
 
@@ -85,56 +97,213 @@ def percentile(xs, q):
     return float(np.percentile(np.asarray(xs), q))
 
 
-def gpu_membership(sbw, torch, dev, key, gamma, seeding):
-    """Green-list membership of (prev, cand) pairs through the library's detect
-    entry point: a 2-token sequence [prev, cand] scores 1 iff cand is green."""
+def oracle_membership(key, gamma, seeding):
+    """Green-list membership of (prev, cand) pairs by the CPU oracle, for the
+    watermarked half of the detect batch (the batch does not depend on the code
+    under test)."""
+    import oracle
+
     def member(p, v):
-        pairs = torch.from_numpy(np.stack([p, v], axis=1).astype(np.int32)).to(dev)
-        counts, _ = sbw.detect(pairs, key, gamma, seeding)
-        return (counts == 1).cpu().numpy()
+        return oracle.is_green_many(key, p, v, gamma, seeding)
     return member
 
 
-def cpu_baseline(x, prev, tok_ss, seconds):
-    """The CPU oracle, untuned and single-threaded, on a bounded sample."""
+def _threads():
+    try:
+        return len(os.sched_getaffinity(0))
+    except AttributeError:
+        return os.cpu_count() or 1
+
+
+def _split_run(fn, n, threads):
+    """fn(lo, hi) over [0, n) cut into `threads` contiguous slices, one Python thread
+    each (the oracle's ctypes calls release the GIL)."""
+    import threading
+    cuts = [n * t // threads for t in range(threads + 1)]
+    ts = [threading.Thread(target=fn, args=(cuts[t], cuts[t + 1]))
+          for t in range(threads) if cuts[t + 1] > cuts[t]]
+    for t in ts:
+        t.start()
+    for t in ts:
+        t.join()
+
+
+def _median_seconds(run, runs, warmup=3):
+    for _ in range(warmup):
+        run()
+    times = []
+    for _ in range(runs):
+        t0 = time.perf_counter()
+        run()
+        times.append(time.perf_counter() - t0)
+    return float(np.median(times))
+
+
+def cpu_baseline(x, prev, toks, runs):
+    """The CPU oracle as it stands (plain single-threaded C, untuned), timed on this
+    host: the same function over row slices (sequence slices for detect) from one
+    Python thread per available core, and from one thread on a smaller sample.  Each
+    figure is the median of `runs` timed runs after 3 warm-up runs."""
     import oracle
-    c = workloads.C4
-    rows = 64
-    sample = np.ascontiguousarray(x[:rows])
-    p = prev[:rows]
-    passes, t0 = 0, time.perf_counter()
-    while True:
-        oracle.watermark(sample, p, workloads.PAPER_KEY, c["gamma"], c["delta"], "self_salt")
-        passes += 1
-        if time.perf_counter() - t0 >= 0.8 * seconds:
-            break
-    wm_s = time.perf_counter() - t0
-    det_passes, t1 = 0, time.perf_counter()
-    while True:
-        oracle.detect(tok_ss, workloads.PAPER_KEY, workloads.C5["gamma"], "self_salt")
-        det_passes += 1
-        if time.perf_counter() - t1 >= 0.2 * seconds:
-            break
-    det_s = time.perf_counter() - t1
-    elems = passes * rows * x.shape[1]
-    return {
-        "value": elems / wm_s / 1e9,
-        "unit": "Gelem/s",
-        "cores": 1,
-        "kind": "oracle",
-        "sample": (f"self-salt watermark of c4 rows 0-{rows - 1} (64 x {x.shape[1]} fp32), "
-                   f"{passes} passes in {wm_s:.1f} s; self-salt detect of the c5 batch "
-                   f"({tok_ss.shape[0]} x {tok_ss.shape[1]}), {det_passes} passes in {det_s:.1f} s"),
-        "detect_seq_per_s": det_passes * tok_ss.shape[0] / det_s,
-        "cpu": _cpu_model(),
-        "nproc": os.cpu_count(),
-    }
+    c4, c5, key = workloads.C4, workloads.C5, workloads.PAPER_KEY
+    threads = _threads()
+    B, V = x.shape
+    rows_1t = min(32, B)                            # the one-thread sample
+    out = {"unit": "Gelem/s", "kind": "oracle", "cores": threads, "cpu": _cpu_model(),
+           "nproc": os.cpu_count(), "runs": f"3 warm-up + {runs} timed, median"}
+    wm = {}
+    for seeding in ("self_salt", "context"):
+        def rows(lo, hi, s=seeding):
+            oracle.watermark(x[lo:hi], prev[lo:hi], key, c4["gamma"], c4["delta"], s)
+        t_all = _median_seconds(lambda: _split_run(rows, B, threads), runs)
+        t_one = _median_seconds(lambda: rows(0, rows_1t), runs)
+        wm[seeding] = {"gelem_per_s": B * V / t_all / 1e9,
+                       "gelem_per_s_1thread": rows_1t * V / t_one / 1e9}
+    det = {}
+    for seeding, tok in toks.items():
+        N = tok.shape[0]
+        n_1t = min(512, N)
+
+        def seqs(lo, hi, s=seeding, t=tok):
+            oracle.detect(t[lo:hi], key, c5["gamma"], s)
+        t_all = _median_seconds(lambda: _split_run(seqs, N, threads), runs)
+        t_one = _median_seconds(lambda: seqs(0, n_1t), runs)
+        det[seeding] = {"seq_per_s": N / t_all, "seq_per_s_1thread": n_1t / t_one}
+    out.update({
+        "value": wm["self_salt"]["gelem_per_s"],
+        "value_1thread": wm["self_salt"]["gelem_per_s_1thread"],
+        "watermark": wm,
+        "detect_seq_per_s": det["self_salt"]["seq_per_s"],
+        "detect": det,
+        "sample": (f"c4 watermark (B={B} x V={V} fp32, gamma={c4['gamma']}, delta={c4['delta']}) "
+                   f"over {threads} threads, and rows 0-{rows_1t - 1} on one thread; c5 detect "
+                   f"({toks['self_salt'].shape[0]} x {toks['self_salt'].shape[1]}) over {threads} "
+                   f"threads, and its first {min(512, toks['self_salt'].shape[0])} sequences on one "
+                   f"thread; both seedings"),
+    })
+    return out
 
 
-def _mean_us(torch, launch, n_launch, warmup=10, warm_ms=5.0, reps=3):
+def philox_roof(torch, warm_ms=50.0, reps=10):
+    """The Philox4x32-10 roof measured on this GPU by libsbw_rate.so: blocks with a
+    fresh per-lane key each (the self-salt draw), no memory traffic, the chip full of
+    waves, timed after `warm_ms` of the same load.  The probe's workgroups also read
+    the shader-clock and real-time counters, which give the core clock it ran at.
+    The single-instruction chains give each instruction kind's issue rate in
+    lane-ops per compute-unit clock (64 is one VALU issue per lane per clock)."""
+    import ctypes
+    lib = ctypes.CDLL(RATE_LIBRARY)
+    P, i32, u32 = ctypes.c_void_p, ctypes.c_int, ctypes.c_uint32
+    lib.sbw_rate_philox.restype = i32
+    lib.sbw_rate_philox.argtypes = [P, P, i32, i32, u32, P]
+    lib.sbw_rate_op.restype = i32
+    lib.sbw_rate_op.argtypes = [i32, P, P, i32, i32, u32, P]
+    threads, chains = lib.sbw_rate_threads(), lib.sbw_rate_chains()
+    wall_hz = lib.sbw_rate_wall_clock_khz() * 1e3
+    workgroups = CUS * 8                     # 8 workgroups (32 waves) per compute unit
+    out_buf = torch.empty(workgroups * threads, dtype=torch.int32, device="cuda")
+    clk = torch.empty(4 * workgroups, dtype=torch.int64, device="cuda")
+    stream = torch.cuda.current_stream().cuda_stream
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+
+    def measure(launch, lane_ops):
+        spent = 0.0
+        while spent < warm_ms:
+            a.record()
+            launch()
+            b.record()
+            torch.cuda.synchronize()
+            spent += a.elapsed_time(b)
+        rates, mhz = [], []
+        for _ in range(reps):
+            a.record()
+            launch()
+            b.record()
+            torch.cuda.synchronize()
+            rates.append(lane_ops / (a.elapsed_time(b) * 1e-3))
+            c = clk.cpu().numpy().view(np.uint64).reshape(-1, 4).astype(np.float64)
+            mhz.append(float(np.median((c[:, 1] - c[:, 0]) / (c[:, 3] - c[:, 2]))) * wall_hz / 1e6)
+        return float(np.median(rates)), float(np.median(mhz))
+
+    def check(rc):
+        if rc != 0:
+            raise RuntimeError(f"libsbw_rate launch failed: hipError {rc}")
+
+    lanes = workgroups * threads
+    iters = 64
+    blocks = lanes * iters * chains
+    rate, mhz = measure(lambda: check(lib.sbw_rate_philox(out_buf.data_ptr(), clk.data_ptr(),
+                                                          workgroups, iters, 1, stream)), blocks)
+    issue = {}
+    op_iters = 128
+    for kind, name, per_link in ((1, "v_mad_u64_u32", 1), (2, "v_bitop3_b32", 1),
+                                 (3, "v_add_u32", 1), (4, "mix: mad + bitop3 + add", 3)):
+        ops = lanes * op_iters * 16 * chains * per_link
+        r, m = measure(lambda k=kind: check(lib.sbw_rate_op(k, out_buf.data_ptr(), clk.data_ptr(),
+                                                            workgroups, op_iters, 1, stream)), ops)
+        issue[name] = r / (CUS * m * 1e6)    # lane-ops per compute-unit clock
+    return {"gblocks_per_s": rate / 1e9, "clock_mhz": mhz,
+            "gblocks_per_s_at_2400mhz": rate / 1e9 * 2400.0 / mhz,
+            "blocks_per_cu_clock": rate / (CUS * mhz * 1e6),
+            "lane_ops_per_cu_clock": issue,
+            "probe": (f"{workgroups} workgroups x {threads} lanes, {iters * chains} blocks per "
+                      f"lane in {chains} chains, counter (c,0,0,0), a fresh key per block; "
+                      f"median of {reps} launches after {warm_ms:.0f} ms of the same load")}
+
+
+class ClockSampler:
+    """GFX clock readings (amdsmi, read-only) taken from a host thread every ~2 ms
+    while it runs; `between(t0, t1)` keeps the ones inside a wall-clock interval."""
+
+    def __init__(self):
+        import threading
+        self.samples, self._stop, self._th = [], threading.Event(), None
+        try:
+            import amdsmi
+            amdsmi.amdsmi_init()
+            self._smi = amdsmi
+            self._h = amdsmi.amdsmi_get_processor_handles()[0]
+        except Exception:                       # no amdsmi here: no reading
+            self._smi = None
+
+    def __enter__(self):
+        import threading
+        if self._smi is not None:
+            self._th = threading.Thread(target=self._run, daemon=True)
+            self._th.start()
+        return self
+
+    def _run(self):
+        while not self._stop.is_set():
+            t = time.perf_counter()
+            try:
+                m = self._smi.amdsmi_get_gpu_metrics_info(self._h)
+                self.samples.append((t, m.get("current_gfxclk"), m.get("current_socket_power")))
+            except Exception:
+                pass
+            time.sleep(0.002)
+
+    def __exit__(self, *exc):
+        self._stop.set()
+        if self._th is not None:
+            self._th.join()
+        return False
+
+    def between(self, t0, t1):
+        inside = [s for s in self.samples if t0 <= s[0] <= t1]
+        if not inside:   # the region was shorter than one sampling period: the nearest one
+            inside = sorted(self.samples, key=lambda s: abs(s[0] - (t0 + t1) / 2))[:1]
+        clk = [float(s[1]) for s in inside if isinstance(s[1], (int, float))]
+        pw = [float(s[2]) for s in inside if isinstance(s[2], (int, float))]
+        return {"gfx_mhz": float(np.median(clk)) if clk else None,
+                "socket_w": float(np.median(pw)) if pw else None, "readings": len(inside),
+                "source": "amdsmi current_gfxclk, current_socket_power"}
+
+
+def _mean_us(torch, launch, n_launch, warmup=10, warm_ms=50.0, reps=3):
     """Mean GPU duration of one launch at steady state: n_launch launches captured in a
-    HIP graph; the graph is replayed until warm_ms of GPU time have passed (after the
-    idle gaps of an eager latency loop the clocks need that long to come back up), then
+    HIP graph; the graph is replayed until warm_ms of GPU time have passed (after an
+    idle gap an all-VALU kernel needs ~30 ms of load before its clock settles), then
     the median of `reps` timed replays between two events (no host overhead inside)."""
     for i in range(warmup):
         launch(i)
@@ -403,63 +572,35 @@ def _cpu_model():
     return "unknown"
 
 
-def power_probe(torch, sbw, dev, seconds=2.5):
-    """The clock and power the sustained self-salt pass runs at: amd-smi samples
-    (read-only) taken while 200-launch graph replays of the c4 pass run back to back."""
-    import subprocess
-    import threading
-    c4, key = workloads.C4, workloads.PAPER_KEY
+def launch_only(torch, sbw, dev, k):
+    """Each measured kernel launched k times, eagerly, on the synthetic inputs of its
+    configuration, for a profiler (counters are taken per dispatch)."""
+    key = workloads.PAPER_KEY
+    c4, c5 = workloads.C4, workloads.C5
     x, prev = workloads.watermark_inputs("c4")
-    bufs = [torch.from_numpy(x).to(dev) for _ in range(6)]
-    p = torch.from_numpy(prev).to(dev)
-
-    def fn(i):
-        sbw.watermark(bufs[i % 6], p, key, c4["gamma"], c4["delta"], "self_salt")
-    for i in range(5):
-        fn(i)
+    t, p = torch.from_numpy(x).to(dev), torch.from_numpy(prev).to(dev)
+    rng = workloads.rng_for("c5", salt=3)
+    tok = {s: torch.from_numpy(workloads.uniform_tokens(c5["N"], c5["L"], c5["V"], rng)).to(dev)
+           for s in ("self_salt", "context")}
+    x2, prev2 = workloads.watermark_inputs("c2")
+    t2 = torch.from_numpy(x2.view(np.int16)).to(dev).view(torch.bfloat16)
+    p2 = torch.from_numpy(prev2).to(dev)
+    x3, prev3 = workloads.watermark_inputs("c3")
+    t3, p3 = torch.from_numpy(x3).to(dev), torch.from_numpy(prev3).to(dev)
+    seeds = torch.arange(1, c4["B"] + 1, dtype=torch.int64, device=dev)
+    for _ in range(k):
+        for s in ("self_salt", "context"):
+            sbw.watermark(t, p, key, c4["gamma"], c4["delta"], s)
+            sbw.detect(tok[s], key, c5["gamma"], s)
+            sbw.watermark_argmax(t, p, key, c4["gamma"], c4["delta"], s)
+            sbw.watermark_sample(t, p, key, c4["gamma"], c4["delta"], seeds, s, 1.0)
+        sbw.watermark(t2, p2, key, 0.5, 2.0, "context")
+        sbw.watermark(t3, p3, key, workloads.C3["gamma"], workloads.C3["delta"], "self_salt")
     torch.cuda.synchronize()
-    g = torch.cuda.CUDAGraph()
-    with torch.cuda.graph(g):
-        for i in range(200):
-            fn(i)
-    samples, stop = [], threading.Event()
-
-    def sampler():
-        while not stop.is_set():
-            t = time.time()
-            r = subprocess.run(["amd-smi", "metric", "-g", "0", "--clock", "--power", "--json"],
-                               capture_output=True, text=True)
-            try:
-                d = json.loads(r.stdout)
-                d = d["gpu_data"][0] if "gpu_data" in d else (d[0] if isinstance(d, list) else d)
-                samples.append((t, float(d["clock"]["gfx_0"]["clk"]["value"]),
-                                float(d["power"]["socket_power"]["value"])))
-            except (ValueError, KeyError, IndexError, TypeError):
-                pass
-            time.sleep(0.05)
-    th = threading.Thread(target=sampler)
-    th.start()
-    time.sleep(1.0)
-    t0, per_launch = time.time(), []
-    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    while time.time() - t0 < seconds:
-        a.record()
-        g.replay()
-        b.record()
-        torch.cuda.synchronize()
-        per_launch.append(a.elapsed_time(b) / 200 * 1e3)
-    t1 = time.time()
-    stop.set()
-    th.join()
-    idle = [s for s in samples if s[0] < t0]
-    busy = [s for s in samples if t0 + 0.5 <= s[0] < t1]     # past the first clock step
-    med = lambda xs: float(np.median(xs)) if xs else None
-    return {"probe": "self-salt c4 watermark, 200-launch graph replays back to back",
-            "seconds": round(t1 - t0, 2), "replays": len(per_launch),
-            "us_per_launch_first_replay": per_launch[0], "us_per_launch_median": med(per_launch),
-            "gfx_mhz_idle_median": med([s[1] for s in idle]),
-            "gfx_mhz_busy_median": med([s[1] for s in busy]),
-            "socket_w_busy_median": med([s[2] for s in busy]), "samples_busy": len(busy)}
+    # the roof probe's kernels, once each (warm_ms=0: no warm-up launches)
+    philox_roof(torch, warm_ms=0.0, reps=1)
+    torch.cuda.synchronize()
+    print(json.dumps({"launch_only": k}))
 
 
 def main():
@@ -468,19 +609,15 @@ def main():
         print(json.dumps({"error": "this build runs on one GPU; --gpus must be 1",
                           "n_gpus": args.gpus}))
         sys.exit(2)
-    if args.power_probe:
-        import torch
-        import paper_2609_03844_amd as sbw
-        dev = torch.device("cuda:0")
-        torch.cuda.set_device(dev)
-        print(json.dumps(power_probe(torch, sbw, dev)))
-        return
 
     import torch
     import paper_2609_03844_amd as sbw
 
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    if args.launch_only:
+        launch_only(torch, sbw, dev, args.launch_only)
+        return
     c4, c5 = workloads.C4, workloads.C5
     key = workloads.PAPER_KEY
     B, V = c4["B"], c4["V"]
@@ -492,7 +629,7 @@ def main():
     prev_d = torch.from_numpy(prev).to(dev)
     toks = {}
     for seeding in ("self_salt", "context"):
-        member = gpu_membership(sbw, torch, dev, key, c5["gamma"], seeding)
+        member = oracle_membership(key, c5["gamma"], seeding)
         toks[seeding] = workloads.detect_inputs(c5["N"], c5["L"], c5["V"], c5["gamma"],
                                                 c5["delta"], seeding, member)
     tok_d = {s: torch.from_numpy(t).to(dev) for s, t in toks.items()}
@@ -526,22 +663,37 @@ def main():
             for i in range(args.steps):
                 launch(name, seeding, i)
         graphs.append(g)
-    for g in graphs:        # one untimed replay each
-        g.replay()
-    torch.cuda.synchronize()
+
+    # Warm-up by GPU time, not by step count: the four graphs replayed in the timed
+    # order until --warm-ms have passed, so the timed region starts at steady state.
+    w0, w1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    warm_ms, warm_cycles = 0.0, 0
+    while warm_ms < args.warm_ms:
+        w0.record()
+        for g in graphs:
+            g.replay()
+        w1.record()
+        torch.cuda.synchronize()
+        warm_ms += w0.elapsed_time(w1)
+        warm_cycles += 1
 
     # Timed region: exactly `steps` steps, their launches grouped by kernel (one graph
     # replay per kernel), with a HIP event on the launching stream at each group
-    # boundary: a kernel's mean launch duration is its group time / steps.
+    # boundary: a kernel's mean launch duration is its group time / steps.  A host
+    # thread reads the GFX clock meanwhile.
     marks = [torch.cuda.Event(enable_timing=True) for _ in range(len(launches) + 1)]
-    torch.cuda.synchronize()
-    wall0 = time.perf_counter()
-    marks[0].record()
-    for k, g in enumerate(graphs):
-        g.replay()
-        marks[k + 1].record()
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - wall0
+    with ClockSampler() as clock:
+        time.sleep(0.005)
+        torch.cuda.synchronize()
+        wall0 = time.perf_counter()
+        marks[0].record()
+        for k, g in enumerate(graphs):
+            g.replay()
+            marks[k + 1].record()
+        torch.cuda.synchronize()
+        wall1 = time.perf_counter()
+    wall = wall1 - wall0
+    clock_timed = clock.between(wall0, wall1)
     total_ms = marks[0].elapsed_time(marks[-1])
     mean_ms = {name: marks[k].elapsed_time(marks[k + 1]) / args.steps
                for k, (name, _) in enumerate(launches)}
@@ -591,6 +743,7 @@ def main():
         hits = [v for k, v in traffic.items() if k.startswith(prefix)]
         return hits[0] if len(hits) == 1 else None
 
+    roof = philox_roof(torch)
     out = {
         "metric": "watermarked logits Gelem/s + achieved HBM GB/s (B=256,V=152064); detect seq/s",
         "value": ss["gelem_per_s"],
@@ -604,28 +757,38 @@ def main():
         "vs_baseline": None,
         "dtype": "f32",
         "data": "synthetic",
-        "config": {"workload": ("c4: watermark B=256 x V=152064 fp32 logits 3*N(0,1)+8*[U<0.05], "
-                                "gamma=0.25, delta=2, full-vocabulary self-salt (value); context "
-                                "seeding at the same shape; detect c5 N=4096 x L=512, V=128256, "
-                                "both seedings"),
+        "config": {"workload": ("c4 watermark B=256 x V=152064 fp32, self-salt (value) and "
+                                "context seeding; c5 detect N=4096 x L=512, both seedings"),
                    "B": B, "V": V, "gamma": c4["gamma"], "delta": c4["delta"],
                    "detect_N": c5["N"], "detect_L": c5["L"], "rotating_buffers": args.buffers,
+                   "warm_ms": round(warm_ms, 1), "warm_cycles": warm_cycles,
                    "parallelism": "single GPU"},
         "hbm_gbps": ss["hbm_gbps"],
         "detect_seq_per_s": det_stats("det_self_salt")["seq_per_s"],
         "watermark": {"self_salt": ss, "context": ctx},
         "detect": {"self_salt": det_stats("det_self_salt"), "context": det_stats("det_context")},
-        "roofline": {"bound": "alu", "kernel": "watermark_ss_rows_kernel<float> (self-salt)",
-                     "achieved": ss_blocks, "peak": PHILOX_PEAK_GBLOCKS,
-                     "unit": "G Philox4x32-10 blocks/s", "frac": ss_blocks / PHILOX_PEAK_GBLOCKS,
-                     "traffic": traffic_of("sbw::watermark_ss_rows_kernel<float,"),
-                     "algorithmic_per_launch": f"{elems} Philox blocks (one per logit), "
-                                               f"{bytes_wm} HBM bytes"},
-        "roofline_context": {"bound": "hbm", "kernel": "watermark_vec_kernel<float, context>",
-                             "achieved": ctx["hbm_gbps"], "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                             "frac": ctx["hbm_frac"],
-                             "traffic": traffic_of("sbw::watermark_vec_kernel<float,"),
-                             "algorithmic_per_launch": f"{bytes_wm} bytes"},
+        "roofline": {
+            "bound": "alu", "kernel": "watermark_ss_rows_kernel<float> (self-salt)",
+            "achieved": ss_blocks, "peak": PHILOX_PEAK_GBLOCKS,
+            "unit": "G Philox4x32-10 blocks/s", "frac": ss_blocks / PHILOX_PEAK_GBLOCKS,
+            "traffic": traffic_of("sbw::watermark_ss_rows_kernel<float,"),
+            "us_per_launch": ss["us_mean"],
+            "algorithmic_per_launch": f"{elems} Philox blocks (one per logit), "
+                                      f"{bytes_wm} HBM bytes",
+            "peak_basis": ("49 issue slots per block (40 products and xors at one per lane "
+                           "per clock, 18 adds at two per slot), 256 CUs x 64 lanes x 2.4 GHz"),
+            "peak_measured": roof["gblocks_per_s"],
+            "frac_measured": ss_blocks / roof["gblocks_per_s"],
+            "clock_mhz": roof["clock_mhz"],
+            "clock_timed_region": clock_timed,
+            "probe": roof,
+            "hbm_context": {"kernel": "watermark_vec_kernel<float> (context seeding)",
+                            "achieved": ctx["hbm_gbps"], "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                            "frac": ctx["hbm_frac"], "us_per_launch": ctx["us_mean"],
+                            "gelem_per_s": ctx["gelem_per_s"],
+                            "traffic": traffic_of("sbw::watermark_vec_kernel<float,"),
+                            "algorithmic_per_launch": f"{bytes_wm} bytes"},
+        },
         "wall_s_timed": wall,
     }
     if not args.no_configs:
@@ -642,7 +805,7 @@ def main():
                 out["configs"][cfg][seeding]["traffic"] = hits[0] if len(hits) == 1 else None
         out["paper_table"] = paper_table(torch, sbw, dev)
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(x, prev, toks["self_salt"], args.cpu_seconds)
+        out["cpu_baseline"] = cpu_baseline(x, prev, toks, args.cpu_runs)
     print(json.dumps(out))
 
 

@@ -1,4 +1,5 @@
-"""Builds libsbw.so in-tree with hipcc for gfx950."""
+"""Builds libsbw.so in-tree with hipcc for gfx950, and libsbw_rate.so, the Philox
+throughput probe that only the benchmark loads (not part of the ABI)."""
 from __future__ import annotations
 
 import os
@@ -10,6 +11,8 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIBRARY = os.path.join(PKG, "libsbw.so")
 SOURCES = [os.path.join(CSRC, "sbw_kernels.hip")]
+RATE_LIBRARY = os.path.join(PKG, "libsbw_rate.so")
+RATE_SOURCES = [os.path.join(CSRC, "philox_rate.hip")]
 HEADERS = [os.path.join(CSRC, "sbw_device.hpp"), os.path.join(INCLUDE, "sbw.h")]
 
 HIPCC_FLAGS = [
@@ -37,13 +40,20 @@ def hipcc() -> str:
     return "hipcc"
 
 
-def build(extra_flags: list[str] | None = None, output: str = LIBRARY) -> str:
+def build(extra_flags: list[str] | None = None, output: str = LIBRARY,
+          sources: list[str] | None = None) -> str:
     cmd = [hipcc(), *HIPCC_FLAGS, *(extra_flags or []), "-I", INCLUDE, "-I", CSRC,
-           *SOURCES, "-o", output + ".tmp"]
+           *(sources or SOURCES), "-o", output + ".tmp"]
     subprocess.run(cmd, check=True)
     os.replace(output + ".tmp", output)
     return output
 
 
+def build_rate() -> str:
+    """The benchmark's Philox throughput probe, in a library of its own."""
+    return build(output=RATE_LIBRARY, sources=RATE_SOURCES)
+
+
 if __name__ == "__main__":
     print(build())
+    print(build_rate())

@@ -21,10 +21,40 @@ def test_more_than_one_gpu_exits_with_a_message():
 
 
 def test_philox_roof_from_unit_counts():
-    # 256 CUs x 64 lanes x 2.4 GHz full-rate lane-ops over 58 lane-ops per block
-    assert abs(bench.PHILOX_PEAK_GBLOCKS - 256 * 64 * 2.4 / 58) < 1e-9
-    assert 670 < bench.PHILOX_PEAK_GBLOCKS < 690
+    # 256 CUs x 64 lanes x 2.4 GHz issue slots over 49 slots per block: 40 products and
+    # xors at one slot each, 18 key adds at two per slot
+    assert bench.PHILOX_ISSUE_SLOTS == 49
+    assert abs(bench.PHILOX_PEAK_GBLOCKS - 256 * 64 * 2.4 / 49) < 1e-9
+    assert 800 < bench.PHILOX_PEAK_GBLOCKS < 805
     assert bench.HBM_PEAK_GBPS == 8000.0
+
+
+def test_rate_probe_source_counts_match_the_roof():
+    # the probe's block is the 58-op block the roof counts: 10 rounds, counter (c,0,0,0)
+    src = open(os.path.join(ROOT, "paper_2609_03844_amd", "csrc", "philox_rate.hip")).read()
+    assert "for (int r = 0; r < 10; ++r)" in src
+    assert "kChains = 8" in src
+    assert os.path.basename(bench.RATE_LIBRARY) == "libsbw_rate.so"
+
+
+def test_cpu_baseline_fields(monkeypatch):
+    # the CPU leg on a tiny batch: every field the benchmark line reports is there
+    import numpy as np
+    import workloads
+    monkeypatch.setattr(workloads, "C4", dict(workloads.C4))
+    x = np.random.default_rng(0).standard_normal((4, 64)).astype(np.float32)
+    prev = np.arange(4, dtype=np.int32)
+    toks = {s: np.random.default_rng(1).integers(0, 64, (8, 16)).astype(np.int32)
+            for s in ("self_salt", "context")}
+    monkeypatch.setattr(bench, "_threads", lambda: 2)
+    out = bench.cpu_baseline(x, prev, toks, runs=1)
+    for k in ("value", "value_1thread", "unit", "cores", "kind", "sample", "cpu", "nproc",
+              "detect_seq_per_s", "runs"):
+        assert k in out, k
+    assert out["kind"] == "oracle" and out["cores"] == 2
+    for s in ("self_salt", "context"):
+        assert out["watermark"][s]["gelem_per_s"] > 0
+        assert out["detect"][s]["seq_per_s"] > 0 and out["detect"][s]["seq_per_s_1thread"] > 0
 
 
 def test_traffic_lookup_refuses_counters_of_other_sources(tmp_path):
