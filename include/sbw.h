@@ -11,7 +11,9 @@
  *              Eq. 2; full-vocabulary self-salt, Sec. 5.2).  In place, one read and
  *              one write per logit.
  *   watermark_argmax     greedy decoding fused with the watermark: the index of
- *              the largest watermarked logit per row, the logits read once.
+ *              the largest watermarked logit per row, the logits read once;
+ *              watermark_argmax_noalloc the same for callers that cannot allocate
+ *              (its scratch in a static device array).
  *   watermark_sample     sampling fused with the watermark (Gumbel-max).
  *   watermark_candidates the watermark on caller-given candidate ids only (the
  *              top-k self-salt scheme of Sec. 4).
@@ -46,7 +48,8 @@
  *     (App. E, memory).
  *   - Work is enqueued on `stream` (a hipStream_t; NULL = the null stream) and the
  *     call returns without synchronising the host.  Functions hold no global
- *     mutable state and are reentrant.
+ *     mutable state and are reentrant, except sbw_watermark_argmax_noalloc, whose
+ *     scratch array is shared by all of its calls on a device.
  *   - All arguments are checked on the host before any HIP call, so an error
  *     return means nothing was enqueued.  Token values are not checked (that
  *     would need a device read): every definition holds for any 32-bit pattern.
@@ -295,6 +298,36 @@ sbw_status_t sbw_watermark_sample(const void *logits, sbw_dtype_t dtype, int64_t
 /* Workspace size, in uint64 elements, that sbw_watermark_argmax needs for B rows of
  * V logits: B * ceil(V / 2048) (0 when B or V is not positive). */
 int64_t sbw_watermark_argmax_workspace(int64_t B, int64_t V);
+
+/* Capacity, in uint64 elements, of the scratch array of sbw_watermark_argmax_noalloc
+ * (2 MiB per device). */
+#define SBW_NOALLOC_SCRATCH_ELEMS 262144
+
+/*
+ * sbw_watermark_argmax_noalloc -- sbw_watermark_argmax without a workspace argument,
+ * for callers that cannot allocate device memory at all: code being captured into a
+ * HIP graph, tight serving loops, harnesses that forbid hipMalloc.  The per-segment
+ * partials go to a scratch array that the library holds in its own code object
+ * (one copy per device, kept until the process ends); the call itself allocates
+ * nothing, on host or device, and makes no hipMalloc or hipFree.
+ *
+ *   logits, dtype, B, V, row_stride, context, width, key, gamma, delta, seeding,
+ *   tokens, values, stream   as for sbw_watermark_argmax, with the same results.
+ *   Limit: sbw_watermark_argmax_workspace(B, V) <= SBW_NOALLOC_SCRATCH_ELEMS (for
+ *   example B <= 3495 rows of 152064 logits), else SBW_ERR_UNSUPPORTED, before any
+ *   HIP call.
+ *   Sharing: every call on a device uses that device's one array, so calls that
+ *   overlap in time on one device race (keep them on one stream, or ordered); calls on
+ *   different devices do not interact.  Nothing needs to be cleared between calls.
+ *   First call: the first call made on a device looks up the array's address on that
+ *   device (hipGetSymbolAddress); make it outside graph capture.  Later calls can be
+ *   captured.
+ */
+sbw_status_t sbw_watermark_argmax_noalloc(const void *logits, sbw_dtype_t dtype, int64_t B,
+                                          int64_t V, int64_t row_stride, const int32_t *context,
+                                          int64_t width, uint64_t key, double gamma, float delta,
+                                          sbw_seeding_t seeding, int32_t *tokens, float *values,
+                                          void *stream);
 
 /*
  * Vocabulary shards.  A token's colour depends only on the row's seed and on its own

@@ -7,6 +7,7 @@ fallback: if the library is missing this module raises on import.
 
     watermark(logits, prev_tokens, key, gamma, delta, seeding="context")   in place
     watermark_argmax(logits, prev_tokens, key, gamma, delta) -> (tokens [B], values [B])
+    watermark_argmax_noalloc(...)  the same with the library's static scratch array
     watermark_sample(logits, prev_tokens, key, gamma, delta, seeds) -> (tokens [B], scores [B])
     green_mask(prev_tokens, V, key, gamma, seeding="context") -> int32 [B, ceil(V/32)]
     detect(tokens, key, gamma, seeding="context") -> (counts int32 [N], z float64 [N])
@@ -28,7 +29,8 @@ import torch  # loads torch's HIP runtime first, so libsbw binds to the same one
 
 from ._build import LIBRARY, build  # noqa: F401  (build is re-exported)
 
-__all__ = ["watermark", "watermark_argmax", "watermark_sample", "watermark_shard",
+__all__ = ["watermark", "watermark_argmax", "watermark_argmax_noalloc", "watermark_sample",
+           "watermark_shard",
            "watermark_argmax_shard", "watermark_sample_shard", "watermark_candidates",
            "green_mask", "detect", "detect_ex", "SbwError", "version", "library_path",
            "SEED_CONTEXT", "SEED_SELF_SALT"]
@@ -52,8 +54,9 @@ EXPORTED = ("sbw_watermark", "sbw_green_mask", "sbw_detect", "sbw_watermark_wind
             "sbw_green_mask_window", "sbw_detect_window", "sbw_watermark_argmax",
             "sbw_watermark_argmax_workspace", "sbw_watermark_candidates", "sbw_detect_ex",
             "sbw_watermark_sample", "sbw_watermark_shard", "sbw_watermark_argmax_shard",
-            "sbw_watermark_sample_shard",
+            "sbw_watermark_sample_shard", "sbw_watermark_argmax_noalloc",
             "sbw_strerror", "sbw_last_hip_error", "sbw_version")
+NOALLOC_SCRATCH_ELEMS = 262144   # SBW_NOALLOC_SCRATCH_ELEMS
 DETECT_IGNORE_REPEATED = 1
 MAX_UNIQUE_POSITIONS = 4096
 MAX_CANDIDATES = 1024
@@ -110,6 +113,9 @@ def _load() -> ctypes.CDLL:
     lib.sbw_watermark_candidates.restype = i32
     lib.sbw_watermark_candidates.argtypes = [P, i32, i64, i64, i64, P, i64, P, i64, u64, f64, f32,
                                              i32, P]
+    lib.sbw_watermark_argmax_noalloc.restype = i32
+    lib.sbw_watermark_argmax_noalloc.argtypes = [P, i32, i64, i64, i64, P, i64, u64, f64, f32, i32,
+                                                 P, P, P]
     lib.sbw_watermark_argmax_workspace.restype = i64
     lib.sbw_watermark_argmax_workspace.argtypes = [i64, i64]
     lib.sbw_strerror.restype = ctypes.c_char_p
@@ -322,6 +328,47 @@ def watermark_argmax(logits: torch.Tensor, prev_tokens: torch.Tensor, key: int, 
                                                _key(key), float(gamma), float(delta),
                                                _seeding(seeding), tokens.data_ptr(), vptr,
                                                workspace.data_ptr(), _stream(stream)))
+    return tokens, values
+
+
+def watermark_argmax_noalloc(logits: torch.Tensor, prev_tokens: torch.Tensor, key: int,
+                             gamma: float, delta: float, seeding="context",
+                             tokens: torch.Tensor | None = None,
+                             values: torch.Tensor | None = None, with_values: bool = True,
+                             stream=None):
+    """watermark_argmax() without a workspace: the library keeps the partials in a static
+    device array (``sbw_watermark_argmax_noalloc``), so with ``tokens`` (and ``values``)
+    given nothing is allocated.  Calls on one device share that array: keep them ordered.
+    Returns (tokens int32 [B], values float32 [B] or None)."""
+    if logits.dim() != 2:
+        raise ValueError("logits must be [B, V]")
+    if logits.dtype == torch.float32:
+        dtype = F32
+    elif logits.dtype == torch.bfloat16:
+        dtype = BF16
+    else:
+        raise TypeError("logits must be float32 or bfloat16")
+    B, V = logits.shape
+    if B > 0 and V > 0 and logits.stride(1) != 1:
+        raise ValueError("logits must have unit stride along the vocabulary")
+    context, width = _window(prev_tokens, B)
+    dev = logits.device
+    if tokens is None:
+        tokens = torch.empty(B, dtype=torch.int32, device=dev)
+    if values is None and with_values:
+        values = torch.empty(B, dtype=torch.float32, device=dev)
+    if tokens.shape != (B,) or tokens.dtype != torch.int32 or not tokens.is_contiguous():
+        raise ValueError("tokens must be contiguous int32 [B]")
+    if values is not None and (values.shape != (B,) or values.dtype != torch.float32
+                               or not values.is_contiguous()):
+        raise ValueError("values must be contiguous float32 [B]")
+    row_stride = logits.stride(0) if B > 1 else max(V, logits.stride(0))
+    _on_device(logits=logits, prev_tokens=context, tokens=tokens, values=values)
+    _check(_lib.sbw_watermark_argmax_noalloc(logits.data_ptr(), dtype, B, V, row_stride,
+                                             context.data_ptr(), width, _key(key), float(gamma),
+                                             float(delta), _seeding(seeding), tokens.data_ptr(),
+                                             values.data_ptr() if values is not None else None,
+                                             _stream(stream)))
     return tokens, values
 
 

@@ -27,6 +27,7 @@
 #include <math.h>
 #include <stdint.h>
 
+#include <atomic>
 #include <type_traits>
 
 #include "sbw.h"
@@ -1615,13 +1616,64 @@ bool vector_path_ok(const void* logits, int64_t row_stride, sbw_dtype_t dtype, u
          (static_cast<uint64_t>(row_stride) * esize) % 16 == 0 && vbase % (16u / esize) == 0;
 }
 
+// ---------------------------------------------------------------------------
+// Scratch of sbw_watermark_argmax_noalloc: the per-segment partials that the other
+// decoding calls keep in the caller's workspace, in an array of the code object, one
+// copy per device, shared by every call on that device.  In host code the name is
+// only a handle: the array's device address comes from hipGetSymbolAddress, resolved
+// once per device with that device current, and only that address reaches a kernel.
+// ---------------------------------------------------------------------------
+constexpr int64_t kScratchElems = int64_t{1} << 18;  // uint64 partials: 2 MiB
+static_assert(kScratchElems == SBW_NOALLOC_SCRATCH_ELEMS, "the header states the limit");
+constexpr int kMaxDevices = 64;
+std::atomic<uint64_t*> g_scratch_of_device[kMaxDevices];
+
+}  // namespace
+}  // namespace sbw
+
+static __device__ __align__(256) uint64_t scratch[sbw::kScratchElems];
+
+namespace sbw {
+namespace {
+
+// The device address of `scratch` on the current device (resolved on the first call
+// made on that device).
+sbw_status_t scratch_address(uint64_t** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) {
+    g_last_hip_error = e;
+    (void)hipGetLastError();
+    return SBW_ERR_NO_DEVICE;
+  }
+  if (dev < 0 || dev >= kMaxDevices) return SBW_ERR_UNSUPPORTED;
+  uint64_t* p = g_scratch_of_device[dev].load(std::memory_order_acquire);
+  if (p == nullptr) {
+    void* addr = nullptr;
+    e = hipGetSymbolAddress(&addr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || addr == nullptr) {
+      g_last_hip_error = e != hipSuccess ? e : hipErrorInvalidSymbol;
+      (void)hipGetLastError();
+      return SBW_ERR_HIP;
+    }
+    p = static_cast<uint64_t*>(addr);
+    // every thread that resolves it gets the same address, so a race only repeats work
+    g_scratch_of_device[dev].store(p, std::memory_order_release);
+  }
+  *out = p;
+  return SBW_OK;
+}
+
 // Greedy decoding and sampling: validation, then the segment pass and the read-out.
+// With use_scratch the partials go to the device's `scratch` array instead of
+// `workspace` (which may then be null).
 template <bool kSample>
 sbw_status_t decode_impl(const void* logits, sbw_dtype_t dtype, int64_t B, int64_t V,
                          int64_t row_stride, const int32_t* context, int64_t width,
                          int64_t v_offset, uint64_t key, double gamma, float delta,
                          sbw_seeding_t seeding, const SampleArgs& sa, int32_t* tokens,
-                         float* values, uint64_t* workspace, void* stream) {
+                         float* values, uint64_t* workspace, void* stream,
+                         bool use_scratch = false) {
   if (B < 0 || V < 0 || row_stride < V || v_offset < 0) return SBW_ERR_INVALID_ARG;
   sbw_status_t s = check_width(width);
   if (s != SBW_OK) return s;
@@ -1632,11 +1684,16 @@ sbw_status_t decode_impl(const void* logits, sbw_dtype_t dtype, int64_t B, int64
   if (!ids_fit(V, v_offset)) return SBW_ERR_UNSUPPORTED;
   if (B == 0) return SBW_OK;
   if (V == 0) return SBW_ERR_INVALID_ARG;  // no token to choose
-  if (logits == nullptr || context == nullptr || tokens == nullptr || workspace == nullptr)
+  if (logits == nullptr || context == nullptr || tokens == nullptr ||
+      (workspace == nullptr && !use_scratch))
     return SBW_ERR_INVALID_ARG;
   if (B > INT64_MAX / 4 / row_stride) return SBW_ERR_UNSUPPORTED;
   s = check_device();
   if (s != SBW_OK) return s;
+  if (use_scratch) {
+    s = scratch_address(&workspace);
+    if (s != SBW_OK) return s;
+  }
 
   // gamma == 0: nothing is green, every logit (and the value returned) is unchanged.
   const uint64_t T = threshold_of(gamma);
@@ -1789,6 +1846,20 @@ sbw_status_t sbw_watermark_sample_shard(const void* logits, sbw_dtype_t dtype, i
   return decode_impl<true>(logits, dtype, B, V, row_stride, context, width, v_offset, key, gamma,
                            delta, seeding, SampleArgs{seeds, inv_temperature}, tokens, scores,
                            workspace, stream);
+}
+
+sbw_status_t sbw_watermark_argmax_noalloc(const void* logits, sbw_dtype_t dtype, int64_t B,
+                                          int64_t V, int64_t row_stride, const int32_t* context,
+                                          int64_t width, uint64_t key, double gamma, float delta,
+                                          sbw_seeding_t seeding, int32_t* tokens, float* values,
+                                          void* stream) {
+  // The partials must fit the static array: B * ceil(V / kArgmaxSegElems) elements,
+  // compared by division so that no product overflows.
+  if (B > 0 && V > 0 && B > kScratchElems / ((V + kArgmaxSegElems - 1) / kArgmaxSegElems))
+    return SBW_ERR_UNSUPPORTED;
+  return decode_impl<false>(logits, dtype, B, V, row_stride, context, width, 0, key, gamma, delta,
+                            seeding, SampleArgs{nullptr, 1.0f}, tokens, values, nullptr, stream,
+                            /*use_scratch=*/true);
 }
 
 int64_t sbw_watermark_argmax_workspace(int64_t B, int64_t V) {

@@ -39,7 +39,8 @@ def test_header_declares_the_boundary():
     assert _declared() == ["sbw_detect", "sbw_detect_ex", "sbw_detect_window", "sbw_green_mask",
                            "sbw_green_mask_window", "sbw_last_hip_error", "sbw_strerror",
                            "sbw_version", "sbw_watermark", "sbw_watermark_argmax",
-                           "sbw_watermark_argmax_shard", "sbw_watermark_argmax_workspace",
+                           "sbw_watermark_argmax_noalloc", "sbw_watermark_argmax_shard",
+                           "sbw_watermark_argmax_workspace",
                            "sbw_watermark_candidates", "sbw_watermark_sample",
                            "sbw_watermark_sample_shard", "sbw_watermark_shard",
                            "sbw_watermark_window"]
@@ -261,6 +262,40 @@ def test_argmax_rejects_bad_arguments(lib):
     assert am(lib, B=0) == OK
     if not _gpu_visible():
         assert am(lib, values=NULL) == NO_DEVICE   # values may be NULL
+
+
+def amn(lib, logits=DUMMY, dtype=0, B=2, V=8, stride=8, context=DUMMY, width=1, gamma=0.25,
+        delta=2.0, seeding=0, tokens=DUMMY, values=DUMMY):
+    return lib.sbw_watermark_argmax_noalloc(logits, dtype, B, V, stride, context, width, KEY,
+                                            gamma, delta, seeding, tokens, values, None)
+
+
+def test_argmax_noalloc_rejects_bad_arguments(lib, sbw):
+    assert sbw.NOALLOC_SCRATCH_ELEMS == 262144
+    assert re.search(r"#define SBW_NOALLOC_SCRATCH_ELEMS 262144\b", open(HEADER).read())
+    assert amn(lib, V=0, stride=0) == INVALID
+    assert amn(lib, B=-1) == INVALID
+    assert amn(lib, stride=7) == INVALID
+    for name in ("logits", "context", "tokens"):
+        assert amn(lib, **{name: NULL}) == INVALID, name
+    assert amn(lib, width=9) == UNSUPPORTED
+    assert amn(lib, dtype=3) == UNSUPPORTED
+    assert amn(lib, seeding=2) == UNSUPPORTED
+    assert amn(lib, gamma=2.0) == GAMMA
+    assert amn(lib, delta=math.nan) == DELTA
+    assert amn(lib, B=0) == OK
+    # the partials must fit the static array: B * ceil(V / 2048) <= 262144
+    V = 152064
+    assert lib.sbw_watermark_argmax_workspace(3495, V) <= 262144 < \
+        lib.sbw_watermark_argmax_workspace(3496, V)
+    assert amn(lib, B=3496, V=V, stride=V) == UNSUPPORTED
+    assert amn(lib, B=262145, V=1, stride=1) == UNSUPPORTED
+    assert amn(lib, B=1 << 40, V=1 << 20, stride=1 << 20) == UNSUPPORTED
+    if not _gpu_visible():
+        # within the limit, validation passes and the device lookup reports its absence
+        assert amn(lib, B=3495, V=V, stride=V) == NO_DEVICE
+        assert amn(lib, B=262144, V=2048, stride=2048) == NO_DEVICE
+        assert amn(lib, values=NULL) == NO_DEVICE
 
 
 def test_argmax_workspace_size(lib):
