@@ -183,6 +183,26 @@ def test_argmax_skip_bound_edges(env, dtype, seeding):
 SMALL_DECODE_GRID = 900
 
 
+def decode_segment(dtype, sample):
+    """Logits per full-width decode segment, read from the kernel source's launch knobs
+    (16-byte vectors per lane x 256 lanes), and the small-grid threshold, so that a
+    retune of either keeps these tests honest about which kernel they run."""
+    import os
+    import re
+    src = open(os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))),
+                            "paper_2609_03844_amd", "csrc", "sbw_kernels.hip")).read()
+
+    def knob(name):
+        return int(re.search(rf"#define {name} (\d+)", src).group(1))
+    threshold = int(re.search(r"kSmallDecodeGrid = (\d+);", src).group(1))
+    assert threshold == SMALL_DECODE_GRID
+    name = {("f32", False): "SBW_DECODE_VECS_F32_GREEDY", ("f32", True): "SBW_DECODE_VECS_F32",
+            ("bf16", False): "SBW_DECODE_VECS_BF16",
+            ("bf16", True): "SBW_DECODE_VECS_BF16_SAMPLE"}[(dtype, sample)]
+    return (4 if dtype == "f32" else 8) * 256 * knob(name)
+
+
+
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("seeding", ["context", "self_salt"])
 def test_argmax_both_launch_shapes(env, dtype, seeding):
@@ -191,11 +211,12 @@ def test_argmax_both_launch_shapes(env, dtype, seeding):
     rng = np.random.default_rng(93)
     V = 40001
     edge = bound_rows(rng, V, dtype)
-    seg = 6144 if dtype == "f32" else 8192       # logits per full-width segment
+    seg = decode_segment(dtype, sample=False)      # logits per full-width segment
     for B in (8, 256):
         x = np.concatenate([edge] * (-(-B // edge.shape[0])))[:B].copy()
         ctx = workloads.context_tokens(B, 1, V, rng)[:, 0].copy()
         big = B * (-(-V // seg)) >= SMALL_DECODE_GRID
+        assert big == (B == 256), (B, seg)         # both launch shapes are exercised
         for gamma, delta in [(0.25, 2.0), (0.5, -1.0)]:
             say(f"argmax launch shapes {dtype} {seeding} B={B} big={big} gamma={gamma}")
             assert_argmax_equal(run_argmax(env, x, ctx, WIDE, gamma, delta, seeding),

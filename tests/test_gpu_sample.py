@@ -10,7 +10,7 @@ import pytest
 
 import oracle
 import workloads
-from test_gpu_argmax import assert_argmax_equal, hard_rows
+from test_gpu_argmax import SMALL_DECODE_GRID, assert_argmax_equal, decode_segment, hard_rows
 from test_gpu_parity import KEY, WIDE, _to_device, env, say  # noqa: F401
 
 pytestmark = pytest.mark.gpu
@@ -208,10 +208,13 @@ def test_sample_both_launch_shapes(env, dtype, seeding):
     rng = np.random.default_rng(470)
     V = 40001
     edge = queue_rows(rng, V, dtype)
+    seg = decode_segment(dtype, sample=True)
     for B in (8, 256):
         x = np.concatenate([edge] * (-(-B // edge.shape[0])))[:B].copy()
         ctx = workloads.context_tokens(B, 1, V, rng)[:, 0].copy()
         seeds = seeds_for(rng, B)
+        big = B * (-(-V // seg)) >= SMALL_DECODE_GRID
+        assert big == (B == 256), (B, seg)         # both launch shapes are exercised
         for gamma, delta, inv_t in [(0.25, 2.0, 1.0), (0.5, -1.0, 0.37)]:
             say(f"sample launch shapes {dtype} {seeding} B={B} gamma={gamma}")
             assert_argmax_equal(run_sample(env, x, ctx, seeds, WIDE, gamma, delta, seeding, inv_t),
