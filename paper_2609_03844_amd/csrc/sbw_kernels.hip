@@ -40,6 +40,9 @@ namespace {
 #ifndef SBW_CONTEXT_UNROLL
 #define SBW_CONTEXT_UNROLL 2   // 16-byte vectors per lane, context seeding (HBM-bound)
 #endif
+#ifndef SBW_CONTEXT_UNROLL_BF16
+#define SBW_CONTEXT_UNROLL_BF16 2
+#endif
 #ifndef SBW_SELF_SALT_UNROLL
 #define SBW_SELF_SALT_UNROLL 2 // 16-byte vectors per lane, self-salt fp32 (Philox-bound)
 #endif
@@ -64,6 +67,20 @@ namespace {
 #endif
 #ifndef SBW_SELF_SALT_PREFETCH_BF16
 #define SBW_SELF_SALT_PREFETCH_BF16 1
+#endif
+// Context seeding: rows per workgroup (the same tile of each, the next row's loads in
+// flight while the current row is drawn and stored), while at least
+// SBW_CONTEXT_MIN_GROUPS workgroups remain.  1 = one row per workgroup.
+#ifndef SBW_CONTEXT_ROW_ITERS
+#define SBW_CONTEXT_ROW_ITERS 1
+#endif
+#ifndef SBW_CONTEXT_MIN_GROUPS
+#define SBW_CONTEXT_MIN_GROUPS 2048
+#endif
+// Self-salt fp32, width 1: one vector per lane when that is what it takes to group 4 rows
+// per workgroup (batches of 64 rows of a 128K vocabulary).  0 = off.
+#ifndef SBW_SELF_SALT_NARROW
+#define SBW_SELF_SALT_NARROW 1
 #endif
 #ifndef SBW_SELF_SALT_MIN_GROUPS
 #define SBW_SELF_SALT_MIN_GROUPS 1024  // 2048 measured 5 % slower for B * V of 5-10 M logits
@@ -247,6 +264,76 @@ watermark_vec_kernel(T* __restrict__ logits, int64_t row_stride, uint32_t V, int
         for (uint32_t e = 0; e < tail; ++e)
           bias_one<T, kContext>(row_ptr, full * kPer + e, rs, tm1, delta, vbase);
       }
+    }
+  }
+}
+
+// The same pass with each workgroup taking the same tile of several rows, y,
+// y + gridDim.y, ..., loading the next row's vectors before it draws and stores the
+// current row's (tiles that end inside the row's last vectors take the plain kernel's
+// per-vector guards and no prefetch).
+template <typename T, int kU, int kW>
+__global__ void __launch_bounds__(kThreads)
+watermark_vec_rows_kernel(T* __restrict__ logits, int64_t row_stride, uint32_t V, int64_t B,
+                          const int32_t* __restrict__ context, int width, uint64_t key,
+                          uint32_t tm1, float delta, uint32_t vbase) {
+  using VecT = typename std::conditional<sizeof(T) == 4, f32x4, u32x4>::type;
+  constexpr uint32_t kPer = 16u / sizeof(T);
+  const uint32_t full = V / kPer;
+  const uint32_t tail = V % kPer;
+  const uint32_t jbase = vbase / kPer;
+  const uint32_t first = blockIdx.x * (kThreads * kU);
+  int64_t row = blockIdx.y;
+  if (row >= B) return;
+  if (first + kThreads * kU <= full) {
+    auto load = [&](VecT (&buf)[kU], int64_t r) {
+      const VecT* vec = reinterpret_cast<const VecT*>(logits + r * row_stride);
+#pragma unroll
+      for (int u = 0; u < kU; ++u) buf[u] = stream_load(vec + first + u * kThreads + threadIdx.x);
+    };
+    auto draw_store = [&](const VecT (&buf)[kU], int64_t r) {
+      VecT* vec = reinterpret_cast<VecT*>(logits + r * row_stride);
+      const RowSeed<kW> rs = row_seed<kContext, kW>(key, context + r * width, width);
+#pragma unroll
+      for (int u = 0; u < kU; ++u) {
+        const uint32_t j = first + u * kThreads + threadIdx.x;
+        stream_store(vec + j, bias_vec_context(buf[u], j + jbase, rs.seed, tm1, delta));
+      }
+    };
+    VecT a[kU], b[kU];
+    load(a, row);
+    for (;;) {
+      const int64_t r1 = row + gridDim.y;
+      if (r1 < B) load(b, r1);
+      draw_store(a, row);
+      if (r1 >= B) break;
+      const int64_t r2 = r1 + gridDim.y;
+      if (r2 < B) load(a, r2);
+      draw_store(b, r1);
+      if (r2 >= B) break;
+      row = r2;
+    }
+    return;
+  }
+  for (; row < B; row += gridDim.y) {
+    T* row_ptr = logits + row * row_stride;
+    VecT* vec = reinterpret_cast<VecT*>(row_ptr);
+    VecT buf[kU];
+#pragma unroll
+    for (int u = 0; u < kU; ++u) {
+      const uint32_t j = first + u * kThreads + threadIdx.x;
+      if (j < full) buf[u] = stream_load(vec + j);
+    }
+    const RowSeed<kW> rs = row_seed<kContext, kW>(key, context + row * width, width);
+#pragma unroll
+    for (int u = 0; u < kU; ++u) {
+      const uint32_t j = first + u * kThreads + threadIdx.x;
+      if (j < full) stream_store(vec + j, bias_vec_context(buf[u], j + jbase, rs.seed, tm1, delta));
+    }
+    if (tail != 0u && threadIdx.x == 0 && full >= first &&
+        full - first < static_cast<uint32_t>(kThreads * kU)) {
+      for (uint32_t e = 0; e < tail; ++e)
+        bias_one<T, kContext>(row_ptr, full * kPer + e, rs, tm1, delta, vbase);
     }
   }
 }
@@ -1062,12 +1149,22 @@ green_mask_kernel(uint32_t* __restrict__ bits, uint32_t V, uint32_t words_per_ro
 constexpr int kWave = 64;
 constexpr int kWavesPerBlock = kThreads / kWave;
 
-// Self-salt membership of token v after token p, from J(p) and J(v).
-__device__ __forceinline__ bool green_from_hashes(uint64_t key, uint32_t jp, uint32_t jv, uint32_t v,
-                                                  uint32_t tm1) {
-  const uint64_t self = mul_64x64(key, wide_mul(jv, jv));
-  const uint64_t t = mul_64x32(key * static_cast<uint64_t>(jp), jv);
-  return is_green(cbrng(v, t < self ? t : self), tm1);
+// Lane `l`'s 64-bit value, in every lane.
+__device__ __forceinline__ uint64_t readlane64(uint64_t x, int l) {
+  const uint32_t lo = __builtin_amdgcn_readlane(static_cast<uint32_t>(x), l);
+  const uint32_t hi = __builtin_amdgcn_readlane(static_cast<uint32_t>(x >> 32), l);
+  return (static_cast<uint64_t>(hi) << 32) | lo;
+}
+
+// Lane t gets lane t - 1's x (wave_shr:1); lane 0 gets `first`.
+__device__ __forceinline__ uint64_t wave_shift_right(uint64_t x, uint64_t first) {
+  const uint32_t lo = static_cast<uint32_t>(__builtin_amdgcn_update_dpp(
+      static_cast<int>(static_cast<uint32_t>(first)), static_cast<int>(static_cast<uint32_t>(x)),
+      0x138, 0xF, 0xF, false));
+  const uint32_t hi = static_cast<uint32_t>(__builtin_amdgcn_update_dpp(
+      static_cast<int>(static_cast<uint32_t>(first >> 32)),
+      static_cast<int>(static_cast<uint32_t>(x >> 32)), 0x138, 0xF, 0xF, false));
+  return (static_cast<uint64_t>(hi) << 32) | lo;
 }
 
 // Membership of token v at a position whose window is w[0..width-1].
@@ -1123,65 +1220,71 @@ __device__ __forceinline__ void detect_store(const DetectIO& io, int64_t n, uint
   io.z[n] = numerator / denominator;
 }
 
+// Positions are 32-bit (L < 2^31).  Lanes past the end of the sequence load the last
+// token instead (a valid address), so the loads need no branch; their positions are
+// masked out of the count.
 template <int kSeeding, int kChunk, int kW>
 __global__ void __launch_bounds__(kThreads)
 detect_kernel(const int32_t* __restrict__ tokens, int64_t N, int64_t L, int64_t row_stride,
               int width, uint64_t key, uint32_t tm1, double gamma, DetectIO io) {
   const int lane = threadIdx.x % kWave;
-  const int64_t wave0 = static_cast<int64_t>(blockIdx.x) * kWavesPerBlock + threadIdx.x / kWave;
+  // the wave's sequence index, in scalar registers
+  const int64_t wave0 = static_cast<int64_t>(blockIdx.x) * kWavesPerBlock +
+                        __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x / kWave));
   for (int64_t n = wave0; n < N; n += static_cast<int64_t>(gridDim.x) * kWavesPerBlock) {
     const int32_t* seq = tokens + n * row_stride;
-    const int64_t len = sequence_length(io.lengths, n, L);
+    const uint32_t len = static_cast<uint32_t>(sequence_length(io.lengths, n, L));
     uint32_t green = 0u;  // wave-uniform count
-    for (int64_t base = width; base < len; base += kWave * kChunk) {
+    for (uint32_t base = static_cast<uint32_t>(width); base < len; base += kWave * kChunk) {
       uint32_t w[kChunk][kW], v[kChunk];
+      bool in[kChunk];
 #pragma unroll
       for (int c = 0; c < kChunk; ++c) {
-        const int64_t i = base + c * kWave + lane;
-        v[c] = 0u;
+        const uint32_t i = base + static_cast<uint32_t>(c * kWave + lane);
+        in[c] = i < len;
+        const uint32_t ic = in[c] ? i : len - 1u;   // >= width: base < len
+        v[c] = static_cast<uint32_t>(seq[ic]);
+        constexpr bool kShared = kSeeding == kSelfSalt && kW == 1;   // terms handed over
 #pragma unroll
-        for (int k = 0; k < kW; ++k) w[c][k] = 0u;
-        if (i < len) {
-          v[c] = static_cast<uint32_t>(seq[i]);
-          constexpr bool kShared = kSeeding == kSelfSalt && kW == 1;   // hashes handed over
-#pragma unroll
-          for (int k = 0; k < kW; ++k)
-            if ((kW == 1 || k < width) && (!kShared || c == 0))
-              w[c][k] = static_cast<uint32_t>(seq[i - width + k]);
-        }
+        for (int k = 0; k < kW; ++k)
+          w[c][k] = ((kW == 1 || k < width) && (!kShared || c == 0))
+                        ? static_cast<uint32_t>(seq[ic - static_cast<uint32_t>(width - k)])
+                        : 0u;
       }
       // Independent membership chains first (instruction-level parallelism), then
       // one ballot per chunk.
       bool g[kChunk];
       if constexpr (kSeeding == kSelfSalt && kW == 1) {
-        // Self-salt, width 1: the hash of position i's previous token is the hash of
-        // position i - 1's token, held by the lane before (lane 63 of the chunk before,
-        // for lane 0; the window token itself for the pass's first position).  A wave
-        // shift hands it over instead of hashing every token twice.
+        // Self-salt, width 1: the seed of position i is min(K J(p) J(v), K J(v) J(v))
+        // with p the token at i - 1.  Each lane computes K J(v) of its own token once;
+        // position i's K J(p) is position i - 1's K J(v), held by the lane before (lane
+        // 63 of the chunk before, for lane 0; from the window token itself for the
+        // pass's first position), and a wave shift hands it over.
         uint32_t jv[kChunk];
-#pragma unroll
-        for (int c = 0; c < kChunk; ++c) jv[c] = jenkins32(v[c]);
-        uint32_t carry = jenkins32(w[0][0]);
+        uint64_t kj[kChunk];
 #pragma unroll
         for (int c = 0; c < kChunk; ++c) {
-          if (c > 0) carry = __builtin_amdgcn_readlane(jv[c - 1], kWave - 1);
-          // wave_shr:1: lane t takes lane t - 1's value, lane 0 keeps `carry`
-          const uint32_t jp = static_cast<uint32_t>(__builtin_amdgcn_update_dpp(
-              static_cast<int>(carry), static_cast<int>(jv[c]), 0x138, 0xF, 0xF, false));
-          const int64_t i = base + c * kWave + lane;
-          g[c] = green_from_hashes(key, jp, jv[c], v[c], tm1) && i < len;
+          jv[c] = jenkins32(v[c]);
+          kj[c] = mul_64x32(key, jv[c]);
+        }
+        uint64_t carry = mul_64x32(key, jenkins32(w[0][0]));
+#pragma unroll
+        for (int c = 0; c < kChunk; ++c) {
+          if (c > 0) carry = readlane64(kj[c - 1], kWave - 1);
+          const uint64_t kjp = wave_shift_right(kj[c], carry);
+          const uint64_t self = mul_64x32(kj[c], jv[c]);
+          const uint64_t t = mul_64x32(kjp, jv[c]);
+          g[c] = is_green(cbrng(v[c], t < self ? t : self), tm1) && in[c];
         }
       } else {
 #pragma unroll
-        for (int c = 0; c < kChunk; ++c) {
-          const int64_t i = base + c * kWave + lane;
-          g[c] = window_green<kSeeding, kW>(key, w[c], width, v[c], tm1) && i < len;
-        }
+        for (int c = 0; c < kChunk; ++c)
+          g[c] = window_green<kSeeding, kW>(key, w[c], width, v[c], tm1) && in[c];
       }
 #pragma unroll
       for (int c = 0; c < kChunk; ++c) green += static_cast<uint32_t>(__popcll(__ballot(g[c])));
     }
-    if (lane == 0) detect_store(io, n, green, len > width ? len - width : 0, gamma);
+    if (lane == 0) detect_store(io, n, green, len > static_cast<uint32_t>(width) ? len - width : 0, gamma);
   }
 }
 
@@ -1329,8 +1432,9 @@ sbw_status_t check_width(int64_t width) {
 // row groups that load their successor while drawing.
 template <int kSeeding, typename T>
 constexpr int unroll_for() {
-  return kSeeding == kContext ? SBW_CONTEXT_UNROLL
-                              : (sizeof(T) == 4 ? SBW_SELF_SALT_UNROLL : SBW_SELF_SALT_UNROLL_BF16);
+  return kSeeding == kContext
+             ? (sizeof(T) == 4 ? SBW_CONTEXT_UNROLL : SBW_CONTEXT_UNROLL_BF16)
+             : (sizeof(T) == 4 ? SBW_SELF_SALT_UNROLL : SBW_SELF_SALT_UNROLL_BF16);
 }
 
 template <typename T, int kSeeding, int kW>
@@ -1347,6 +1451,20 @@ void launch_watermark(void* logits, int64_t B, uint32_t V, int64_t row_stride,
     if constexpr (kSeeding == kSelfSalt) {
       constexpr int kMaxRows = kW > 1 ? 1 : (sizeof(T) == 4 ? 4 : 2);
       const int64_t work = static_cast<int64_t>(tiles) * B;
+      if constexpr (SBW_SELF_SALT_NARROW && kMaxRows == 4 && kU > 1) {
+        // Too few tiles for 4-row groups at kU vectors per lane, enough at one: the
+        // narrower tiles keep the candidate terms shared by 4 rows.
+        const uint32_t tiles1 = static_cast<uint32_t>((vectors + kThreads - 1) / kThreads);
+        if (work < 4 * int64_t{SBW_SELF_SALT_MIN_GROUPS} &&
+            static_cast<int64_t>(tiles1) * B >= 4 * int64_t{SBW_SELF_SALT_MIN_GROUPS}) {
+          const int64_t groups = (B + 3) / 4;
+          const dim3 grid(tiles1, static_cast<uint32_t>(groups < kMaxGridY ? groups : kMaxGridY));
+          hipLaunchKernelGGL((watermark_ss_rows_kernel<T, 1, kW, 4, false>), grid, dim3(kThreads),
+                             0, stream, p, row_stride, V, B, context, width, key, tm1, delta,
+                             vbase);
+          return;
+        }
+      }
       const int rows_per_group = work >= kMaxRows * int64_t{SBW_SELF_SALT_MIN_GROUPS} ? kMaxRows
                                  : (kMaxRows >= 2 && work >= 2 * int64_t{SBW_SELF_SALT_MIN_GROUPS})
                                      ? 2
@@ -1374,9 +1492,22 @@ void launch_watermark(void* logits, int64_t B, uint32_t V, int64_t row_stride,
         hipLaunchKernelGGL((watermark_ss_rows_kernel<T, kU, kW, 1, kPf>), grid, dim3(kThreads), 0,
                            stream, p, row_stride, V, B, context, width, key, tm1, delta, vbase);
     } else {
-      hipLaunchKernelGGL((watermark_vec_kernel<T, kU, kW>), dim3(tiles, rows),
-                         dim3(kThreads), 0, stream, p, row_stride, V, B, context, width, key, tm1,
-                         delta, vbase);
+      // Rows per workgroup: the most, up to SBW_CONTEXT_ROW_ITERS, that still leave
+      // SBW_CONTEXT_MIN_GROUPS workgroups.
+      int64_t per = SBW_CONTEXT_ROW_ITERS;
+      while (per > 1 && static_cast<int64_t>(tiles) * ((B + per - 1) / per) < SBW_CONTEXT_MIN_GROUPS)
+        --per;
+      if (per > 1) {
+        const int64_t slots = (B + per - 1) / per;
+        hipLaunchKernelGGL((watermark_vec_rows_kernel<T, kU, kW>),
+                           dim3(tiles, static_cast<uint32_t>(slots < kMaxGridY ? slots : kMaxGridY)),
+                           dim3(kThreads), 0, stream, p, row_stride, V, B, context, width, key,
+                           tm1, delta, vbase);
+      } else {
+        hipLaunchKernelGGL((watermark_vec_kernel<T, kU, kW>), dim3(tiles, rows),
+                           dim3(kThreads), 0, stream, p, row_stride, V, B, context, width, key,
+                           tm1, delta, vbase);
+      }
     }
   } else {
     const uint32_t tiles = static_cast<uint32_t>((static_cast<uint64_t>(V) + kThreads - 1) / kThreads);
@@ -1516,9 +1647,10 @@ void dispatch_argmax(const void* logits, int64_t B, uint32_t V, int64_t row_stri
 }
 
 template <int kSeeding, int kW>
-void launch_detect(int64_t positions, int64_t blocks, hipStream_t st, const int32_t* tokens,
-                   int64_t N, int64_t L, int64_t row_stride, int width, uint64_t key, uint32_t tm1,
-                   double gamma, const DetectIO& io) {
+void launch_detect(int64_t positions, hipStream_t st, const int32_t* tokens, int64_t N, int64_t L,
+                   int64_t row_stride, int width, uint64_t key, uint32_t tm1, double gamma,
+                   const DetectIO& io) {
+  const int64_t blocks = grid_for((N + kWavesPerBlock - 1) / kWavesPerBlock);
   if (positions <= kWave)
     hipLaunchKernelGGL((detect_kernel<kSeeding, 1, kW>), dim3(blocks), dim3(kThreads), 0, st,
                        tokens, N, L, row_stride, width, key, tm1, gamma, io);
@@ -1586,16 +1718,15 @@ sbw_status_t detect_impl(const int32_t* tokens, int64_t N, int64_t L, int64_t ro
     }
     return after_launch();
   }
-  const int64_t blocks = grid_for((N + kWavesPerBlock - 1) / kWavesPerBlock);
   if (w == 1) {
-    if (ctx) launch_detect<kContext, 1>(positions, blocks, st, tokens, N, L, row_stride, w, key, tm1, gamma, io);
-    else launch_detect<kSelfSalt, 1>(positions, blocks, st, tokens, N, L, row_stride, w, key, tm1, gamma, io);
+    if (ctx) launch_detect<kContext, 1>(positions, st, tokens, N, L, row_stride, w, key, tm1, gamma, io);
+    else launch_detect<kSelfSalt, 1>(positions, st, tokens, N, L, row_stride, w, key, tm1, gamma, io);
   } else if (w <= kMidWidth) {
-    if (ctx) launch_detect<kContext, kMidWidth>(positions, blocks, st, tokens, N, L, row_stride, w, key, tm1, gamma, io);
-    else launch_detect<kSelfSalt, kMidWidth>(positions, blocks, st, tokens, N, L, row_stride, w, key, tm1, gamma, io);
+    if (ctx) launch_detect<kContext, kMidWidth>(positions, st, tokens, N, L, row_stride, w, key, tm1, gamma, io);
+    else launch_detect<kSelfSalt, kMidWidth>(positions, st, tokens, N, L, row_stride, w, key, tm1, gamma, io);
   } else {
-    if (ctx) launch_detect<kContext, kMaxWidth>(positions, blocks, st, tokens, N, L, row_stride, w, key, tm1, gamma, io);
-    else launch_detect<kSelfSalt, kMaxWidth>(positions, blocks, st, tokens, N, L, row_stride, w, key, tm1, gamma, io);
+    if (ctx) launch_detect<kContext, kMaxWidth>(positions, st, tokens, N, L, row_stride, w, key, tm1, gamma, io);
+    else launch_detect<kSelfSalt, kMaxWidth>(positions, st, tokens, N, L, row_stride, w, key, tm1, gamma, io);
   }
   return after_launch();
 }
