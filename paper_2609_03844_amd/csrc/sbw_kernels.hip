@@ -68,15 +68,6 @@ namespace {
 #ifndef SBW_SELF_SALT_PREFETCH_BF16
 #define SBW_SELF_SALT_PREFETCH_BF16 1
 #endif
-// Context seeding: rows per workgroup (the same tile of each, the next row's loads in
-// flight while the current row is drawn and stored), while at least
-// SBW_CONTEXT_MIN_GROUPS workgroups remain.  1 = one row per workgroup.
-#ifndef SBW_CONTEXT_ROW_ITERS
-#define SBW_CONTEXT_ROW_ITERS 1
-#endif
-#ifndef SBW_CONTEXT_MIN_GROUPS
-#define SBW_CONTEXT_MIN_GROUPS 2048
-#endif
 // Self-salt fp32, width 1: one vector per lane when that is what it takes to group 4 rows
 // per workgroup (batches of 64 rows of a 128K vocabulary).  0 = off.
 #ifndef SBW_SELF_SALT_NARROW
@@ -264,76 +255,6 @@ watermark_vec_kernel(T* __restrict__ logits, int64_t row_stride, uint32_t V, int
         for (uint32_t e = 0; e < tail; ++e)
           bias_one<T, kContext>(row_ptr, full * kPer + e, rs, tm1, delta, vbase);
       }
-    }
-  }
-}
-
-// The same pass with each workgroup taking the same tile of several rows, y,
-// y + gridDim.y, ..., loading the next row's vectors before it draws and stores the
-// current row's (tiles that end inside the row's last vectors take the plain kernel's
-// per-vector guards and no prefetch).
-template <typename T, int kU, int kW>
-__global__ void __launch_bounds__(kThreads)
-watermark_vec_rows_kernel(T* __restrict__ logits, int64_t row_stride, uint32_t V, int64_t B,
-                          const int32_t* __restrict__ context, int width, uint64_t key,
-                          uint32_t tm1, float delta, uint32_t vbase) {
-  using VecT = typename std::conditional<sizeof(T) == 4, f32x4, u32x4>::type;
-  constexpr uint32_t kPer = 16u / sizeof(T);
-  const uint32_t full = V / kPer;
-  const uint32_t tail = V % kPer;
-  const uint32_t jbase = vbase / kPer;
-  const uint32_t first = blockIdx.x * (kThreads * kU);
-  int64_t row = blockIdx.y;
-  if (row >= B) return;
-  if (first + kThreads * kU <= full) {
-    auto load = [&](VecT (&buf)[kU], int64_t r) {
-      const VecT* vec = reinterpret_cast<const VecT*>(logits + r * row_stride);
-#pragma unroll
-      for (int u = 0; u < kU; ++u) buf[u] = stream_load(vec + first + u * kThreads + threadIdx.x);
-    };
-    auto draw_store = [&](const VecT (&buf)[kU], int64_t r) {
-      VecT* vec = reinterpret_cast<VecT*>(logits + r * row_stride);
-      const RowSeed<kW> rs = row_seed<kContext, kW>(key, context + r * width, width);
-#pragma unroll
-      for (int u = 0; u < kU; ++u) {
-        const uint32_t j = first + u * kThreads + threadIdx.x;
-        stream_store(vec + j, bias_vec_context(buf[u], j + jbase, rs.seed, tm1, delta));
-      }
-    };
-    VecT a[kU], b[kU];
-    load(a, row);
-    for (;;) {
-      const int64_t r1 = row + gridDim.y;
-      if (r1 < B) load(b, r1);
-      draw_store(a, row);
-      if (r1 >= B) break;
-      const int64_t r2 = r1 + gridDim.y;
-      if (r2 < B) load(a, r2);
-      draw_store(b, r1);
-      if (r2 >= B) break;
-      row = r2;
-    }
-    return;
-  }
-  for (; row < B; row += gridDim.y) {
-    T* row_ptr = logits + row * row_stride;
-    VecT* vec = reinterpret_cast<VecT*>(row_ptr);
-    VecT buf[kU];
-#pragma unroll
-    for (int u = 0; u < kU; ++u) {
-      const uint32_t j = first + u * kThreads + threadIdx.x;
-      if (j < full) buf[u] = stream_load(vec + j);
-    }
-    const RowSeed<kW> rs = row_seed<kContext, kW>(key, context + row * width, width);
-#pragma unroll
-    for (int u = 0; u < kU; ++u) {
-      const uint32_t j = first + u * kThreads + threadIdx.x;
-      if (j < full) stream_store(vec + j, bias_vec_context(buf[u], j + jbase, rs.seed, tm1, delta));
-    }
-    if (tail != 0u && threadIdx.x == 0 && full >= first &&
-        full - first < static_cast<uint32_t>(kThreads * kU)) {
-      for (uint32_t e = 0; e < tail; ++e)
-        bias_one<T, kContext>(row_ptr, full * kPer + e, rs, tm1, delta, vbase);
     }
   }
 }
@@ -1492,22 +1413,9 @@ void launch_watermark(void* logits, int64_t B, uint32_t V, int64_t row_stride,
         hipLaunchKernelGGL((watermark_ss_rows_kernel<T, kU, kW, 1, kPf>), grid, dim3(kThreads), 0,
                            stream, p, row_stride, V, B, context, width, key, tm1, delta, vbase);
     } else {
-      // Rows per workgroup: the most, up to SBW_CONTEXT_ROW_ITERS, that still leave
-      // SBW_CONTEXT_MIN_GROUPS workgroups.
-      int64_t per = SBW_CONTEXT_ROW_ITERS;
-      while (per > 1 && static_cast<int64_t>(tiles) * ((B + per - 1) / per) < SBW_CONTEXT_MIN_GROUPS)
-        --per;
-      if (per > 1) {
-        const int64_t slots = (B + per - 1) / per;
-        hipLaunchKernelGGL((watermark_vec_rows_kernel<T, kU, kW>),
-                           dim3(tiles, static_cast<uint32_t>(slots < kMaxGridY ? slots : kMaxGridY)),
-                           dim3(kThreads), 0, stream, p, row_stride, V, B, context, width, key,
-                           tm1, delta, vbase);
-      } else {
-        hipLaunchKernelGGL((watermark_vec_kernel<T, kU, kW>), dim3(tiles, rows),
-                           dim3(kThreads), 0, stream, p, row_stride, V, B, context, width, key,
-                           tm1, delta, vbase);
-      }
+      hipLaunchKernelGGL((watermark_vec_kernel<T, kU, kW>), dim3(tiles, rows),
+                         dim3(kThreads), 0, stream, p, row_stride, V, B, context, width, key, tm1,
+                         delta, vbase);
     }
   } else {
     const uint32_t tiles = static_cast<uint32_t>((static_cast<uint64_t>(V) + kThreads - 1) / kThreads);
