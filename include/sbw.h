@@ -67,17 +67,26 @@
 extern "C" {
 #endif
 
-typedef enum {
+/* In C++ the enumerations have the fixed underlying type int32_t, so that every value a
+ * C caller can pass is a value of the type (the library answers an unknown one with
+ * SBW_ERR_UNSUPPORTED); in C they are plain enumerations of the same size. */
+#ifdef __cplusplus
+#define SBW_ENUM_TYPE : int32_t
+#else
+#define SBW_ENUM_TYPE
+#endif
+
+typedef enum SBW_ENUM_TYPE {
     SBW_SEED_CONTEXT = 0,   /* seed from the previous token only          */
     SBW_SEED_SELF_SALT = 1  /* seed from the previous token and candidate */
 } sbw_seeding_t;
 
-typedef enum {
+typedef enum SBW_ENUM_TYPE {
     SBW_F32 = 0,            /* IEEE binary32 logits                        */
     SBW_BF16 = 1            /* bfloat16 logits (upper half of binary32)    */
 } sbw_dtype_t;
 
-typedef enum {
+typedef enum SBW_ENUM_TYPE {
     SBW_OK = 0,
     SBW_ERR_INVALID_ARG = 1, /* null pointer, negative size, stride too small */
     SBW_ERR_GAMMA = 2,       /* gamma outside the allowed range              */
@@ -183,7 +192,7 @@ sbw_status_t sbw_detect_window(const int32_t *tokens, int64_t N, int64_t L, int6
                                int32_t *green_counts, double *z, void *stream);
 
 /* Flags of sbw_detect_ex. */
-typedef enum {
+typedef enum SBW_ENUM_TYPE {
     SBW_DETECT_IGNORE_REPEATED = 1   /* score each distinct (width+1)-gram once */
 } sbw_detect_flags_t;
 

@@ -6,7 +6,8 @@
  *   capi_check cpu   version string, status texts, and the argument checks that
  *                    return before any HIP call (no GPU needed).
  *   capi_check gpu   watermark (context and self-salt, window of 4, fp32), greedy
- *                    decoding, Gumbel-max sampling and detection on HIP device
+ *                    decoding (with a workspace and without: sbw_watermark_argmax_noalloc),
+ *                    Gumbel-max sampling and detection on HIP device
  *                    buffers, each compared bit for bit with the oracle (z within
  *                    1e-6 relative).
  *
@@ -88,6 +89,30 @@ static int cpu_checks(void)
     CHECK(sbw_watermark_shard(&dummy, SBW_F32, 1, 2, 2, &prev, 1, (int64_t)1 << 32, 1, 0.25, 2.0f, SBW_SEED_CONTEXT, NULL) == SBW_ERR_UNSUPPORTED, "ids past 2^32");
     CHECK(sbw_watermark_argmax_workspace(256, 152064) == 256 * 75, "workspace size");
     CHECK(sbw_watermark_argmax_workspace(0, 5) == 0, "workspace of nothing");
+    /* the other entry points' host checks (unknown enum values included) */
+    int32_t tok = 0, cnt = 0, cand = 0;
+    uint32_t bits = 0;
+    uint64_t ws = 0, seed = 1;
+    double z = 0.0;
+    CHECK(sbw_watermark_window(&dummy, SBW_BF16, 1, 1, 1, &prev, 9, 1, 0.25, 2.0f, SBW_SEED_SELF_SALT, NULL) == SBW_ERR_UNSUPPORTED, "width 9");
+    CHECK(sbw_watermark_window(&dummy, SBW_F32, 1, 1, 1, &prev, 0, 1, 0.25, 2.0f, SBW_SEED_SELF_SALT, NULL) == SBW_ERR_INVALID_ARG, "width 0");
+    CHECK(sbw_green_mask(&bits, 1, 1, &prev, 1, 0.25, (sbw_seeding_t)5, NULL) == SBW_ERR_UNSUPPORTED, "seeding 5");
+    CHECK(sbw_green_mask_window(&bits, -1, 1, &prev, 1, 1, 0.25, SBW_SEED_CONTEXT, NULL) == SBW_ERR_INVALID_ARG, "mask B < 0");
+    CHECK(sbw_detect(&tok, 1, 2, 2, 1, 0.0, SBW_SEED_CONTEXT, &cnt, &z, NULL) == SBW_ERR_GAMMA, "detect gamma 0");
+    CHECK(sbw_detect(&tok, 1, 2, 1, 1, 0.25, SBW_SEED_CONTEXT, &cnt, &z, NULL) == SBW_ERR_INVALID_ARG, "detect stride < L");
+    CHECK(sbw_detect(NULL, 0, 5, 5, 1, 0.25, SBW_SEED_CONTEXT, NULL, NULL, NULL) == SBW_OK, "detect N = 0");
+    CHECK(sbw_detect_window(&tok, 1, (int64_t)1 << 31, (int64_t)1 << 31, 1, 1, 0.25, SBW_SEED_CONTEXT, &cnt, &z, NULL) == SBW_ERR_UNSUPPORTED, "L = 2^31");
+    CHECK(sbw_detect_ex(&tok, 1, 2, 2, NULL, 1, 1, 0.25, SBW_SEED_CONTEXT, 2u, &cnt, NULL, &z, NULL) == SBW_ERR_UNSUPPORTED, "unknown flag");
+    CHECK(sbw_detect_ex(&tok, 1, 5000, 5000, NULL, 1, 1, 0.25, SBW_SEED_CONTEXT, SBW_DETECT_IGNORE_REPEATED, &cnt, NULL, &z, NULL) == SBW_ERR_UNSUPPORTED, "repeat rule beyond 4096");
+    CHECK(sbw_watermark_candidates(&dummy, SBW_F32, 1, 1, 1, &cand, 1025, &prev, 1, 1, 0.25, 2.0f, SBW_SEED_SELF_SALT, NULL) == SBW_ERR_UNSUPPORTED, "k > 1024");
+    CHECK(sbw_watermark_candidates(&dummy, SBW_F32, 1, 1, 1, &cand, -1, &prev, 1, 1, 0.25, 2.0f, SBW_SEED_SELF_SALT, NULL) == SBW_ERR_INVALID_ARG, "k < 0");
+    CHECK(sbw_watermark_argmax(&dummy, SBW_F32, 1, 1, 1, &prev, 1, 1, 0.25, 2.0f, SBW_SEED_CONTEXT, &tok, NULL, NULL, NULL) == SBW_ERR_INVALID_ARG, "argmax without workspace");
+    CHECK(sbw_watermark_argmax(&dummy, SBW_F32, 1, 0, 0, &prev, 1, 1, 0.25, 2.0f, SBW_SEED_CONTEXT, &tok, NULL, &ws, NULL) == SBW_ERR_INVALID_ARG, "argmax V = 0");
+    CHECK(sbw_watermark_sample(&dummy, SBW_F32, 1, 1, 1, &prev, 1, 1, 0.25, 2.0f, SBW_SEED_CONTEXT, &seed, 0.0f, &tok, NULL, &ws, NULL) == SBW_ERR_INVALID_ARG, "1/T = 0");
+    CHECK(sbw_watermark_sample(&dummy, SBW_F32, 1, 1, 1, &prev, 1, 1, 0.25, 2.0f, SBW_SEED_CONTEXT, NULL, 1.0f, &tok, NULL, &ws, NULL) == SBW_ERR_INVALID_ARG, "no seeds");
+    CHECK(sbw_watermark_argmax_noalloc(&dummy, SBW_F32, 3496, 152064, 152064, &prev, 1, 1, 0.25, 2.0f, SBW_SEED_CONTEXT, &tok, NULL, NULL) == SBW_ERR_UNSUPPORTED, "noalloc beyond its array");
+    CHECK(sbw_watermark_argmax_noalloc(&dummy, (sbw_dtype_t)2, 1, 1, 1, &prev, 1, 1, 0.25, 2.0f, SBW_SEED_CONTEXT, &tok, NULL, NULL) == SBW_ERR_UNSUPPORTED, "noalloc dtype 2");
+    CHECK(sbw_watermark_argmax_noalloc(&dummy, SBW_F32, 0, 1, 1, &prev, 1, 1, 0.25, 2.0f, SBW_SEED_CONTEXT, &tok, NULL, NULL) == SBW_OK, "noalloc B = 0");
     printf("capi cpu ok: libsbw %s\n", v);
     return 0;
 }
@@ -142,6 +167,14 @@ static int gpu_checks(void)
         oracle_watermark_argmax_f32_w(x, B, V, V, ctx, W, key, gamma, delta, seeding, etok, evals);
         CHECK(memcmp(gtok, etok, sizeof etok) == 0 && memcmp(gvals, evals, sizeof evals) == 0,
               "argmax, seeding %d", seeding);
+        /* the same through the call that keeps its partials in the library's own array */
+        HIP(hipMemset(d_tokens, 0xFF, B * sizeof(int32_t)));
+        SBW(sbw_watermark_argmax_noalloc(d_x, SBW_F32, B, V, V, d_ctx, W, key, gamma, delta, sd,
+                                         d_tokens, d_vals, NULL));
+        HIP(hipMemcpy(gtok, d_tokens, sizeof gtok, hipMemcpyDeviceToHost));
+        HIP(hipMemcpy(gvals, d_vals, sizeof gvals, hipMemcpyDeviceToHost));
+        CHECK(memcmp(gtok, etok, sizeof etok) == 0 && memcmp(gvals, evals, sizeof evals) == 0,
+              "argmax without a workspace, seeding %d", seeding);
         SBW(sbw_watermark_sample(d_x, SBW_F32, B, V, V, d_ctx, W, key, gamma, delta, sd, d_seeds,
                                  inv_t, d_tokens, d_vals, d_ws, NULL));
         HIP(hipMemcpy(gtok, d_tokens, sizeof gtok, hipMemcpyDeviceToHost));
