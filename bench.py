@@ -86,11 +86,21 @@ def parse():
     ap.add_argument("--no-configs", action="store_true")
     ap.add_argument("--warm-ms", type=float, default=100.0,
                     help="GPU time of graph replays before the timed region")
+    ap.add_argument("--config-warm-ms", type=float, default=50.0,
+                    help="GPU time of graph replays before each other configuration's timing")
     ap.add_argument("--cpu-runs", type=int, default=10,
                     help="timed runs of each CPU-oracle measurement (after 3 warm-up runs)")
     ap.add_argument("--launch-only", type=int, default=0, metavar="K",
                     help="launch every measured kernel K times eagerly and exit (for profilers)")
+    ap.add_argument("--floors", action="store_true",
+                    help="only time the small configurations against their size (detect against "
+                         "L, watermark against rows) and print fixed cost and marginal rate")
     return ap.parse_args()
+
+
+def progress(msg):
+    """A progress line on stderr (stdout carries only the JSON line)."""
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
 def percentile(xs, q):
@@ -251,56 +261,39 @@ def philox_roof(torch, warm_ms=50.0, reps=10):
                       f"median of {reps} launches after {warm_ms:.0f} ms of the same load")}
 
 
-class ClockSampler:
-    """GFX clock readings (amdsmi, read-only) taken from a host thread every ~2 ms
-    while it runs; `between(t0, t1)` keeps the ones inside a wall-clock interval."""
+class GfxClock:
+    """One read-only amdsmi reading of the GFX clock and socket power (None where amdsmi
+    is missing).  A call takes ~0.4 ms; the benchmark makes one while the timed region
+    runs on the GPU, after every launch of it is queued, so nothing polls meanwhile."""
 
     def __init__(self):
-        import threading
-        self.samples, self._stop, self._th = [], threading.Event(), None
         try:
             import amdsmi
             amdsmi.amdsmi_init()
             self._smi = amdsmi
             self._h = amdsmi.amdsmi_get_processor_handles()[0]
-        except Exception:                       # no amdsmi here: no reading
+        except Exception:
             self._smi = None
 
-    def __enter__(self):
-        import threading
-        if self._smi is not None:
-            self._th = threading.Thread(target=self._run, daemon=True)
-            self._th.start()
-        return self
-
-    def _run(self):
-        while not self._stop.is_set():
-            t = time.perf_counter()
-            try:
-                m = self._smi.amdsmi_get_gpu_metrics_info(self._h)
-                self.samples.append((t, m.get("current_gfxclk"), m.get("current_socket_power")))
-            except Exception:
-                pass
-            time.sleep(0.002)
-
-    def __exit__(self, *exc):
-        self._stop.set()
-        if self._th is not None:
-            self._th.join()
-        return False
-
-    def between(self, t0, t1):
-        inside = [s for s in self.samples if t0 <= s[0] <= t1]
-        if not inside:   # the region was shorter than one sampling period: the nearest one
-            inside = sorted(self.samples, key=lambda s: abs(s[0] - (t0 + t1) / 2))[:1]
-        clk = [float(s[1]) for s in inside if isinstance(s[1], (int, float))]
-        pw = [float(s[2]) for s in inside if isinstance(s[2], (int, float))]
-        return {"gfx_mhz": float(np.median(clk)) if clk else None,
-                "socket_w": float(np.median(pw)) if pw else None, "readings": len(inside),
-                "source": "amdsmi current_gfxclk, current_socket_power"}
+    def read(self):
+        if self._smi is None:
+            return {"gfx_mhz": None, "socket_w": None}
+        try:
+            m = self._smi.amdsmi_get_gpu_metrics_info(self._h)
+            clk = m.get("current_gfxclks") or [m.get("current_gfxclk")]
+            clk = [float(c) for c in clk if isinstance(c, (int, float))]
+            pw = m.get("current_socket_power")
+            return {"gfx_mhz": max(clk) if clk else None, "gfx_mhz_per_xcd": clk,
+                    "socket_w": float(pw) if isinstance(pw, (int, float)) else None,
+                    "source": "amdsmi current_gfxclks (max over XCDs), current_socket_power"}
+        except Exception:
+            return {"gfx_mhz": None, "socket_w": None}
 
 
-def _mean_us(torch, launch, n_launch, warmup=10, warm_ms=50.0, reps=3):
+CONFIG_WARM_MS = [50.0]   # set from --config-warm-ms
+
+
+def _mean_us(torch, launch, n_launch, warmup=10, warm_ms=None, reps=3):
     """Mean GPU duration of one launch at steady state: n_launch launches captured in a
     HIP graph; the graph is replayed until warm_ms of GPU time have passed (after an
     idle gap an all-VALU kernel needs ~30 ms of load before its clock settles), then
@@ -322,7 +315,7 @@ def _mean_us(torch, launch, n_launch, warmup=10, warm_ms=50.0, reps=3):
         return a.elapsed_time(b)
 
     spent = 0.0
-    while spent < warm_ms:
+    while spent < (CONFIG_WARM_MS[0] if warm_ms is None else warm_ms):
         spent += replay_ms()
     times = sorted(replay_ms() for _ in range(reps))
     return times[len(times) // 2] / n_launch * 1e3
@@ -356,6 +349,7 @@ def other_configs(torch, sbw, dev, steps, c5_tokens):
                  "detect_8x200_us": det}
     del bufs
 
+    progress("c1 done")
     # c2: B=64 x V=128256 bf16, context, 8 (gamma, delta) pairs
     c = workloads.C2
     x, prev = workloads.watermark_inputs("c2")
@@ -369,6 +363,7 @@ def other_configs(torch, sbw, dev, steps, c5_tokens):
     res["c2"] = sweep
     del bufs
 
+    progress("c2 done")
     # c3: B=64 x V=128256 fp32, self-salt, gamma=0.25, delta=4
     c = workloads.C3
     x, prev = workloads.watermark_inputs("c3")
@@ -379,6 +374,7 @@ def other_configs(torch, sbw, dev, steps, c5_tokens):
                  "philox_gblocks_per_s": c["B"] * c["V"] / us / 1e3}
     del bufs
 
+    progress("c3 done")
     # fused watermark + greedy decoding on the c4 batch (B=256): one read of each logit
     c = workloads.C4
     x, prev = workloads.watermark_inputs("c4")
@@ -397,6 +393,7 @@ def other_configs(torch, sbw, dev, steps, c5_tokens):
     res["c4_watermark_argmax"] = fused
     del bufs
 
+    progress("greedy decoding done")
     # sampling fused with the watermark on the c4 batch: one Gumbel-max draw per row
     c = workloads.C4
     x, prev = workloads.watermark_inputs("c4")
@@ -416,6 +413,7 @@ def other_configs(torch, sbw, dev, steps, c5_tokens):
     res["c4_watermark_sample"] = sampled
     del bufs
 
+    progress("sampling done")
     # one GPU's share of the c4 vocabulary split 8 ways (a tensor-parallel LM head): B=256
     # rows of 19008 columns holding token ids 57024..76031, through the shard entry points
     c = workloads.C4
@@ -448,6 +446,7 @@ def other_configs(torch, sbw, dev, steps, c5_tokens):
     res["c4_tp8_shard"] = shard
     del bufs
 
+    progress("vocabulary shard done")
     # SBW-ss on the c4 batch: the self-salt watermark (width 4) on the top-40 ids only
     c = workloads.C4
     x, _ = workloads.watermark_inputs("c4")
@@ -464,6 +463,7 @@ def other_configs(torch, sbw, dev, steps, c5_tokens):
         del bufs
     res["c4_sbw_ss_top40"] = topk
 
+    progress("candidates done")
     # c5 detection, texts of lengths drawn in [L/2, L], every position or each distinct
     # n-gram once
     c5 = workloads.C5
@@ -482,6 +482,7 @@ def other_configs(torch, sbw, dev, steps, c5_tokens):
             det[f"{seeding}/{rule}"] = {"us": us, "seq_per_s": c5["N"] / us * 1e6}
     res["c5_detect_ex"] = det
 
+    progress("detection variants done")
     # c4 at B=1024 (623 MB per buffer), both seedings
     c = workloads.C4
     x, prev = workloads.watermark_inputs("c4", B=c["B_large"])
@@ -536,6 +537,7 @@ def paper_table(torch, sbw, dev, calls=200, warmup=20):
     rng = np.random.default_rng(workloads.PAPER_SEED)
     out = {}
     for B in PAPER_B:
+        progress(f"paper table B={B}")
         nbuf = max(2, -(-(400 << 20) // (B * V * 4)))
         bufs = [torch.randn(B, V, device=dev) for _ in range(nbuf)]
         ctx = torch.from_numpy(workloads.context_tokens(B, 4, V, rng)).to(dev)
@@ -603,6 +605,58 @@ def launch_only(torch, sbw, dev, k):
     print(json.dumps({"launch_only": k}))
 
 
+def floors(torch, sbw, dev, steps=100):
+    """Where the small configurations' time goes: each time series is fitted by least
+    squares to t = fixed + size / rate, so the fixed part (launch and the first
+    memory round trip) and the marginal rate (what more work costs) can be read apart.
+    The launch floor itself is a watermark of one row of 64 logits."""
+    key, out = workloads.PAPER_KEY, {}
+
+    def fit(xs, ts):
+        A = np.vstack([np.ones(len(xs)), np.asarray(xs, dtype=np.float64)]).T
+        (a, b), *_ = np.linalg.lstsq(A, np.asarray(ts), rcond=None)
+        return {"fixed_us": float(a), "per_unit_us": float(b), "rate_per_s": float(1e6 / b)}
+
+    tiny = torch.zeros((1, 64), device=dev)
+    p1 = torch.zeros(1, dtype=torch.int32, device=dev)
+    out["launch_floor_us"] = _mean_us(torch, lambda i: sbw.watermark(tiny, p1, key, 0.25, 2.0,
+                                                                     "context"), steps)
+    rng = np.random.default_rng(workloads.PAPER_SEED)
+    c5 = workloads.C5
+    for seeding in ("context", "self_salt"):
+        progress(f"floors: detect {seeding}")
+        Ls, ts = (2, 65, 129, 257, 512, 1024), []
+        for L in Ls:
+            tok = torch.from_numpy(workloads.uniform_tokens(c5["N"], L, c5["V"], rng)).to(dev)
+            cnt = torch.empty(c5["N"], dtype=torch.int32, device=dev)
+            z = torch.empty(c5["N"], dtype=torch.float64, device=dev)
+            ts.append(_mean_us(torch, lambda i, t=tok: sbw.detect(t, key, c5["gamma"], seeding,
+                                                                  counts=cnt, z=z), steps))
+        out[f"detect_N4096_{seeding}"] = {"L": list(Ls), "us": ts,
+                                          "fit_per_scored_token": fit([c5["N"] * (L - 1) for L in Ls], ts)}
+    for name, dt, V, seeding, gamma, delta in (("bf16_context_V128256", torch.bfloat16, 128256,
+                                                "context", 0.5, 2.0),
+                                               ("fp32_context_V152064", torch.float32, 152064,
+                                                "context", 0.25, 2.0),
+                                               ("fp32_self_salt_V128256", torch.float32, 128256,
+                                                "self_salt", 0.25, 4.0)):
+        Bs, ts = (16, 32, 64, 128, 256), []
+        for B in Bs:
+            x = torch.randn(B, V, device=dev).to(dt)
+            nb = max(2, -(-(600 << 20) // (x.numel() * x.element_size())))
+            bufs = [x.clone() for _ in range(nb)]
+            p = torch.from_numpy(rng.integers(0, V, B).astype(np.int32)).to(dev)
+            ts.append(_mean_us(torch, lambda i, b=bufs, p=p: sbw.watermark(
+                b[i % len(b)], p, key, gamma, delta, seeding), steps))
+            del bufs, x
+        esize = 2 if dt == torch.bfloat16 else 4
+        out[name] = {"B": list(Bs), "us": ts,
+                     "fit_per_logit": fit([B * V for B in Bs], ts),
+                     "fit_per_hbm_byte": fit([2 * esize * B * V for B in Bs], ts)}
+        torch.cuda.empty_cache()
+    return out
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -615,8 +669,12 @@ def main():
 
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    CONFIG_WARM_MS[0] = args.config_warm_ms
     if args.launch_only:
         launch_only(torch, sbw, dev, args.launch_only)
+        return
+    if args.floors:
+        print(json.dumps({"floors": floors(torch, sbw, dev)}))
         return
     c4, c5 = workloads.C4, workloads.C5
     key = workloads.PAPER_KEY
@@ -633,6 +691,7 @@ def main():
         toks[seeding] = workloads.detect_inputs(c5["N"], c5["L"], c5["V"], c5["gamma"],
                                                 c5["delta"], seeding, member)
     tok_d = {s: torch.from_numpy(t).to(dev) for s, t in toks.items()}
+    progress("inputs ready")
     counts = {s: torch.empty(c5["N"], dtype=torch.int32, device=dev) for s in toks}
     zs = {s: torch.empty(c5["N"], dtype=torch.float64, device=dev) for s in toks}
     torch.cuda.synchronize()
@@ -665,9 +724,12 @@ def main():
         graphs.append(g)
 
     # Warm-up by GPU time, not by step count: the four graphs replayed in the timed
-    # order until --warm-ms have passed, so the timed region starts at steady state.
+    # order until --warm-ms have passed, so the timed region starts at steady state,
+    # right after it (no idle gap).  A host thread reads the GFX clock throughout.
     w0, w1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    marks = [torch.cuda.Event(enable_timing=True) for _ in range(len(launches) + 1)]
     warm_ms, warm_cycles = 0.0, 0
+    clock = GfxClock()
     while warm_ms < args.warm_ms:
         w0.record()
         for g in graphs:
@@ -679,21 +741,19 @@ def main():
 
     # Timed region: exactly `steps` steps, their launches grouped by kernel (one graph
     # replay per kernel), with a HIP event on the launching stream at each group
-    # boundary: a kernel's mean launch duration is its group time / steps.  A host
-    # thread reads the GFX clock meanwhile.
-    marks = [torch.cuda.Event(enable_timing=True) for _ in range(len(launches) + 1)]
-    with ClockSampler() as clock:
-        time.sleep(0.005)
-        torch.cuda.synchronize()
-        wall0 = time.perf_counter()
-        marks[0].record()
-        for k, g in enumerate(graphs):
-            g.replay()
-            marks[k + 1].record()
-        torch.cuda.synchronize()
-        wall1 = time.perf_counter()
+    # boundary: a kernel's mean launch duration is its group time / steps.  Once all
+    # of it is queued, one GFX-clock reading is taken while the GPU runs it.
+    wall0 = time.perf_counter()
+    marks[0].record()
+    for k, g in enumerate(graphs):
+        g.replay()
+        marks[k + 1].record()
+    t_read = time.perf_counter()
+    clock_timed = clock.read()
+    torch.cuda.synchronize()
+    wall1 = time.perf_counter()
+    clock_timed["read_ms_after_start"] = (t_read - wall0) * 1e3
     wall = wall1 - wall0
-    clock_timed = clock.between(wall0, wall1)
     total_ms = marks[0].elapsed_time(marks[-1])
     mean_ms = {name: marks[k].elapsed_time(marks[k + 1]) / args.steps
                for k, (name, _) in enumerate(launches)}
@@ -743,7 +803,9 @@ def main():
         hits = [v for k, v in traffic.items() if k.startswith(prefix)]
         return hits[0] if len(hits) == 1 else None
 
+    progress(f"timed region done ({total_ms:.2f} ms)")
     roof = philox_roof(torch)
+    progress("Philox roof measured")
     out = {
         "metric": "watermarked logits Gelem/s + achieved HBM GB/s (B=256,V=152064); detect seq/s",
         "value": ss["gelem_per_s"],
@@ -795,16 +857,21 @@ def main():
         del bufs
         torch.cuda.empty_cache()
         out["configs"] = other_configs(torch, sbw, dev, args.steps, toks)
-        # The fused argmax and sampling passes run at one shape only, so the name keys them.
+        # The fused decoding passes at B = 256: the profile keys them by name and by
+        # workgroups, one per (row, segment) of 6144 (greedy) or 8192 (sampling) logits.
         traffic_cfg = measured_traffic(PROFILE_CONFIGS)
-        for cfg, mode in (("c4_watermark_argmax", "false"), ("c4_watermark_sample", "true")):
+        for cfg, mode, seg in (("c4_watermark_argmax", "false", 6144),
+                               ("c4_watermark_sample", "true", 8192)):
+            groups = B * -(-V // seg)
             for seeding, code in (("context", 0), ("self_salt", 1)):
                 hits = [v for k, v in traffic_cfg.items()
                         if k.startswith(f"sbw::decode_vec_kernel<float, {code},")
-                        and k.split("@")[0].endswith(f", {mode}>")]
+                        and k.split("@")[0].endswith(f", {mode}>")
+                        and k.split("@")[1] == str(groups)]
                 out["configs"][cfg][seeding]["traffic"] = hits[0] if len(hits) == 1 else None
         out["paper_table"] = paper_table(torch, sbw, dev)
     if not args.no_cpu_baseline:
+        progress("CPU oracle baseline")
         out["cpu_baseline"] = cpu_baseline(x, prev, toks, args.cpu_runs)
     print(json.dumps(out))
 
