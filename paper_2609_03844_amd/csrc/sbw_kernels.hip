@@ -1157,19 +1157,24 @@ detect_kernel(const int32_t* __restrict__ tokens, int64_t N, int64_t L, int64_t 
     const uint32_t len = static_cast<uint32_t>(sequence_length(io.lengths, n, L));
     uint32_t green = 0u;  // wave-uniform count
     for (uint32_t base = static_cast<uint32_t>(width); base < len; base += kWave * kChunk) {
+      // The pass's tokens and their windows from two wave-uniform bases, so that each
+      // load needs only the lane's small offset.
+      const int32_t* pass = seq + base;
+      const int32_t* pass_w = pass - width;
+      const uint32_t rem = len - base;              // positions left, > 0
       uint32_t w[kChunk][kW], v[kChunk];
       bool in[kChunk];
 #pragma unroll
       for (int c = 0; c < kChunk; ++c) {
-        const uint32_t i = base + static_cast<uint32_t>(c * kWave + lane);
-        in[c] = i < len;
-        const uint32_t ic = in[c] ? i : len - 1u;   // >= width: base < len
-        v[c] = static_cast<uint32_t>(seq[ic]);
+        const uint32_t o = static_cast<uint32_t>(c * kWave + lane);
+        in[c] = o < rem;
+        const uint32_t oc = min(o, rem - 1u);        // o when in range; at most o < 64 kChunk
+        v[c] = static_cast<uint32_t>(pass[oc]);
         constexpr bool kShared = kSeeding == kSelfSalt && kW == 1;   // terms handed over
 #pragma unroll
         for (int k = 0; k < kW; ++k)
           w[c][k] = ((kW == 1 || k < width) && (!kShared || c == 0))
-                        ? static_cast<uint32_t>(seq[ic - static_cast<uint32_t>(width - k)])
+                        ? static_cast<uint32_t>(pass_w[oc + static_cast<uint32_t>(k)])
                         : 0u;
       }
       // Independent membership chains first (instruction-level parallelism), then
