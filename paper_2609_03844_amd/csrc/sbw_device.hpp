@@ -142,6 +142,17 @@ __device__ __forceinline__ uint64_t mul_64x32(uint64_t a, uint32_t b) {
   return (static_cast<uint64_t>(hi) << 32) | static_cast<uint32_t>(lo);
 }
 
+// Low 64 bits of a * b for a per-lane b: the high word's product and the carry-in add
+// stay two instructions (a fused multiply-add with a 64-bit addend would need the
+// carry-in moved into the low half of a register pair first, and the result moved
+// back).
+__device__ __forceinline__ uint64_t lane_mul_64x32(uint64_t a, uint32_t b) {
+  const uint64_t lo = wide_mul(static_cast<uint32_t>(a), b);
+  uint32_t h = static_cast<uint32_t>(a >> 32) * b;
+  asm("" : "+v"(h));
+  return (static_cast<uint64_t>(static_cast<uint32_t>(lo >> 32) + h) << 32) | static_cast<uint32_t>(lo);
+}
+
 // Low 64 bits of a * s for 64-bit a and s (three 32x32 products).
 __device__ __forceinline__ uint64_t mul_64x64(uint64_t a, uint64_t s) {
   const uint32_t a0 = static_cast<uint32_t>(a), a1 = static_cast<uint32_t>(a >> 32);

@@ -144,7 +144,7 @@ __device__ __forceinline__ uint64_t self_salt_seed_t(const RowSeed<kW>& rs, cons
 #pragma unroll
   for (int i = 0; i < kW; ++i) {
     if (kW == 1 || i < rs.width) {
-      const uint64_t x = mul_64x32(rs.kjp[i], t.jv);
+      const uint64_t x = lane_mul_64x32(rs.kjp[i], t.jv);
       best = x < best ? x : best;
     }
   }
@@ -1094,18 +1094,22 @@ __device__ __forceinline__ bool window_green(uint64_t key, const uint32_t (&w)[k
                                              uint32_t v, uint32_t tm1) {
   uint64_t r;
   if (kSeeding == kContext) {
-    uint64_t sum = 0u;
+    if constexpr (kW == 1) {
+      r = lane_mul_64x32(key, w[0]);
+    } else {
+      uint64_t sum = 0u;
 #pragma unroll
-    for (int i = 0; i < kW; ++i)
-      if (kW == 1 || i < width) sum += w[i];
-    r = key * sum;
+      for (int i = 0; i < kW; ++i)
+        if (i < width) sum += w[i];
+      r = key * sum;
+    }
   } else {
     const uint32_t jv = jenkins32(v);
     r = mul_64x64(key, wide_mul(jv, jv));
 #pragma unroll
     for (int i = 0; i < kW; ++i) {
       if (kW == 1 || i < width) {
-        const uint64_t t = mul_64x32(key * static_cast<uint64_t>(jenkins32(w[i])), jv);
+        const uint64_t t = lane_mul_64x32(key * static_cast<uint64_t>(jenkins32(w[i])), jv);
         r = t < r ? t : r;
       }
     }
@@ -1143,74 +1147,99 @@ __device__ __forceinline__ void detect_store(const DetectIO& io, int64_t n, uint
 
 // Positions are 32-bit (L < 2^31).  Lanes past the end of the sequence load the last
 // token instead (a valid address), so the loads need no branch; their positions are
-// masked out of the count.
+// masked out of the count with a lane mask built in scalar registers.  The four waves
+// of a workgroup take four sequences; their counts meet in LDS and one wave computes
+// the four z-scores side by side (lanes 0-3), so the fp64 epilogue issues once per
+// workgroup instead of once per wave.  Every wave of the workgroup runs the same
+// number of outer iterations, so the barriers are reached by all of them.
 template <int kSeeding, int kChunk, int kW>
 __global__ void __launch_bounds__(kThreads)
 detect_kernel(const int32_t* __restrict__ tokens, int64_t N, int64_t L, int64_t row_stride,
               int width, uint64_t key, uint32_t tm1, double gamma, DetectIO io) {
-  const int lane = threadIdx.x % kWave;
-  // the wave's sequence index, in scalar registers
-  const int64_t wave0 = static_cast<int64_t>(blockIdx.x) * kWavesPerBlock +
-                        __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x / kWave));
-  for (int64_t n = wave0; n < N; n += static_cast<int64_t>(gridDim.x) * kWavesPerBlock) {
-    const int32_t* seq = tokens + n * row_stride;
-    const uint32_t len = static_cast<uint32_t>(sequence_length(io.lengths, n, L));
+  __shared__ uint32_t lds_green[kWavesPerBlock], lds_len[kWavesPerBlock];
+  const uint32_t lane = threadIdx.x % kWave;
+  // the wave's index in the workgroup, in a scalar register
+  const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x / kWave));
+  for (int64_t n0 = static_cast<int64_t>(blockIdx.x) * kWavesPerBlock; n0 < N;
+       n0 += static_cast<int64_t>(gridDim.x) * kWavesPerBlock) {
+    const int64_t n = n0 + wave;
     uint32_t green = 0u;  // wave-uniform count
-    for (uint32_t base = static_cast<uint32_t>(width); base < len; base += kWave * kChunk) {
-      // The pass's tokens and their windows from two wave-uniform bases, so that each
-      // load needs only the lane's small offset.
-      const int32_t* pass = seq + base;
-      const int32_t* pass_w = pass - width;
-      const uint32_t rem = len - base;              // positions left, > 0
-      uint32_t w[kChunk][kW], v[kChunk];
-      bool in[kChunk];
-#pragma unroll
-      for (int c = 0; c < kChunk; ++c) {
-        const uint32_t o = static_cast<uint32_t>(c * kWave + lane);
-        in[c] = o < rem;
-        const uint32_t oc = min(o, rem - 1u);        // o when in range; at most o < 64 kChunk
-        v[c] = static_cast<uint32_t>(pass[oc]);
+    uint32_t len = 0u;
+    if (n < N) {
+      const int32_t* seq = tokens + n * row_stride;
+      len = static_cast<uint32_t>(sequence_length(io.lengths, n, L));
+      for (uint32_t base = static_cast<uint32_t>(width); base < len; base += kWave * kChunk) {
+        // The pass's tokens and their windows from two wave-uniform bases; each load
+        // adds the lane's byte offset, clamped to the pass's last position.
+        const char* pass = reinterpret_cast<const char*>(seq + base);
+        const char* pass_w = pass - 4 * width;
+        const uint32_t rem = len - base;              // positions left, > 0
+        const uint32_t last_byte = 4u * (rem - 1u);
+        uint32_t w[kChunk][kW], v[kChunk];
         constexpr bool kShared = kSeeding == kSelfSalt && kW == 1;   // terms handed over
 #pragma unroll
-        for (int k = 0; k < kW; ++k)
-          w[c][k] = ((kW == 1 || k < width) && (!kShared || c == 0))
-                        ? static_cast<uint32_t>(pass_w[oc + static_cast<uint32_t>(k)])
-                        : 0u;
-      }
-      // Independent membership chains first (instruction-level parallelism), then
-      // one ballot per chunk.
-      bool g[kChunk];
-      if constexpr (kSeeding == kSelfSalt && kW == 1) {
-        // Self-salt, width 1: the seed of position i is min(K J(p) J(v), K J(v) J(v))
-        // with p the token at i - 1.  Each lane computes K J(v) of its own token once;
-        // position i's K J(p) is position i - 1's K J(v), held by the lane before (lane
-        // 63 of the chunk before, for lane 0; from the window token itself for the
-        // pass's first position), and a wave shift hands it over.
-        uint32_t jv[kChunk];
-        uint64_t kj[kChunk];
+        for (int c = 0; c < kChunk; ++c) {
+          const uint32_t ob = min(4u * (static_cast<uint32_t>(c * kWave) + lane), last_byte);
+          v[c] = *reinterpret_cast<const uint32_t*>(pass + ob);
+#pragma unroll
+          for (int k = 0; k < kW; ++k)
+            w[c][k] = ((kW == 1 || k < width) && !kShared)
+                          ? *reinterpret_cast<const uint32_t*>(pass_w + ob + 4u * static_cast<uint32_t>(k))
+                          : 0u;
+        }
+        // Independent membership chains first (instruction-level parallelism), then
+        // one ballot per chunk.
+        bool g[kChunk];
+        if constexpr (kShared) {
+          // Self-salt, width 1: the seed of position i is min(K J(p) J(v), K J(v) J(v))
+          // with p the token at i - 1.  Each lane computes K J(v) of its own token once;
+          // position i's K J(p) is position i - 1's K J(v), held by the lane before (lane
+          // 63 of the chunk before, for lane 0), and a wave shift hands it over.  The
+          // pass's first window token is the same for the whole wave: one scalar load,
+          // hashed in scalar registers.
+          uint32_t jv[kChunk];
+          uint64_t kj[kChunk];
+#pragma unroll
+          for (int c = 0; c < kChunk; ++c) {
+            jv[c] = jenkins32(v[c]);
+            kj[c] = lane_mul_64x32(key, jv[c]);
+          }
+          const uint32_t p0 = *reinterpret_cast<const uint32_t*>(pass_w);
+          uint64_t carry = key * static_cast<uint64_t>(jenkins32(p0));
+#pragma unroll
+          for (int c = 0; c < kChunk; ++c) {
+            if (c > 0) carry = readlane64(kj[c - 1], kWave - 1);
+            const uint64_t kjp = wave_shift_right(kj[c], carry);
+            const uint64_t self = lane_mul_64x32(kj[c], jv[c]);
+            const uint64_t t = lane_mul_64x32(kjp, jv[c]);
+            g[c] = is_green(cbrng(v[c], t < self ? t : self), tm1);
+          }
+        } else {
+#pragma unroll
+          for (int c = 0; c < kChunk; ++c) g[c] = window_green<kSeeding, kW>(key, w[c], width, v[c], tm1);
+        }
+        // Chunks before rem / 64 lie inside the sequence, the next one holds its last
+        // rem % 64 positions, the others none (masks in scalar registers).
+        const uint32_t full_chunks = rem / static_cast<uint32_t>(kWave);
+        const uint64_t part_mask = (uint64_t{1} << (rem % static_cast<uint32_t>(kWave))) - 1u;
 #pragma unroll
         for (int c = 0; c < kChunk; ++c) {
-          jv[c] = jenkins32(v[c]);
-          kj[c] = mul_64x32(key, jv[c]);
+          const uint32_t cu = static_cast<uint32_t>(c);
+          const uint64_t valid = cu < full_chunks ? ~uint64_t{0} : (cu == full_chunks ? part_mask : 0u);
+          green += static_cast<uint32_t>(__popcll(__ballot(g[c]) & valid));
         }
-        uint64_t carry = mul_64x32(key, jenkins32(w[0][0]));
-#pragma unroll
-        for (int c = 0; c < kChunk; ++c) {
-          if (c > 0) carry = readlane64(kj[c - 1], kWave - 1);
-          const uint64_t kjp = wave_shift_right(kj[c], carry);
-          const uint64_t self = mul_64x32(kj[c], jv[c]);
-          const uint64_t t = mul_64x32(kjp, jv[c]);
-          g[c] = is_green(cbrng(v[c], t < self ? t : self), tm1) && in[c];
-        }
-      } else {
-#pragma unroll
-        for (int c = 0; c < kChunk; ++c)
-          g[c] = window_green<kSeeding, kW>(key, w[c], width, v[c], tm1) && in[c];
       }
-#pragma unroll
-      for (int c = 0; c < kChunk; ++c) green += static_cast<uint32_t>(__popcll(__ballot(g[c])));
     }
-    if (lane == 0) detect_store(io, n, green, len > static_cast<uint32_t>(width) ? len - width : 0, gamma);
+    if (lane == 0u) {
+      lds_green[wave] = green;
+      lds_len[wave] = len;
+    }
+    __syncthreads();
+    if (wave == 0 && lane < static_cast<uint32_t>(kWavesPerBlock) && n0 + lane < N) {
+      const uint32_t ln = lds_len[lane];
+      detect_store(io, n0 + lane, lds_green[lane], ln > static_cast<uint32_t>(width) ? ln - width : 0, gamma);
+    }
+    __syncthreads();  // the LDS slots are rewritten by the next iteration
   }
 }
 
