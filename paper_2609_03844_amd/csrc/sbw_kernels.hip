@@ -1114,7 +1114,7 @@ __device__ __forceinline__ bool window_green(uint64_t key, const uint32_t (&w)[k
       }
     }
   }
-  return is_green(cbrng(v, r), tm1);
+  return is_green(cbrng_lane(v, r), tm1);
 }
 
 // Positions handled per lane per pass: a pass covers 64 * kChunk positions and
@@ -1212,7 +1212,7 @@ detect_kernel(const int32_t* __restrict__ tokens, int64_t N, int64_t L, int64_t 
             const uint64_t kjp = wave_shift_right(kj[c], carry);
             const uint64_t self = lane_mul_64x32(kj[c], jv[c]);
             const uint64_t t = lane_mul_64x32(kjp, jv[c]);
-            g[c] = is_green(cbrng(v[c], t < self ? t : self), tm1);
+            g[c] = is_green(cbrng_lane(v[c], t < self ? t : self), tm1);
           }
         } else {
 #pragma unroll
