@@ -101,13 +101,16 @@ __device__ __forceinline__ void philox_round_lane(uint32_t& x0, uint32_t& x1, ui
   k1 = k1n;
 }
 
-// philox_block for a per-lane key: round 0 and the last round as in philox_block
-// (the zero counter words fold away; the last round keeps only the words read),
-// rounds 1-8 in the issue order above.  The same block, bit for bit.
+// philox_block for a per-lane key: round 0 as in philox_block (the zero counter words
+// fold away), rounds 1 to kLast in the issue order above, the rest as in philox_block,
+// so that a caller reading only some words lets the last rounds shrink to what those
+// words need (kLast = 7 keeps round 8 open to that too).  The same block, bit for bit.
+template <int kLast = 8>
 __device__ __forceinline__ Block philox_block_lane(uint32_t c0, Key k) {
 #if SBW_PHILOX_SCHED
   static_assert(kPhiloxWeyl0 == 0x9E3779B9u && kPhiloxWeyl1 == 0xBB67AE85u,
                 "the scheduled rounds spell the key increments out");
+  static_assert(kLast >= 1 && kLast <= 8, "rounds 1-8 can be scheduled");
   uint32_t mul_a = kPhiloxMulA, mul_b = kPhiloxMulB;
   const uint64_t pa0 = wide_mul(kPhiloxMulA, c0);
   uint32_t x0 = k.lo;
@@ -116,11 +119,21 @@ __device__ __forceinline__ Block philox_block_lane(uint32_t c0, Key k) {
   uint32_t x3 = static_cast<uint32_t>(pa0);
   uint32_t k0 = k.lo + kPhiloxWeyl0, k1 = k.hi + kPhiloxWeyl1;
 #pragma unroll
-  for (int round = 1; round < 9; ++round) philox_round_lane(x0, x1, x2, x3, k0, k1, mul_a, mul_b);
-  const uint64_t pa = wide_mul(kPhiloxMulA, x0);
-  const uint64_t pb = wide_mul(kPhiloxMulB, x2);
-  return Block{xor3(static_cast<uint32_t>(pb >> 32), x1, k0), static_cast<uint32_t>(pb),
-               xor3(static_cast<uint32_t>(pa >> 32), x3, k1), static_cast<uint32_t>(pa)};
+  for (int round = 1; round <= kLast; ++round) philox_round_lane(x0, x1, x2, x3, k0, k1, mul_a, mul_b);
+#pragma unroll
+  for (int round = kLast + 1; round < 10; ++round) {
+    const uint64_t pa = wide_mul(kPhiloxMulA, x0);
+    const uint64_t pb = wide_mul(kPhiloxMulB, x2);
+    const uint32_t y0 = xor3(static_cast<uint32_t>(pb >> 32), x1, k0);
+    const uint32_t y2 = xor3(static_cast<uint32_t>(pa >> 32), x3, k1);
+    x1 = static_cast<uint32_t>(pb);
+    x3 = static_cast<uint32_t>(pa);
+    x0 = y0;
+    x2 = y2;
+    k0 += kPhiloxWeyl0;
+    k1 += kPhiloxWeyl1;
+  }
+  return Block{x0, x1, x2, x3};
 #else
   return philox_block(c0, k);
 #endif

@@ -268,10 +268,10 @@ watermark_vec_kernel(T* __restrict__ logits, int64_t row_stride, uint32_t V, int
 template <int kW>
 __device__ __forceinline__ f32x4 bias_vec_terms(f32x4 l, uint32_t j, const CandTerm (&ct)[4],
                                                 const RowSeed<kW>& rs, uint32_t tm1, float delta) {
-  const uint32_t x0 = philox_block(j, key_of(self_salt_seed_t(rs, ct[0]))).w0;
-  const uint32_t x1 = philox_block(j, key_of(self_salt_seed_t(rs, ct[1]))).w1;
-  const uint32_t x2 = philox_block(j, key_of(self_salt_seed_t(rs, ct[2]))).w2;
-  const uint32_t x3 = philox_block(j, key_of(self_salt_seed_t(rs, ct[3]))).w3;
+  const uint32_t x0 = philox_block_lane<6>(j, key_of(self_salt_seed_t(rs, ct[0]))).w0;
+  const uint32_t x1 = philox_block_lane<6>(j, key_of(self_salt_seed_t(rs, ct[1]))).w1;
+  const uint32_t x2 = philox_block_lane<6>(j, key_of(self_salt_seed_t(rs, ct[2]))).w2;
+  const uint32_t x3 = philox_block_lane<6>(j, key_of(self_salt_seed_t(rs, ct[3]))).w3;
   f32x4 o;
   o.x = bias_f32(l.x, delta, is_green(x0, tm1));
   o.y = bias_f32(l.y, delta, is_green(x1, tm1));
@@ -286,8 +286,8 @@ __device__ __forceinline__ u32x4 bias_vec_terms(u32x4 raw, uint32_t j, const Can
   uint32_t x[8];
 #pragma unroll
   for (int e = 0; e < 8; ++e)
-    x[e] = block_word(philox_block(2u * j + static_cast<uint32_t>(e >> 2),
-                                   key_of(self_salt_seed_t(rs, ct[e]))),
+    x[e] = block_word(philox_block_lane<6>(2u * j + static_cast<uint32_t>(e >> 2),
+                                           key_of(self_salt_seed_t(rs, ct[e]))),
                       static_cast<uint32_t>(e & 3));
   const uint32_t in[4] = {raw.x, raw.y, raw.z, raw.w};
   uint32_t out[4];
