@@ -15,13 +15,20 @@
 // constant-rate real-time counter (s_memrealtime) at its start and end, so the host
 // can tell the core clock the probe ran at.
 //
+// A second kernel draws the same blocks through the library's per-lane-key block
+// (sbw::philox_block_lane: rounds 1-8 in the fixed issue order products, key adds,
+// xors), so the benchmark can report the better of the two orders.
+//
 // The same launch shape also times single instruction kinds (kChains independent
 // dependency chains per lane, one instruction per link), so that the issue cost of
 // each of the block's three instruction kinds, and of their mix, can be measured in
 // lane-ops per compute-unit clock: 32x32->64-bit products (v_mad_u64_u32), three-input
-// xors (v_bitop3_b32) and 32-bit adds.
+// xors (v_bitop3_b32) and 32-bit adds, with vector operands, and the xor and the add
+// with one scalar operand.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
+
+#include "sbw_device.hpp"
 
 namespace {
 
@@ -90,11 +97,52 @@ philox_rate_kernel(uint32_t* __restrict__ out, uint64_t* __restrict__ clocks, in
   }
 }
 
-enum OpKind : int { kOpMad64 = 1, kOpBitop3 = 2, kOpAdd = 3, kOpPhiloxMix = 4 };
+// The same blocks as philox_rate_kernel through sbw::philox_block_lane.
+__global__ void __launch_bounds__(kThreads)
+philox_sched_kernel(uint32_t* __restrict__ out, uint64_t* __restrict__ clocks, int iters,
+                    uint32_t salt) {
+  uint64_t t0 = 0, r0 = 0;
+  if (threadIdx.x == 0) {
+    r0 = __builtin_amdgcn_s_memrealtime();
+    t0 = __builtin_amdgcn_s_memtime();
+  }
+  const uint32_t lane = blockIdx.x * kThreads + threadIdx.x;
+  uint32_t k0[kChains], k1[kChains];
+#pragma unroll
+  for (int c = 0; c < kChains; ++c) {
+    k0[c] = lane ^ (static_cast<uint32_t>(c) << 24) ^ salt;
+    k1[c] = lane * 0x9E3779B1u + static_cast<uint32_t>(c);
+  }
+  for (int i = 0; i < iters; ++i) {
+#pragma unroll
+    for (int c = 0; c < kChains; ++c) {
+      const sbw::Block b = sbw::philox_block_lane(static_cast<uint32_t>(i), sbw::Key{k0[c], k1[c]});
+      k0[c] = b.w0 ^ b.w1;
+      k1[c] = b.w2 ^ b.w3;
+    }
+  }
+  uint32_t acc = 0u;
+#pragma unroll
+  for (int c = 0; c < kChains; ++c) acc ^= k0[c] ^ k1[c];
+  out[lane] = acc;
+  if (threadIdx.x == 0) {
+    const uint64_t t1 = __builtin_amdgcn_s_memtime();
+    const uint64_t r1 = __builtin_amdgcn_s_memrealtime();
+    clocks[4 * blockIdx.x + 0] = t0;
+    clocks[4 * blockIdx.x + 1] = t1;
+    clocks[4 * blockIdx.x + 2] = r0;
+    clocks[4 * blockIdx.x + 3] = r1;
+  }
+}
+
+enum OpKind : int {
+  kOpMad64 = 1, kOpBitop3 = 2, kOpAdd = 3, kOpPhiloxMix = 4, kOpBitop3Scalar = 5, kOpAddScalar = 6
+};
 
 // kChains chains of `iters` x 16 links of one instruction kind per lane.  kOpPhiloxMix
 // interleaves them in the block's proportions: per link one product, one xor and one
-// add.
+// add.  Every operand is a vector register except in the two scalar kinds, whose xor
+// or add takes one wave-uniform operand.
 template <int kKind>
 __global__ void __launch_bounds__(kThreads)
 op_rate_kernel(uint32_t* __restrict__ out, uint64_t* __restrict__ clocks, int iters,
@@ -111,7 +159,9 @@ op_rate_kernel(uint32_t* __restrict__ out, uint64_t* __restrict__ clocks, int it
     a[c] = lane ^ (static_cast<uint32_t>(c) << 24) ^ salt;
     b[c] = lane * 0x9E3779B1u + static_cast<uint32_t>(c);
   }
-  const uint32_t m = salt | 1u;
+  const uint32_t m = salt | 1u;                  // wave-uniform: a scalar register
+  uint32_t mv = m ^ (lane & 1u);                 // per lane: a vector register
+  asm volatile("" : "+v"(mv));
   for (int i = 0; i < iters; ++i) {
 #pragma unroll
     for (int l = 0; l < 16; ++l) {
@@ -124,15 +174,21 @@ op_rate_kernel(uint32_t* __restrict__ out, uint64_t* __restrict__ clocks, int it
           a[c] = static_cast<uint32_t>(p);
           b[c] = static_cast<uint32_t>(p >> 32);
         } else if constexpr (kKind == kOpBitop3) {
-          a[c] = xor3(a[c], b[c], m);
+          a[c] = xor3(a[c], b[c], mv);
         } else if constexpr (kKind == kOpAdd) {
           // alternating a += b, b += a: no two links fold into one
           if (l & 1) b[c] = b[c] + a[c];
           else a[c] = a[c] + b[c];
-        } else {
+        } else if constexpr (kKind == kOpPhiloxMix) {
           const uint64_t p = static_cast<uint64_t>(kMulA) * a[c];
-          a[c] = xor3(static_cast<uint32_t>(p >> 32), b[c], m);
+          a[c] = xor3(static_cast<uint32_t>(p >> 32), b[c], mv);
           b[c] = b[c] + static_cast<uint32_t>(p);
+        } else if constexpr (kKind == kOpBitop3Scalar) {
+          a[c] = xor3(a[c], b[c], m);
+        } else {
+          // a scalar operand (written out: the compiler would fold a chain of adds of
+          // one uniform value into one product)
+          asm volatile("v_add_u32 %0, %1, %0" : "+v"(a[c]) : "s"(m));
         }
       }
     }
@@ -155,6 +211,16 @@ op_rate_kernel(uint32_t* __restrict__ out, uint64_t* __restrict__ clocks, int it
 
 extern "C" {
 
+// The same with the library's per-lane-key block (fixed round issue order).
+int sbw_rate_philox_sched(uint32_t* out, uint64_t* clocks, int workgroups, int iters,
+                          uint32_t salt, void* stream) {
+  if (out == nullptr || clocks == nullptr || workgroups <= 0 || iters <= 0)
+    return static_cast<int>(hipErrorInvalidValue);
+  hipLaunchKernelGGL(philox_sched_kernel, dim3(workgroups), dim3(kThreads), 0,
+                     static_cast<hipStream_t>(stream), out, clocks, iters, salt);
+  return static_cast<int>(hipGetLastError());
+}
+
 // Blocks drawn per lane and launch: iters * chains.
 int sbw_rate_chains(void) { return kChains; }
 int sbw_rate_threads(void) { return kThreads; }
@@ -173,8 +239,9 @@ int sbw_rate_philox(uint32_t* out, uint64_t* clocks, int workgroups, int iters, 
 }
 
 // The single-kind chains: kind 1 products, 2 three-input xors, 3 adds, 4 the mix of
-// one of each per link.  Each lane runs iters * 16 * sbw_rate_chains() links (the mix:
-// three instructions per link).  Same buffers as sbw_rate_philox.
+// one of each per link, 5 three-input xors and 6 adds with one scalar operand.  Each
+// lane runs iters * 16 * sbw_rate_chains() links (the mix: three instructions per
+// link).  Same buffers as sbw_rate_philox.
 int sbw_rate_op(int kind, uint32_t* out, uint64_t* clocks, int workgroups, int iters,
                 uint32_t salt, void* stream) {
   if (out == nullptr || clocks == nullptr || workgroups <= 0 || iters <= 0)
@@ -193,6 +260,14 @@ int sbw_rate_op(int kind, uint32_t* out, uint64_t* clocks, int workgroups, int i
       break;
     case kOpPhiloxMix:
       hipLaunchKernelGGL(op_rate_kernel<kOpPhiloxMix>, grid, block, 0, st, out, clocks, iters,
+                         salt);
+      break;
+    case kOpBitop3Scalar:
+      hipLaunchKernelGGL(op_rate_kernel<kOpBitop3Scalar>, grid, block, 0, st, out, clocks, iters,
+                         salt);
+      break;
+    case kOpAddScalar:
+      hipLaunchKernelGGL(op_rate_kernel<kOpAddScalar>, grid, block, 0, st, out, clocks, iters,
                          salt);
       break;
     default:
