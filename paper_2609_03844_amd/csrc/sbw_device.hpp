@@ -140,10 +140,13 @@ __device__ __forceinline__ Block philox_block_lane(uint32_t c0, Key k) {
 }
 
 __device__ __forceinline__ uint32_t block_word(const Block& b, uint32_t i) {
-  // i in [0, 4); a select chain, no dynamic register indexing.
-  const uint32_t lo = (i & 1u) ? b.w1 : b.w0;
-  const uint32_t hi = (i & 1u) ? b.w3 : b.w2;
-  return (i & 2u) ? hi : lo;
+  // i in [0, 4): each of its two bits sign-extended into a full mask, then bitwise
+  // selects (three-input LUT 0xCA: m ? x : y per bit), vector registers only.
+  const uint32_t m0 = static_cast<uint32_t>(__builtin_amdgcn_sbfe(static_cast<int>(i), 0, 1));
+  const uint32_t m1 = static_cast<uint32_t>(__builtin_amdgcn_sbfe(static_cast<int>(i), 1, 1));
+  const uint32_t lo = __builtin_amdgcn_bitop3_b32(m0, b.w1, b.w0, 0xCA);
+  const uint32_t hi = __builtin_amdgcn_bitop3_b32(m0, b.w3, b.w2, 0xCA);
+  return __builtin_amdgcn_bitop3_b32(m1, hi, lo, 0xCA);
 }
 
 // A copy of a wave-uniform key that the optimiser cannot see through.  Without it,
