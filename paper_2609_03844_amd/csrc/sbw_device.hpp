@@ -104,7 +104,8 @@ __device__ __forceinline__ void philox_round_lane(uint32_t& x0, uint32_t& x1, ui
 // philox_block for a per-lane key: round 0 as in philox_block (the zero counter words
 // fold away), rounds 1 to kLast in the issue order above, the rest as in philox_block,
 // so that a caller reading only some words lets the last rounds shrink to what those
-// words need (kLast = 7 keeps round 8 open to that too).  The same block, bit for bit.
+// words need (the self-salt watermark, which keeps one word per block, schedules rounds
+// 1-6).  The same block, bit for bit.
 template <int kLast = 8>
 __device__ __forceinline__ Block philox_block_lane(uint32_t c0, Key k) {
 #if SBW_PHILOX_SCHED
