@@ -214,6 +214,39 @@ __device__ __forceinline__ uint32_t jenkins32(uint32_t a) {
   return a;
 }
 
+// Low word of a * m + c by one v_mad_u64_u32: m in a scalar register and c in a
+// vector register pair, or m an inline constant and c in a scalar register pair (one
+// scalar operand either way).  The carry-out goes to a scalar pair nobody reads.
+__device__ __forceinline__ uint32_t mad_lo(uint32_t a, uint32_t m, uint64_t c) {
+  uint64_t r, carry;
+  asm("v_mad_u64_u32 %0, %1, %2, %3, %4" : "=v"(r), "=s"(carry) : "v"(a), "s"(m), "v"(c));
+  return static_cast<uint32_t>(r);
+}
+template <int kM>
+__device__ __forceinline__ uint32_t mad_lo_inline(uint32_t a, uint64_t c) {
+  static_assert(kM >= 0 && kM <= 64, "an inline integer constant");
+  uint64_t r, carry;
+  asm("v_mad_u64_u32 %0, %1, %2, %3, %4" : "=v"(r), "=s"(carry) : "v"(a), "i"(kM), "s"(c));
+  return static_cast<uint32_t>(r);
+}
+
+// jenkins32 for a value that differs from lane to lane, in 9 vector instructions
+// instead of the compiler's 13.  Each add-shift step (a + c) + (a << s) is
+// a * (2^s + 1) + c, the low word of one multiply-add.  The third and fourth steps
+// combine: with b = a * 33 + c3, step four is (b + c4) ^ (b << 9), and
+// b << 9 = a * 16896 + (c3 << 9), so both operands are multiply-adds of a itself.  The
+// first xor-shift is one three-input xor.  Products never dual-issue, so this pays where
+// the hash is taken once per scored token in an issue-bound loop (detection), not where
+// it is taken once per column and reused by many rows (measured slightly slower there).
+__device__ __forceinline__ uint32_t jenkins32_lane(uint32_t a) {
+  a = mad_lo(a, 4097u, 0x7ed55d16u);
+  a = xor3(a, a >> 19, 0xc761c23cu);
+  const uint32_t u = mad_lo_inline<33>(a, 0x165667b1u + 0xd3a2646cu);
+  const uint32_t w = mad_lo(a, 16896u, 0x165667b1u << 9);
+  a = mad_lo_inline<9>(u ^ w, 0xfd7046c5u);
+  return (a ^ 0xb55a4f09u) ^ (a >> 16);
+}
+
 // Context seed: r = key * p mod 2^64.
 __device__ __forceinline__ uint64_t context_seed(uint64_t key, uint32_t p) {
   return key * static_cast<uint64_t>(p);

@@ -1104,12 +1104,12 @@ __device__ __forceinline__ bool window_green(uint64_t key, const uint32_t (&w)[k
       r = key * sum;
     }
   } else {
-    const uint32_t jv = jenkins32(v);
+    const uint32_t jv = jenkins32_lane(v);
     r = mul_64x64(key, wide_mul(jv, jv));
 #pragma unroll
     for (int i = 0; i < kW; ++i) {
       if (kW == 1 || i < width) {
-        const uint64_t t = lane_mul_64x32(key * static_cast<uint64_t>(jenkins32(w[i])), jv);
+        const uint64_t t = lane_mul_64x32(key * static_cast<uint64_t>(jenkins32_lane(w[i])), jv);
         r = t < r ? t : r;
       }
     }
@@ -1201,7 +1201,7 @@ detect_kernel(const int32_t* __restrict__ tokens, int64_t N, int64_t L, int64_t 
           uint64_t kj[kChunk];
 #pragma unroll
           for (int c = 0; c < kChunk; ++c) {
-            jv[c] = jenkins32(v[c]);
+            jv[c] = jenkins32_lane(v[c]);
             kj[c] = lane_mul_64x32(key, jv[c]);
           }
           const uint32_t p0 = *reinterpret_cast<const uint32_t*>(pass_w);
