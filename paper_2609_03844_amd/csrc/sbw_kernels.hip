@@ -73,6 +73,15 @@ namespace {
 #ifndef SBW_SELF_SALT_NARROW
 #define SBW_SELF_SALT_NARROW 1
 #endif
+// Self-salt fp32, width 1: the split-term slab kernel when it makes at least
+// SBW_SLAB_MIN_GROUPS workgroups (below that its long-lived waves leave the chip
+// underfilled and the row-group kernel is faster).  0 = off.
+#ifndef SBW_SELF_SALT_SLAB
+#define SBW_SELF_SALT_SLAB 1
+#endif
+#ifndef SBW_SLAB_MIN_GROUPS
+#define SBW_SLAB_MIN_GROUPS 2000
+#endif
 #ifndef SBW_SELF_SALT_MIN_GROUPS
 #define SBW_SELF_SALT_MIN_GROUPS 1024  // 2048 measured 5 % slower for B * V of 5-10 M logits
 #endif
@@ -385,6 +394,219 @@ watermark_ss_rows_kernel(T* __restrict__ logits, int64_t row_stride, uint32_t V,
       if (g2 >= groups) break;
       g = g2;
     }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Self-salt watermark, fp32, window of one token, by split terms over a slab of
+// rows.  The seed of (row, v) is the smaller of the row term key*J(p)*J(v) and the
+// self term key*J(v)*J(v) (Sec. 2.3 with the window {p, v}); the self term, and so
+// the draw whenever it is the smaller one (about half of the pairs), is the same in
+// every row.  A wave owns 256 columns (one 16-byte vector per lane) of a slab of up
+// to kSlabRows rows:
+//  1. each lane draws its four columns' self-term blocks once and writes those
+//     decisions into the slab's decision map (a byte per row and column, a lane's
+//     four columns in one word) for every row;
+//  2. one word position q at a time, the lanes whose row term is smaller append
+//     (row term, map word, lane) to the wave's queue (ballot + mbcnt give
+//     consecutive entries), and a queue holding 64 pairs is drained at once: 64
+//     Philox draws side by side, each decision written over its map byte; the last
+//     partial chunk is drained after the slab's last row;
+//  3. each row's vector is biased from its map word and stored.
+// The Philox word is a compile-time choice in every draw (q is a template
+// argument), so each block keeps only the work its word needs.  Per logit this
+// draws about 0.57 blocks instead of 1; the queueing costs about 11 instructions.
+// ---------------------------------------------------------------------------
+constexpr int kSlabRows = 12;          // rows of a slab
+constexpr uint32_t kSlabQueue = 128;   // queue entries: fewer than 64 left + one row's 64
+// Map words per row: one more than the lanes, so that the same lane's words in
+// adjacent rows fall in different LDS banks.
+constexpr uint32_t kSlabMapStride = 65;
+constexpr int kSlabLoadRows = 4;       // rows whose logits are loaded together in step 3
+
+// l + delta where bit `bit` of `bits` is set, l's own bits elsewhere: the bit widened
+// to a full mask by a sign-extending field extract, then a bitwise select.
+__device__ __forceinline__ float bias_bit(float l, float delta, uint32_t bits, int bit) {
+  const uint32_t m = static_cast<uint32_t>(__builtin_amdgcn_sbfe(static_cast<int>(bits), bit, 1));
+  return __uint_as_float(
+      __builtin_amdgcn_bitop3_b32(m, __float_as_uint(l + delta), __float_as_uint(l), 0xCA));
+}
+
+template <int kQ>
+__device__ __forceinline__ uint32_t word_of(const Block& b) {
+  return kQ == 0 ? b.w0 : kQ == 1 ? b.w1 : kQ == 2 ? b.w2 : b.w3;
+}
+
+// A queued pair: the row term (the Philox key, two words), its map word and the lane
+// that queued it; one 16-byte record, one address and one LDS operation each way.
+typedef uint32_t SlabEntry __attribute__((ext_vector_type(4)));
+
+// One wave's LDS: the queue, the decision map, and each row's key * J(p).
+struct SlabLds {
+  SlabEntry queue[kSlabQueue];
+  uint32_t map[kSlabRows * kSlabMapStride];
+  alignas(16) uint64_t kjp[kSlabRows + 2];  // two spares for the read-ahead
+};
+
+// Draws the first n (<= 64) queue entries of word position q, one per lane, writes
+// each decision over its map byte, and moves entries 64 .. pending-1 to the front.
+// Lanes past n read entries inside the queue and store nothing.
+template <int kQ>
+__device__ __forceinline__ void slab_drain(SlabLds& s, uint32_t n, uint32_t pending,
+                                           uint32_t lane, uint32_t jid0, uint32_t tm1) {
+  const SlabEntry e = s.queue[lane];
+  SlabEntry e2 = SlabEntry{0u, 0u, 0u, 0u};
+  const bool move = lane + 64u < pending;
+  if (move) e2 = s.queue[lane + 64u];
+  // the pair's column is 4 * (jid0 + lane that queued it) + q
+  const uint32_t x = word_of<kQ>(philox_block_lane<6>(jid0 + e.w, Key{e.x, e.y}));
+  if (lane < n)
+    reinterpret_cast<uint8_t*>(s.map)[4u * e.z + kQ] = static_cast<uint8_t>(is_green(x, tm1));
+  if (move) s.queue[lane] = e2;
+}
+
+// Queues the pairs of one row and word position q whose row term kjp * J(v) is below
+// `bound`, and drains the queue when it holds 64.
+template <int kQ>
+__device__ __forceinline__ void slab_enqueue(SlabLds& s, uint32_t& pending, uint64_t kjp,
+                                             uint32_t jv, uint64_t bound, uint32_t map_word,
+                                             uint32_t lane, uint32_t jid0, uint32_t tm1) {
+  const uint64_t t = lane_mul_64x32(kjp, jv);
+  // the lanes with t < bound, as one wave mask (the compiler shares the compare
+  // with the branch below)
+  const uint64_t mask = __builtin_amdgcn_uicmpl(t, bound, 36 /* unsigned less than */);
+  if (t < bound) {
+    const uint32_t at = pending + __builtin_amdgcn_mbcnt_hi(
+                                      static_cast<uint32_t>(mask >> 32),
+                                      __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(mask), 0u));
+    s.queue[at] = SlabEntry{static_cast<uint32_t>(t), static_cast<uint32_t>(t >> 32), map_word, lane};
+  }
+  pending += static_cast<uint32_t>(__builtin_popcountll(mask));
+  // LDS operations of one wave complete in order; the barriers only keep the
+  // compiler from moving them across the passes.
+  __builtin_amdgcn_wave_barrier();
+  if (pending >= 64u) {
+    slab_drain<kQ>(s, 64u, pending, lane, jid0, tm1);
+    pending -= 64u;
+    __builtin_amdgcn_wave_barrier();
+  }
+}
+
+// Word position q over the rows of the slab: queue, drain at 64, drain the rest.
+template <int kQ>
+__device__ __forceinline__ void slab_position(SlabLds& s, int rows, uint32_t jv, uint64_t bound,
+                                              uint32_t lane, uint32_t jid0, uint32_t tm1) {
+  uint32_t pending = 0u;  // wave-uniform
+  // two rows per iteration; their key * J(p) by one broadcast LDS read, the next
+  // pair's read ahead (entries past the last row are spares: read, never used)
+  typedef uint64_t u64x2 __attribute__((ext_vector_type(2)));
+  u64x2 kjp = *reinterpret_cast<const u64x2*>(&s.kjp[0]);
+  int r = 0;
+#pragma nounroll
+  for (; r + 1 < rows; r += 2) {
+    const u64x2 next = *reinterpret_cast<const u64x2*>(&s.kjp[r + 2]);
+    const uint32_t w0 = static_cast<uint32_t>(r) * kSlabMapStride + lane;
+    slab_enqueue<kQ>(s, pending, kjp.x, jv, bound, w0, lane, jid0, tm1);
+    slab_enqueue<kQ>(s, pending, kjp.y, jv, bound, w0 + kSlabMapStride, lane, jid0, tm1);
+    kjp = next;
+  }
+  if (r < rows)
+    slab_enqueue<kQ>(s, pending, kjp.x, jv, bound, static_cast<uint32_t>(r) * kSlabMapStride + lane,
+                     lane, jid0, tm1);
+  if (pending != 0u) slab_drain<kQ>(s, pending, pending, lane, jid0, tm1);
+  __builtin_amdgcn_wave_barrier();
+}
+
+// Grid: x = tile of kThreads vectors (4 waves of 256 columns), y = a slot taking the
+// slabs y, y + gridDim.y, ... of kSlabRows rows.  Rows 16-byte aligned; vbase a
+// multiple of 4.
+__global__ void __launch_bounds__(kThreads)
+watermark_ss_slab_kernel(float* __restrict__ logits, int64_t row_stride, uint32_t V, int64_t B,
+                         const int32_t* __restrict__ context, uint64_t key, uint32_t tm1,
+                         float delta, uint32_t vbase) {
+  __shared__ SlabLds lds[kThreads / 64];
+  const uint32_t lane = threadIdx.x & 63u;
+  const uint32_t wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  SlabLds& s = lds[wave];
+  const uint32_t full = V / 4u;
+  const uint32_t tail = V % 4u;
+  const uint32_t j0 = blockIdx.x * kThreads + wave * 64u;  // the wave's first vector
+  const uint32_t j = j0 + lane;
+  const bool active = j < full;
+  const uint32_t jid0 = j0 + vbase / 4u;  // in token ids / 4: the Philox counter
+  const uint32_t jid = jid0 + lane;
+  // the lane's four columns: J(v), and the self term as the queueing bound (0, which no
+  // row term is below, for a lane past the row's last whole vector)
+  uint32_t jv[4];
+  uint64_t bound[4];
+  uint32_t self_word;
+  {
+    uint64_t self[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      jv[q] = jenkins32((jid << 2) | static_cast<uint32_t>(q));
+      self[q] = mul_64x64(key, wide_mul(jv[q], jv[q]));
+      bound[q] = active ? self[q] : 0u;
+    }
+    self_word = static_cast<uint32_t>(
+                    is_green(word_of<0>(philox_block_lane<6>(jid, key_of(self[0]))), tm1)) |
+                static_cast<uint32_t>(
+                    is_green(word_of<1>(philox_block_lane<6>(jid, key_of(self[1]))), tm1)) << 8 |
+                static_cast<uint32_t>(
+                    is_green(word_of<2>(philox_block_lane<6>(jid, key_of(self[2]))), tm1)) << 16 |
+                static_cast<uint32_t>(
+                    is_green(word_of<3>(philox_block_lane<6>(jid, key_of(self[3]))), tm1)) << 24;
+  }
+  const int64_t slabs = (B + kSlabRows - 1) / kSlabRows;
+  for (int64_t g = blockIdx.y; g < slabs; g += gridDim.y) {
+    const int64_t row0 = g * kSlabRows;
+    const int rows = static_cast<int>(B - row0 < kSlabRows ? B - row0 : kSlabRows);
+    // step 1: the self decisions for every row, and each row's key * J(p)
+#pragma nounroll
+    for (int r = 0; r < rows; ++r) s.map[static_cast<uint32_t>(r) * kSlabMapStride + lane] = self_word;
+    if (lane < static_cast<uint32_t>(rows))
+      s.kjp[lane] = key * static_cast<uint64_t>(jenkins32(static_cast<uint32_t>(context[row0 + lane])));
+    __builtin_amdgcn_wave_barrier();
+    // step 2: the pairs whose row term is smaller, one word position at a time
+    slab_position<0>(s, rows, jv[0], bound[0], lane, jid0, tm1);
+    slab_position<1>(s, rows, jv[1], bound[1], lane, jid0, tm1);
+    slab_position<2>(s, rows, jv[2], bound[2], lane, jid0, tm1);
+    slab_position<3>(s, rows, jv[3], bound[3], lane, jid0, tm1);
+    // step 3: bias and store, kSlabLoadRows rows' loads in flight at a time
+    if (active) {
+      for (int r0 = 0; r0 < rows; r0 += kSlabLoadRows) {
+        f32x4 buf[kSlabLoadRows];
+        uint32_t dec[kSlabLoadRows];
+#pragma unroll
+        for (int k = 0; k < kSlabLoadRows; ++k) {
+          if (r0 + k < rows) {
+            buf[k] = stream_load(reinterpret_cast<const f32x4*>(logits + (row0 + r0 + k) * row_stride) + j);
+            dec[k] = s.map[static_cast<uint32_t>(r0 + k) * kSlabMapStride + lane];
+          }
+        }
+#pragma unroll
+        for (int k = 0; k < kSlabLoadRows; ++k) {
+          if (r0 + k < rows) {
+            f32x4 o = buf[k];
+            o.x = bias_bit(o.x, delta, dec[k], 0);
+            o.y = bias_bit(o.y, delta, dec[k], 8);
+            o.z = bias_bit(o.z, delta, dec[k], 16);
+            o.w = bias_bit(o.w, delta, dec[k], 24);
+            stream_store(reinterpret_cast<f32x4*>(logits + (row0 + r0 + k) * row_stride) + j, o);
+          }
+        }
+      }
+    }
+    // the rows' partial last vector, by lane 0 of the wave that covers it
+    if (tail != 0u && lane == 0u && full >= j0 && full - j0 < 64u) {
+      for (int r = 0; r < rows; ++r) {
+        const RowSeed<1> rs = row_seed<kSelfSalt, 1>(key, context + row0 + r, 1);
+        for (uint32_t e = 0; e < tail; ++e)
+          bias_one<float, kSelfSalt>(logits + (row0 + r) * row_stride, full * 4u + e, rs, tm1,
+                                     delta, vbase);
+      }
+    }
+    __builtin_amdgcn_wave_barrier();  // the next slab rewrites the map
   }
 }
 
@@ -1404,6 +1626,16 @@ void launch_watermark(void* logits, int64_t B, uint32_t V, int64_t row_stride,
     const uint64_t vectors = (static_cast<uint64_t>(V) + kPer - 1) / kPer;
     const uint32_t tiles = static_cast<uint32_t>((vectors + kThreads * kU - 1) / (kThreads * kU));
     if constexpr (kSeeding == kSelfSalt) {
+      if constexpr (SBW_SELF_SALT_SLAB && kW == 1 && std::is_same<T, float>::value) {
+        const uint32_t tiles1 = static_cast<uint32_t>((vectors + kThreads - 1) / kThreads);
+        const int64_t slabs = (B + kSlabRows - 1) / kSlabRows;
+        if (static_cast<int64_t>(tiles1) * slabs >= int64_t{SBW_SLAB_MIN_GROUPS}) {
+          const dim3 grid(tiles1, static_cast<uint32_t>(slabs < kMaxGridY ? slabs : kMaxGridY));
+          hipLaunchKernelGGL(watermark_ss_slab_kernel, grid, dim3(kThreads), 0, stream, p,
+                             row_stride, V, B, context, key, tm1, delta, vbase);
+          return;
+        }
+      }
       constexpr int kMaxRows = kW > 1 ? 1 : (sizeof(T) == 4 ? 4 : 2);
       const int64_t work = static_cast<int64_t>(tiles) * B;
       if constexpr (SBW_SELF_SALT_NARROW && kMaxRows == 4 && kU > 1) {

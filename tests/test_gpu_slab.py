@@ -1,0 +1,130 @@
+"""GPU parity of the self-salt split-term slab kernel (fp32, window of one token).
+
+Large fp32 self-salt launches take a kernel that draws each column's self-term block
+once per slab of 12 rows and queues in LDS only the (row, token) pairs whose row term
+is the smaller one.  Every case here is sized to take that kernel (the launch rule is
+mirrored in `takes_slab` and asserted), and is compared with the oracle bit for bit:
+  * slabs cut short (B not a multiple of 12), a row tail (V mod 4 != 0), the last
+    workgroup tile partly past the row, padded rows;
+  * special values (NaNs with payloads, infinities, signed zeros, subnormals);
+  * gamma from tiny to 1 (every token green), both key shapes, both signs of delta;
+  * a vocabulary shard whose first token id is a multiple of 4, as one of 8
+    tensor-parallel heads of the 152064-token vocabulary holds it;
+  * two launches back to back, the second smaller (nothing a launch leaves in LDS
+    changes the next one).
+The c4 configurations at full size (B = 256 and 1024) take this kernel too and are
+checked in test_gpu_parity.py.
+"""
+import numpy as np
+import pytest
+
+import oracle
+from test_gpu_parity import (KEY, WIDE, _from_device, _to_device, assert_logits_equal, env,  # noqa: F401
+                             say, special_logits)
+
+pytestmark = pytest.mark.gpu
+
+SLAB_ROWS = 12
+MIN_GROUPS = 2000   # workgroups below which the row-group kernel is taken
+
+
+def takes_slab(B, V):
+    """The launch rule of the fp32 self-salt watermark (rows 16-byte aligned)."""
+    tiles = -(-(-(-V // 4)) // 256)
+    return tiles * -(-B // SLAB_ROWS) >= MIN_GROUPS
+
+
+def run(env, x, prev, key, gamma, delta, stride=None, v_offset=None):
+    torch, sbw, dev = env
+    B, V = x.shape
+    if stride is None:
+        t = _to_device(torch, dev, x)
+        view = t
+    else:
+        t = torch.zeros((B, stride), dtype=torch.float32, device=dev)
+        t[:, :V] = _to_device(torch, dev, x)
+        view = t[:, :V]
+    p = torch.from_numpy(prev).to(dev)
+    if v_offset is None:
+        sbw.watermark(view, p, key, gamma, delta, "self_salt")
+    else:
+        sbw.watermark_shard(view, p, v_offset, key, gamma, delta, "self_salt")
+    torch.cuda.synchronize()
+    out = _from_device(torch, t)
+    return out if stride is None else out[:, :V], (None if stride is None else out[:, V:])
+
+
+@pytest.mark.parametrize("B,V,stride", [
+    (3001, 8195, None),      # slab of 1 row at the end, V mod 4 = 3, 2049 vectors (tile of 1)
+    (2400, 10241, 10248),    # whole slabs, padded rows, V mod 4 = 1
+    (1417, 16386, None),     # V mod 4 = 2, last tile partly past the row
+    (605, 40000, 40004),     # whole vectors, padded rows, slab of 5 rows at the end
+])
+def test_slab_shapes(env, B, V, stride):
+    assert takes_slab(B, V)
+    rng = np.random.default_rng(77 + B + V)
+    x = special_logits(rng, B, V, "f32")
+    prev = rng.integers(0, 1 << 31, B).astype(np.int32)
+    prev[:3] = [0, -1, 2**31 - 1]
+    say(f"slab shapes B={B} V={V} stride={stride}")
+    got, pad = run(env, x, prev, WIDE, 0.25, 2.0, stride)
+    assert_logits_equal(got, oracle.watermark(x, prev, WIDE, 0.25, 2.0, "self_salt"),
+                        f"B={B} V={V}")
+    if pad is not None:
+        assert not pad.any(), "the padding columns were written"
+
+
+@pytest.mark.parametrize("gamma,delta,key", [
+    (0.25, 2.0, KEY),
+    (0.5, -3.0, WIDE),
+    (1e-9, 8.0, WIDE),       # almost no token green
+    (1.0 - 1e-10, 1.0, KEY),
+    (1.0, 4.0, WIDE),        # every token green
+])
+def test_slab_parameters(env, gamma, delta, key):
+    B, V = 1850, 12292
+    assert takes_slab(B, V)
+    rng = np.random.default_rng(int(gamma * 1e6) + int(delta * 10) + 5)
+    x = rng.standard_normal((B, V)).astype(np.float32)
+    prev = rng.integers(0, V, B).astype(np.int32)
+    say(f"slab parameters gamma={gamma} delta={delta}")
+    got, _ = run(env, x, prev, key, gamma, delta)
+    assert_logits_equal(got, oracle.watermark(x, prev, key, gamma, delta, "self_salt"),
+                        f"gamma={gamma} delta={delta}")
+
+
+def test_slab_shard(env):
+    """Columns [57024, 57024 + 19008) of a 152064-token vocabulary (one of 8 shards) at
+    B = 1300: token ids from 57024, the draws those of the full row."""
+    a, n, V, B = 57024, 19008, 152064, 1300
+    assert takes_slab(B, n)
+    rng = np.random.default_rng(4242)
+    x = rng.standard_normal((B, n)).astype(np.float32) * np.float32(3)
+    prev = rng.integers(0, V, B).astype(np.int32)
+    say("slab shard 57024+19008, B=1300")
+    got, _ = run(env, x, prev, WIDE, 0.25, 2.0, v_offset=a)
+    # the oracle's membership of tokens a .. a+n-1 in each row, and its fp32 bias
+    green = oracle.is_green_many(WIDE, np.repeat(prev, n), np.tile(np.arange(a, a + n), B), 0.25,
+                                 "self_salt").reshape(B, n)
+    expect = np.where(green, oracle.bias_f32_many(x, 2.0), x)
+    assert_logits_equal(got, expect, "shard")
+
+
+def test_slab_twice_in_a_row(env):
+    """Two launches back to back, the second smaller, on fresh inputs each: nothing a
+    launch leaves in LDS or in the logits changes the next one's result."""
+    rng = np.random.default_rng(99)
+    for B, V in ((2000, 12300), (1900, 12299)):
+        assert takes_slab(B, V)
+        x = rng.standard_normal((B, V)).astype(np.float32)
+        prev = rng.integers(0, V, B).astype(np.int32)
+        say(f"slab twice B={B} V={V}")
+        got, _ = run(env, x, prev, KEY, 0.25, 2.0)
+        assert_logits_equal(got, oracle.watermark(x, prev, KEY, 0.25, 2.0, "self_salt"),
+                            f"B={B} V={V}")
+
+
+def test_launch_rule_cases():
+    """The c4 configurations take the slab kernel; c3 and small batches do not."""
+    assert takes_slab(256, 152064) and takes_slab(1024, 152064)
+    assert not takes_slab(64, 128256) and not takes_slab(16, 152064)
