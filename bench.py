@@ -21,9 +21,12 @@ after the timed region brackets single launches with events for p50/p95/p99.
 `value` is the self-salt watermark throughput in Gelem/s (B*V / mean launch
 time), the configuration the metric names.  `roofline` is that kernel's, against
 the Philox4x32-10 roof (derived from issue slots, and measured in the same run by
-the probe library libsbw_rate.so at the clock the chip runs); `roofline.hbm_context`
-is the context-seeded launch at the same shape, the HBM-bound one.  All inputs are
-synthetic and resident in HBM before the timed region starts.
+the probe library libsbw_rate.so at the clock the chip runs), counting the work as
+the method defines it: one Philox block per logit (the split-term kernel that runs
+at this shape draws about 0.57 per logit, so its rate in those units can pass the
+roof of the blocks it does draw).  `roofline.hbm_context` is the context-seeded
+launch at the same shape, the HBM-bound one.  All inputs are synthetic and resident
+in HBM before the timed region starts.
 """
 from __future__ import annotations
 
@@ -856,13 +859,14 @@ def main():
         "watermark": {"self_salt": ss, "context": ctx},
         "detect": {"self_salt": det_stats("det_self_salt"), "context": det_stats("det_context")},
         "roofline": {
-            "bound": "alu", "kernel": "watermark_ss_rows_kernel<float> (self-salt)",
+            "bound": "alu", "kernel": "watermark_ss_slab_kernel (self-salt, split terms)",
             "achieved": ss_blocks, "peak": PHILOX_PEAK_GBLOCKS,
             "unit": "G Philox4x32-10 blocks/s", "frac": ss_blocks / PHILOX_PEAK_GBLOCKS,
-            "traffic": traffic_of("sbw::watermark_ss_rows_kernel<float,"),
+            "traffic": traffic_of("sbw::watermark_ss_slab_kernel"),
             "us_per_launch": ss["us_mean"],
-            "algorithmic_per_launch": f"{elems} Philox blocks (one per logit), "
-                                      f"{bytes_wm} HBM bytes",
+            "algorithmic_per_launch": f"{elems} Philox blocks (one per logit, as the method "
+                                      f"defines the draw; the kernel draws about 0.57 per "
+                                      f"logit), {bytes_wm} HBM bytes",
             "peak_basis": ("38 issue slots per block (18 products at one per lane per clock, "
                            "40 adds and xors at two per slot), 256 CUs x 64 lanes x 2.4 GHz"),
             "peak_measured": roof["gblocks_per_s"],
