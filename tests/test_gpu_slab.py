@@ -11,7 +11,8 @@ mirrored in `takes_slab` and asserted), and is compared with the oracle bit for 
   * a vocabulary shard whose first token id is a multiple of 4, as one of 8
     tensor-parallel heads of the 152064-token vocabulary holds it;
   * two launches back to back, the second smaller (nothing a launch leaves in LDS
-    changes the next one).
+    changes the next one);
+  * more slabs than the grid's y dimension holds (workgroups that take two).
 The c4 configurations at full size (B = 256 and 1024) take this kernel too and are
 checked in test_gpu_parity.py.
 """
@@ -122,6 +123,20 @@ def test_slab_twice_in_a_row(env):
         got, _ = run(env, x, prev, KEY, 0.25, 2.0)
         assert_logits_equal(got, oracle.watermark(x, prev, KEY, 0.25, 2.0, "self_salt"),
                             f"B={B} V={V}")
+
+
+def test_slab_grid_stride(env):
+    """More slabs than the 65535 workgroups of the grid's y dimension: some workgroups
+    take a second slab (and 800003 rows of 6 logits: a 2-logit row tail, a last slab of
+    11 rows)."""
+    B, V = 800003, 6
+    assert takes_slab(B, V) and -(-B // SLAB_ROWS) > 65535
+    rng = np.random.default_rng(5150)
+    x = rng.standard_normal((B, V)).astype(np.float32)
+    prev = rng.integers(0, 1 << 20, B).astype(np.int32)
+    say(f"slab grid stride B={B} V={V}")
+    got, _ = run(env, x, prev, WIDE, 0.25, 2.0)
+    assert_logits_equal(got, oracle.watermark(x, prev, WIDE, 0.25, 2.0, "self_salt"), "grid stride")
 
 
 def test_launch_rule_cases():
