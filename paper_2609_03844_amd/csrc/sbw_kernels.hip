@@ -74,8 +74,9 @@ namespace {
 #define SBW_SELF_SALT_NARROW 1
 #endif
 // Self-salt fp32, width 1: the split-term slab kernel when it makes at least
-// SBW_SLAB_MIN_GROUPS workgroups (below that its long-lived waves leave the chip
-// underfilled and the row-group kernel is faster).  0 = off.
+// SBW_SLAB_MIN_GROUPS workgroups with 12-row slabs, else with 8-row slabs (below that
+// its long-lived waves leave the chip underfilled and the row-group kernel is
+// faster).  0 = off.
 #ifndef SBW_SELF_SALT_SLAB
 #define SBW_SELF_SALT_SLAB 1
 #endif
@@ -403,7 +404,8 @@ watermark_ss_rows_kernel(T* __restrict__ logits, int64_t row_stride, uint32_t V,
 // self term key*J(v)*J(v) (Sec. 2.3 with the window {p, v}); the self term, and so
 // the draw whenever it is the smaller one (about half of the pairs), is the same in
 // every row.  A wave owns 256 columns (one 16-byte vector per lane) of a slab of up
-// to kSlabRows rows:
+// to kRows rows (12, or 8 for launches that 12-row slabs would leave with too few
+// workgroups):
 //  1. each lane draws its four columns' self-term blocks once and writes those
 //     decisions into the slab's decision map (a byte per row and column, a lane's
 //     four columns in one word) for every row;
@@ -417,7 +419,6 @@ watermark_ss_rows_kernel(T* __restrict__ logits, int64_t row_stride, uint32_t V,
 // argument), so each block keeps only the work its word needs.  Per logit this
 // draws about 0.57 blocks instead of 1; the queueing costs about 11 instructions.
 // ---------------------------------------------------------------------------
-constexpr int kSlabRows = 12;          // rows of a slab
 constexpr uint32_t kSlabQueue = 128;   // queue entries: fewer than 64 left + one row's 64
 // Map words per row: one more than the lanes, so that the same lane's words in
 // adjacent rows fall in different LDS banks.
@@ -442,17 +443,18 @@ __device__ __forceinline__ uint32_t word_of(const Block& b) {
 typedef uint32_t SlabEntry __attribute__((ext_vector_type(4)));
 
 // One wave's LDS: the queue, the decision map, and each row's key * J(p).
+template <int kRows>
 struct SlabLds {
   SlabEntry queue[kSlabQueue];
-  uint32_t map[kSlabRows * kSlabMapStride];
-  alignas(16) uint64_t kjp[kSlabRows + 2];  // two spares for the read-ahead
+  uint32_t map[kRows * kSlabMapStride];
+  alignas(16) uint64_t kjp[kRows + 2];  // two spares for the read-ahead
 };
 
 // Draws the first n (<= 64) queue entries of word position q, one per lane, writes
 // each decision over its map byte, and moves entries 64 .. pending-1 to the front.
 // Lanes past n read entries inside the queue and store nothing.
-template <int kQ>
-__device__ __forceinline__ void slab_drain(SlabLds& s, uint32_t n, uint32_t pending,
+template <int kQ, int kRows>
+__device__ __forceinline__ void slab_drain(SlabLds<kRows>& s, uint32_t n, uint32_t pending,
                                            uint32_t lane, uint32_t jid0, uint32_t tm1) {
   const SlabEntry e = s.queue[lane];
   SlabEntry e2 = SlabEntry{0u, 0u, 0u, 0u};
@@ -467,8 +469,8 @@ __device__ __forceinline__ void slab_drain(SlabLds& s, uint32_t n, uint32_t pend
 
 // Queues the pairs of one row and word position q whose row term kjp * J(v) is below
 // `bound`, and drains the queue when it holds 64.
-template <int kQ>
-__device__ __forceinline__ void slab_enqueue(SlabLds& s, uint32_t& pending, uint64_t kjp,
+template <int kQ, int kRows>
+__device__ __forceinline__ void slab_enqueue(SlabLds<kRows>& s, uint32_t& pending, uint64_t kjp,
                                              uint32_t jv, uint64_t bound, uint32_t map_word,
                                              uint32_t lane, uint32_t jid0, uint32_t tm1) {
   const uint64_t t = lane_mul_64x32(kjp, jv);
@@ -486,15 +488,15 @@ __device__ __forceinline__ void slab_enqueue(SlabLds& s, uint32_t& pending, uint
   // compiler from moving them across the passes.
   __builtin_amdgcn_wave_barrier();
   if (pending >= 64u) {
-    slab_drain<kQ>(s, 64u, pending, lane, jid0, tm1);
+    slab_drain<kQ, kRows>(s, 64u, pending, lane, jid0, tm1);
     pending -= 64u;
     __builtin_amdgcn_wave_barrier();
   }
 }
 
 // Word position q over the rows of the slab: queue, drain at 64, drain the rest.
-template <int kQ>
-__device__ __forceinline__ void slab_position(SlabLds& s, int rows, uint32_t jv, uint64_t bound,
+template <int kQ, int kRows>
+__device__ __forceinline__ void slab_position(SlabLds<kRows>& s, int rows, uint32_t jv, uint64_t bound,
                                               uint32_t lane, uint32_t jid0, uint32_t tm1) {
   uint32_t pending = 0u;  // wave-uniform
   // two rows per iteration; their key * J(p) by one broadcast LDS read, the next
@@ -506,28 +508,29 @@ __device__ __forceinline__ void slab_position(SlabLds& s, int rows, uint32_t jv,
   for (; r + 1 < rows; r += 2) {
     const u64x2 next = *reinterpret_cast<const u64x2*>(&s.kjp[r + 2]);
     const uint32_t w0 = static_cast<uint32_t>(r) * kSlabMapStride + lane;
-    slab_enqueue<kQ>(s, pending, kjp.x, jv, bound, w0, lane, jid0, tm1);
-    slab_enqueue<kQ>(s, pending, kjp.y, jv, bound, w0 + kSlabMapStride, lane, jid0, tm1);
+    slab_enqueue<kQ, kRows>(s, pending, kjp.x, jv, bound, w0, lane, jid0, tm1);
+    slab_enqueue<kQ, kRows>(s, pending, kjp.y, jv, bound, w0 + kSlabMapStride, lane, jid0, tm1);
     kjp = next;
   }
   if (r < rows)
-    slab_enqueue<kQ>(s, pending, kjp.x, jv, bound, static_cast<uint32_t>(r) * kSlabMapStride + lane,
-                     lane, jid0, tm1);
-  if (pending != 0u) slab_drain<kQ>(s, pending, pending, lane, jid0, tm1);
+    slab_enqueue<kQ, kRows>(s, pending, kjp.x, jv, bound,
+                            static_cast<uint32_t>(r) * kSlabMapStride + lane, lane, jid0, tm1);
+  if (pending != 0u) slab_drain<kQ, kRows>(s, pending, pending, lane, jid0, tm1);
   __builtin_amdgcn_wave_barrier();
 }
 
 // Grid: x = tile of kThreads vectors (4 waves of 256 columns), y = a slot taking the
-// slabs y, y + gridDim.y, ... of kSlabRows rows.  Rows 16-byte aligned; vbase a
-// multiple of 4.
+// slabs y, y + gridDim.y, ... of kRows rows.  Rows 16-byte aligned; vbase a multiple
+// of 4.
+template <int kRows>
 __global__ void __launch_bounds__(kThreads)
 watermark_ss_slab_kernel(float* __restrict__ logits, int64_t row_stride, uint32_t V, int64_t B,
                          const int32_t* __restrict__ context, uint64_t key, uint32_t tm1,
                          float delta, uint32_t vbase) {
-  __shared__ SlabLds lds[kThreads / 64];
+  __shared__ SlabLds<kRows> lds[kThreads / 64];
   const uint32_t lane = threadIdx.x & 63u;
   const uint32_t wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  SlabLds& s = lds[wave];
+  SlabLds<kRows>& s = lds[wave];
   const uint32_t full = V / 4u;
   const uint32_t tail = V % 4u;
   const uint32_t j0 = blockIdx.x * kThreads + wave * 64u;  // the wave's first vector
@@ -557,10 +560,10 @@ watermark_ss_slab_kernel(float* __restrict__ logits, int64_t row_stride, uint32_
                 static_cast<uint32_t>(
                     is_green(word_of<3>(philox_block_lane<6>(jid, key_of(self[3]))), tm1)) << 24;
   }
-  const int64_t slabs = (B + kSlabRows - 1) / kSlabRows;
+  const int64_t slabs = (B + kRows - 1) / kRows;
   for (int64_t g = blockIdx.y; g < slabs; g += gridDim.y) {
-    const int64_t row0 = g * kSlabRows;
-    const int rows = static_cast<int>(B - row0 < kSlabRows ? B - row0 : kSlabRows);
+    const int64_t row0 = g * kRows;
+    const int rows = static_cast<int>(B - row0 < kRows ? B - row0 : kRows);
     // step 1: the self decisions for every row, and each row's key * J(p)
 #pragma nounroll
     for (int r = 0; r < rows; ++r) s.map[static_cast<uint32_t>(r) * kSlabMapStride + lane] = self_word;
@@ -568,10 +571,10 @@ watermark_ss_slab_kernel(float* __restrict__ logits, int64_t row_stride, uint32_
       s.kjp[lane] = key * static_cast<uint64_t>(jenkins32(static_cast<uint32_t>(context[row0 + lane])));
     __builtin_amdgcn_wave_barrier();
     // step 2: the pairs whose row term is smaller, one word position at a time
-    slab_position<0>(s, rows, jv[0], bound[0], lane, jid0, tm1);
-    slab_position<1>(s, rows, jv[1], bound[1], lane, jid0, tm1);
-    slab_position<2>(s, rows, jv[2], bound[2], lane, jid0, tm1);
-    slab_position<3>(s, rows, jv[3], bound[3], lane, jid0, tm1);
+    slab_position<0, kRows>(s, rows, jv[0], bound[0], lane, jid0, tm1);
+    slab_position<1, kRows>(s, rows, jv[1], bound[1], lane, jid0, tm1);
+    slab_position<2, kRows>(s, rows, jv[2], bound[2], lane, jid0, tm1);
+    slab_position<3, kRows>(s, rows, jv[3], bound[3], lane, jid0, tm1);
     // step 3: bias and store, kSlabLoadRows rows' loads in flight at a time
     if (active) {
       for (int r0 = 0; r0 < rows; r0 += kSlabLoadRows) {
@@ -1628,10 +1631,16 @@ void launch_watermark(void* logits, int64_t B, uint32_t V, int64_t row_stride,
     if constexpr (kSeeding == kSelfSalt) {
       if constexpr (SBW_SELF_SALT_SLAB && kW == 1 && std::is_same<T, float>::value) {
         const uint32_t tiles1 = static_cast<uint32_t>((vectors + kThreads - 1) / kThreads);
-        const int64_t slabs = (B + kSlabRows - 1) / kSlabRows;
-        if (static_cast<int64_t>(tiles1) * slabs >= int64_t{SBW_SLAB_MIN_GROUPS}) {
-          const dim3 grid(tiles1, static_cast<uint32_t>(slabs < kMaxGridY ? slabs : kMaxGridY));
-          hipLaunchKernelGGL(watermark_ss_slab_kernel, grid, dim3(kThreads), 0, stream, p,
+        const int64_t slabs12 = (B + 11) / 12, slabs8 = (B + 7) / 8;
+        if (static_cast<int64_t>(tiles1) * slabs12 >= int64_t{SBW_SLAB_MIN_GROUPS}) {
+          const dim3 grid(tiles1, static_cast<uint32_t>(slabs12 < kMaxGridY ? slabs12 : kMaxGridY));
+          hipLaunchKernelGGL((watermark_ss_slab_kernel<12>), grid, dim3(kThreads), 0, stream, p,
+                             row_stride, V, B, context, key, tm1, delta, vbase);
+          return;
+        }
+        if (static_cast<int64_t>(tiles1) * slabs8 >= int64_t{SBW_SLAB_MIN_GROUPS}) {
+          const dim3 grid(tiles1, static_cast<uint32_t>(slabs8 < kMaxGridY ? slabs8 : kMaxGridY));
+          hipLaunchKernelGGL((watermark_ss_slab_kernel<8>), grid, dim3(kThreads), 0, stream, p,
                              row_stride, V, B, context, key, tm1, delta, vbase);
           return;
         }

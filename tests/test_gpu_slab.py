@@ -1,9 +1,10 @@
 """GPU parity of the self-salt split-term slab kernel (fp32, window of one token).
 
 Large fp32 self-salt launches take a kernel that draws each column's self-term block
-once per slab of 12 rows and queues in LDS only the (row, token) pairs whose row term
-is the smaller one.  Every case here is sized to take that kernel (the launch rule is
-mirrored in `takes_slab` and asserted), and is compared with the oracle bit for bit:
+once per slab of 12 rows (8 for launches that 12-row slabs would leave with too few
+workgroups) and queues in LDS only the (row, token) pairs whose row term is the
+smaller one.  Every case here is sized to take that kernel (the launch rule is
+mirrored in `slab_rows` and asserted), and is compared with the oracle bit for bit:
   * slabs cut short (B not a multiple of 12), a row tail (V mod 4 != 0), the last
     workgroup tile partly past the row, padded rows;
   * special values (NaNs with payloads, infinities, signed zeros, subnormals);
@@ -26,13 +27,21 @@ from test_gpu_parity import (KEY, WIDE, _from_device, _to_device, assert_logits_
 pytestmark = pytest.mark.gpu
 
 SLAB_ROWS = 12
-MIN_GROUPS = 2000   # workgroups below which the row-group kernel is taken
+MIN_GROUPS = 2000   # workgroups below which the next slab height (or kernel) is taken
+
+
+def slab_rows(B, V):
+    """The launch rule of the fp32 self-salt watermark (rows 16-byte aligned): the slab
+    height the launch takes, or 0 for the row-group kernel."""
+    tiles = -(-(-(-V // 4)) // 256)
+    for rows in (12, 8):
+        if tiles * -(-B // rows) >= MIN_GROUPS:
+            return rows
+    return 0
 
 
 def takes_slab(B, V):
-    """The launch rule of the fp32 self-salt watermark (rows 16-byte aligned)."""
-    tiles = -(-(-(-V // 4)) // 256)
-    return tiles * -(-B // SLAB_ROWS) >= MIN_GROUPS
+    return slab_rows(B, V) == SLAB_ROWS
 
 
 def run(env, x, prev, key, gamma, delta, stride=None, v_offset=None):
@@ -139,7 +148,25 @@ def test_slab_grid_stride(env):
     assert_logits_equal(got, oracle.watermark(x, prev, WIDE, 0.25, 2.0, "self_salt"), "grid stride")
 
 
+@pytest.mark.parametrize("B,V", [
+    (128, 128256),    # whole 8-row slabs
+    (131, 128255),    # a last slab of 3 rows, V mod 4 = 3
+])
+def test_slab_eight_rows(env, B, V):
+    """Launches that 12-row slabs would leave with too few workgroups take 8-row ones."""
+    assert slab_rows(B, V) == 8
+    rng = np.random.default_rng(808 + B)
+    x = special_logits(rng, B, V, "f32")
+    prev = rng.integers(0, V, B).astype(np.int32)
+    say(f"slab 8 rows B={B} V={V}")
+    got, _ = run(env, x, prev, WIDE, 0.25, 2.0)
+    assert_logits_equal(got, oracle.watermark(x, prev, WIDE, 0.25, 2.0, "self_salt"),
+                        f"B={B} V={V}")
+
+
 def test_launch_rule_cases():
-    """The c4 configurations take the slab kernel; c3 and small batches do not."""
-    assert takes_slab(256, 152064) and takes_slab(1024, 152064)
-    assert not takes_slab(64, 128256) and not takes_slab(16, 152064)
+    """The c4 configurations take 12-row slabs, B = 128 of a 128256-token vocabulary
+    8-row ones; c3 and small batches take the row-group kernel."""
+    assert slab_rows(256, 152064) == 12 and slab_rows(1024, 152064) == 12
+    assert slab_rows(128, 128256) == 8
+    assert slab_rows(64, 128256) == 0 and slab_rows(16, 152064) == 0
