@@ -859,7 +859,7 @@ def main():
         "watermark": {"self_salt": ss, "context": ctx},
         "detect": {"self_salt": det_stats("det_self_salt"), "context": det_stats("det_context")},
         "roofline": {
-            "bound": "alu", "kernel": "watermark_ss_slab_kernel (self-salt, split terms)",
+            "bound": "alu", "kernel": "watermark_ss_slab_kernel<12> (self-salt, split terms)",
             "achieved": ss_blocks, "peak": PHILOX_PEAK_GBLOCKS,
             "unit": "G Philox4x32-10 blocks/s", "frac": ss_blocks / PHILOX_PEAK_GBLOCKS,
             "traffic": traffic_of("sbw::watermark_ss_slab_kernel"),
