@@ -7,7 +7,10 @@
 //             tokens, the context seed, key * J(p_i)) sit in scalar registers.
 //             Context seeding shares one Philox block between the 4 tokens of a
 //             counter; self-salt needs one block per token, and its workgroups
-//             share each candidate's hash and self term across up to 4 rows.
+//             share each candidate's hash and self term across up to 4 rows.  Large
+//             fp32 self-salt launches (window of one token) instead draw each
+//             column's self-term block once per slab of 12 or 8 rows and queue in
+//             LDS only the pairs whose row term is the smaller one (about half).
 // argmax      greedy decoding of the watermarked logits without writing them: one
 //             read of each logit, a per-segment (value, index) partial, a read-out
 //             kernel per row.  Colours are drawn only for logits that can still
