@@ -8,7 +8,7 @@
 //             Context seeding shares one Philox block between the 4 tokens of a
 //             counter; self-salt needs one block per token, and its workgroups
 //             share each candidate's hash and self term across up to 4 rows.  Large
-//             fp32 self-salt launches (window of one token) instead draw each
+//             self-salt launches (window of one token) instead draw each
 //             column's self-term block once per slab of 12 or 8 rows and queue in
 //             LDS only the pairs whose row term is the smaller one (about half).
 // argmax      greedy decoding of the watermarked logits without writing them: one
@@ -76,7 +76,7 @@ namespace {
 #ifndef SBW_SELF_SALT_NARROW
 #define SBW_SELF_SALT_NARROW 1
 #endif
-// Self-salt fp32, width 1: the split-term slab kernel when it makes at least
+// Self-salt, width 1 (fp32 and bf16): the split-term slab kernel when it makes at least
 // SBW_SLAB_MIN_GROUPS workgroups with 12-row slabs, else with 8-row slabs (below that
 // its long-lived waves leave the chip underfilled and the row-group kernel is
 // faster).  0 = off.
@@ -445,35 +445,39 @@ __device__ __forceinline__ uint32_t word_of(const Block& b) {
 // that queued it; one 16-byte record, one address and one LDS operation each way.
 typedef uint32_t SlabEntry __attribute__((ext_vector_type(4)));
 
-// One wave's LDS: the queue, the decision map, and each row's key * J(p).
-template <int kRows>
+// One wave's LDS: the queue, the decision map (kPer bytes per row and lane: the
+// decisions of a lane's kPer tokens), and each row's key * J(p).
+template <int kRows, int kPer>
 struct SlabLds {
   SlabEntry queue[kSlabQueue];
-  uint32_t map[kRows * kSlabMapStride];
+  uint32_t map[kRows * kSlabMapStride * (kPer / 4)];
   alignas(16) uint64_t kjp[kRows + 2];  // two spares for the read-ahead
 };
 
-// Draws the first n (<= 64) queue entries of word position q, one per lane, writes
-// each decision over its map byte, and moves entries 64 .. pending-1 to the front.
-// Lanes past n read entries inside the queue and store nothing.
-template <int kQ, int kRows>
-__device__ __forceinline__ void slab_drain(SlabLds<kRows>& s, uint32_t n, uint32_t pending,
+// Draws the first n (<= 64) queue entries of token position kE (of the kPer tokens
+// of a lane's vector), one per lane, writes each decision over its map byte, and
+// moves entries 64 .. pending-1 to the front.  Lanes past n read entries inside the
+// queue and store nothing.
+template <int kE, int kRows, int kPer>
+__device__ __forceinline__ void slab_drain(SlabLds<kRows, kPer>& s, uint32_t n, uint32_t pending,
                                            uint32_t lane, uint32_t jid0, uint32_t tm1) {
   const SlabEntry e = s.queue[lane];
   SlabEntry e2 = SlabEntry{0u, 0u, 0u, 0u};
   const bool move = lane + 64u < pending;
   if (move) e2 = s.queue[lane + 64u];
-  // the pair's column is 4 * (jid0 + lane that queued it) + q
-  const uint32_t x = word_of<kQ>(philox_block_lane<6>(jid0 + e.w, Key{e.x, e.y}));
+  // the pair's token is kPer * (jid0 + lane that queued it) + kE: Philox counter
+  // (kPer / 4) * (jid0 + lane) + kE / 4, word kE mod 4
+  const uint32_t x = word_of<kE % 4>(philox_block_lane<6>(
+      (kPer / 4) * (jid0 + e.w) + static_cast<uint32_t>(kE / 4), Key{e.x, e.y}));
   if (lane < n)
-    reinterpret_cast<uint8_t*>(s.map)[4u * e.z + kQ] = static_cast<uint8_t>(is_green(x, tm1));
+    reinterpret_cast<uint8_t*>(s.map)[kPer * e.z + kE] = static_cast<uint8_t>(is_green(x, tm1));
   if (move) s.queue[lane] = e2;
 }
 
-// Queues the pairs of one row and word position q whose row term kjp * J(v) is below
-// `bound`, and drains the queue when it holds 64.
-template <int kQ, int kRows>
-__device__ __forceinline__ void slab_enqueue(SlabLds<kRows>& s, uint32_t& pending, uint64_t kjp,
+// Queues the pairs of one row and token position kE whose row term kjp * J(v) is
+// below `bound`, and drains the queue when it holds 64.
+template <int kE, int kRows, int kPer>
+__device__ __forceinline__ void slab_enqueue(SlabLds<kRows, kPer>& s, uint32_t& pending, uint64_t kjp,
                                              uint32_t jv, uint64_t bound, uint32_t map_word,
                                              uint32_t lane, uint32_t jid0, uint32_t tm1) {
   const uint64_t t = lane_mul_64x32(kjp, jv);
@@ -491,15 +495,15 @@ __device__ __forceinline__ void slab_enqueue(SlabLds<kRows>& s, uint32_t& pendin
   // compiler from moving them across the passes.
   __builtin_amdgcn_wave_barrier();
   if (pending >= 64u) {
-    slab_drain<kQ, kRows>(s, 64u, pending, lane, jid0, tm1);
+    slab_drain<kE, kRows, kPer>(s, 64u, pending, lane, jid0, tm1);
     pending -= 64u;
     __builtin_amdgcn_wave_barrier();
   }
 }
 
-// Word position q over the rows of the slab: queue, drain at 64, drain the rest.
-template <int kQ, int kRows>
-__device__ __forceinline__ void slab_position(SlabLds<kRows>& s, int rows, uint32_t jv, uint64_t bound,
+// Token position kE over the rows of the slab: queue, drain at 64, drain the rest.
+template <int kE, int kRows, int kPer>
+__device__ __forceinline__ void slab_position(SlabLds<kRows, kPer>& s, int rows, uint32_t jv, uint64_t bound,
                                               uint32_t lane, uint32_t jid0, uint32_t tm1) {
   uint32_t pending = 0u;  // wave-uniform
   // two rows per iteration; their key * J(p) by one broadcast LDS read, the next
@@ -511,57 +515,101 @@ __device__ __forceinline__ void slab_position(SlabLds<kRows>& s, int rows, uint3
   for (; r + 1 < rows; r += 2) {
     const u64x2 next = *reinterpret_cast<const u64x2*>(&s.kjp[r + 2]);
     const uint32_t w0 = static_cast<uint32_t>(r) * kSlabMapStride + lane;
-    slab_enqueue<kQ, kRows>(s, pending, kjp.x, jv, bound, w0, lane, jid0, tm1);
-    slab_enqueue<kQ, kRows>(s, pending, kjp.y, jv, bound, w0 + kSlabMapStride, lane, jid0, tm1);
+    slab_enqueue<kE, kRows, kPer>(s, pending, kjp.x, jv, bound, w0, lane, jid0, tm1);
+    slab_enqueue<kE, kRows, kPer>(s, pending, kjp.y, jv, bound, w0 + kSlabMapStride, lane, jid0, tm1);
     kjp = next;
   }
   if (r < rows)
-    slab_enqueue<kQ, kRows>(s, pending, kjp.x, jv, bound,
-                            static_cast<uint32_t>(r) * kSlabMapStride + lane, lane, jid0, tm1);
-  if (pending != 0u) slab_drain<kQ, kRows>(s, pending, pending, lane, jid0, tm1);
+    slab_enqueue<kE, kRows, kPer>(s, pending, kjp.x, jv, bound,
+                                  static_cast<uint32_t>(r) * kSlabMapStride + lane, lane, jid0, tm1);
+  if (pending != 0u) slab_drain<kE, kRows, kPer>(s, pending, pending, lane, jid0, tm1);
   __builtin_amdgcn_wave_barrier();
 }
 
-// Grid: x = tile of kThreads vectors (4 waves of 256 columns), y = a slot taking the
-// slabs y, y + gridDim.y, ... of kRows rows.  Rows 16-byte aligned; vbase a multiple
-// of 4.
-template <int kRows>
+// The bias of a bf16 pair from its two map bytes (bits blo and bhi of the decision
+// word d): one fp32 add each, one rounding, the non-green half's bits kept.
+__device__ __forceinline__ uint32_t bias_pair_bits(uint32_t pair, float delta, uint32_t d, int blo,
+                                                   int bhi) {
+  const uint32_t mlo = static_cast<uint32_t>(__builtin_amdgcn_sbfe(static_cast<int>(d), blo, 1));
+  const uint32_t mhi = static_cast<uint32_t>(__builtin_amdgcn_sbfe(static_cast<int>(d), bhi, 1));
+  const uint32_t take = __builtin_amdgcn_bitop3_b32(0x0000FFFFu, mlo, mhi, 0xCA);
+  const uint32_t biased = to_bf16x2(__uint_as_float(pair << 16) + delta,
+                                    __uint_as_float(pair & 0xFFFF0000u) + delta);
+  return __builtin_amdgcn_bitop3_b32(take, biased, pair, 0xCA);
+}
+
+// Step 3 of a row's vector: the bias from the row's kPer map bytes.
+__device__ __forceinline__ f32x4 slab_bias(f32x4 o, float delta, const uint32_t (&d)[1]) {
+  o.x = bias_bit(o.x, delta, d[0], 0);
+  o.y = bias_bit(o.y, delta, d[0], 8);
+  o.z = bias_bit(o.z, delta, d[0], 16);
+  o.w = bias_bit(o.w, delta, d[0], 24);
+  return o;
+}
+__device__ __forceinline__ u32x4 slab_bias(u32x4 o, float delta, const uint32_t (&d)[2]) {
+  o.x = bias_pair_bits(o.x, delta, d[0], 0, 8);
+  o.y = bias_pair_bits(o.y, delta, d[0], 16, 24);
+  o.z = bias_pair_bits(o.z, delta, d[1], 0, 8);
+  o.w = bias_pair_bits(o.w, delta, d[1], 16, 24);
+  return o;
+}
+
+// The kPer token positions of a lane's vector, one after another.
+template <int kE, int kRows, int kPer>
+__device__ __forceinline__ void slab_positions(SlabLds<kRows, kPer>& s, int rows,
+                                               const uint32_t (&jv)[kPer],
+                                               const uint64_t (&bound)[kPer], uint32_t lane,
+                                               uint32_t jid0, uint32_t tm1) {
+  if constexpr (kE < kPer) {
+    slab_position<kE, kRows, kPer>(s, rows, jv[kE], bound[kE], lane, jid0, tm1);
+    slab_positions<kE + 1, kRows, kPer>(s, rows, jv, bound, lane, jid0, tm1);
+  }
+}
+
+// Grid: x = tile of kThreads vectors (4 waves of 256 vectors), y = a slot taking the
+// slabs y, y + gridDim.y, ... of kRows rows.  T: float (4 tokens a vector) or bf16
+// bits (8).  Rows 16-byte aligned; vbase a multiple of the tokens per vector.
+template <typename T, int kRows>
 __global__ void __launch_bounds__(kThreads)
-watermark_ss_slab_kernel(float* __restrict__ logits, int64_t row_stride, uint32_t V, int64_t B,
+watermark_ss_slab_kernel(T* __restrict__ logits, int64_t row_stride, uint32_t V, int64_t B,
                          const int32_t* __restrict__ context, uint64_t key, uint32_t tm1,
                          float delta, uint32_t vbase) {
-  __shared__ SlabLds<kRows> lds[kThreads / 64];
+  using VecT = typename std::conditional<sizeof(T) == 4, f32x4, u32x4>::type;
+  constexpr int kPer = 16 / sizeof(T);  // tokens a vector
+  constexpr int kWords = kPer / 4;      // map words (and Philox counters) a vector
+  __shared__ SlabLds<kRows, kPer> lds[kThreads / 64];
   const uint32_t lane = threadIdx.x & 63u;
   const uint32_t wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  SlabLds<kRows>& s = lds[wave];
-  const uint32_t full = V / 4u;
-  const uint32_t tail = V % 4u;
+  SlabLds<kRows, kPer>& s = lds[wave];
+  const uint32_t full = V / kPer;
+  const uint32_t tail = V % kPer;
   const uint32_t j0 = blockIdx.x * kThreads + wave * 64u;  // the wave's first vector
   const uint32_t j = j0 + lane;
   const bool active = j < full;
-  const uint32_t jid0 = j0 + vbase / 4u;  // in token ids / 4: the Philox counter
+  const uint32_t jid0 = j0 + vbase / kPer;  // in token ids / kPer
   const uint32_t jid = jid0 + lane;
-  // the lane's four columns: J(v), and the self term as the queueing bound (0, which no
-  // row term is below, for a lane past the row's last whole vector)
-  uint32_t jv[4];
-  uint64_t bound[4];
-  uint32_t self_word;
+  // the lane's tokens: J(v), and the self term as the queueing bound (0, which no row
+  // term is below, for a lane past the row's last whole vector)
+  uint32_t jv[kPer];
+  uint64_t bound[kPer];
+  uint32_t self_word[kWords];
   {
-    uint64_t self[4];
+    uint64_t self[kPer];
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      jv[q] = jenkins32((jid << 2) | static_cast<uint32_t>(q));
-      self[q] = mul_64x64(key, wide_mul(jv[q], jv[q]));
-      bound[q] = active ? self[q] : 0u;
+    for (int e = 0; e < kPer; ++e) {
+      jv[e] = jenkins32(jid * kPer + static_cast<uint32_t>(e));
+      self[e] = mul_64x64(key, wide_mul(jv[e], jv[e]));
+      bound[e] = active ? self[e] : 0u;
     }
-    self_word = static_cast<uint32_t>(
-                    is_green(word_of<0>(philox_block_lane<6>(jid, key_of(self[0]))), tm1)) |
-                static_cast<uint32_t>(
-                    is_green(word_of<1>(philox_block_lane<6>(jid, key_of(self[1]))), tm1)) << 8 |
-                static_cast<uint32_t>(
-                    is_green(word_of<2>(philox_block_lane<6>(jid, key_of(self[2]))), tm1)) << 16 |
-                static_cast<uint32_t>(
-                    is_green(word_of<3>(philox_block_lane<6>(jid, key_of(self[3]))), tm1)) << 24;
+#pragma unroll
+    for (int w = 0; w < kWords; ++w) {
+      const uint32_t c = jid * kWords + static_cast<uint32_t>(w);  // Philox counter
+      self_word[w] =
+          static_cast<uint32_t>(is_green(word_of<0>(philox_block_lane<6>(c, key_of(self[4 * w]))), tm1)) |
+          static_cast<uint32_t>(is_green(word_of<1>(philox_block_lane<6>(c, key_of(self[4 * w + 1]))), tm1)) << 8 |
+          static_cast<uint32_t>(is_green(word_of<2>(philox_block_lane<6>(c, key_of(self[4 * w + 2]))), tm1)) << 16 |
+          static_cast<uint32_t>(is_green(word_of<3>(philox_block_lane<6>(c, key_of(self[4 * w + 3]))), tm1)) << 24;
+    }
   }
   const int64_t slabs = (B + kRows - 1) / kRows;
   for (int64_t g = blockIdx.y; g < slabs; g += gridDim.y) {
@@ -569,37 +617,35 @@ watermark_ss_slab_kernel(float* __restrict__ logits, int64_t row_stride, uint32_
     const int rows = static_cast<int>(B - row0 < kRows ? B - row0 : kRows);
     // step 1: the self decisions for every row, and each row's key * J(p)
 #pragma nounroll
-    for (int r = 0; r < rows; ++r) s.map[static_cast<uint32_t>(r) * kSlabMapStride + lane] = self_word;
+    for (int r = 0; r < rows; ++r) {
+#pragma unroll
+      for (int w = 0; w < kWords; ++w)
+        s.map[(static_cast<uint32_t>(r) * kSlabMapStride + lane) * kWords + w] = self_word[w];
+    }
     if (lane < static_cast<uint32_t>(rows))
       s.kjp[lane] = key * static_cast<uint64_t>(jenkins32(static_cast<uint32_t>(context[row0 + lane])));
     __builtin_amdgcn_wave_barrier();
-    // step 2: the pairs whose row term is smaller, one word position at a time
-    slab_position<0, kRows>(s, rows, jv[0], bound[0], lane, jid0, tm1);
-    slab_position<1, kRows>(s, rows, jv[1], bound[1], lane, jid0, tm1);
-    slab_position<2, kRows>(s, rows, jv[2], bound[2], lane, jid0, tm1);
-    slab_position<3, kRows>(s, rows, jv[3], bound[3], lane, jid0, tm1);
+    // step 2: the pairs whose row term is smaller, one token position at a time
+    slab_positions<0, kRows, kPer>(s, rows, jv, bound, lane, jid0, tm1);
     // step 3: bias and store, kSlabLoadRows rows' loads in flight at a time
     if (active) {
       for (int r0 = 0; r0 < rows; r0 += kSlabLoadRows) {
-        f32x4 buf[kSlabLoadRows];
-        uint32_t dec[kSlabLoadRows];
+        VecT buf[kSlabLoadRows];
+        uint32_t dec[kSlabLoadRows][kWords];
 #pragma unroll
         for (int k = 0; k < kSlabLoadRows; ++k) {
           if (r0 + k < rows) {
-            buf[k] = stream_load(reinterpret_cast<const f32x4*>(logits + (row0 + r0 + k) * row_stride) + j);
-            dec[k] = s.map[static_cast<uint32_t>(r0 + k) * kSlabMapStride + lane];
+            buf[k] = stream_load(reinterpret_cast<const VecT*>(logits + (row0 + r0 + k) * row_stride) + j);
+#pragma unroll
+            for (int w = 0; w < kWords; ++w)
+              dec[k][w] = s.map[(static_cast<uint32_t>(r0 + k) * kSlabMapStride + lane) * kWords + w];
           }
         }
 #pragma unroll
         for (int k = 0; k < kSlabLoadRows; ++k) {
-          if (r0 + k < rows) {
-            f32x4 o = buf[k];
-            o.x = bias_bit(o.x, delta, dec[k], 0);
-            o.y = bias_bit(o.y, delta, dec[k], 8);
-            o.z = bias_bit(o.z, delta, dec[k], 16);
-            o.w = bias_bit(o.w, delta, dec[k], 24);
-            stream_store(reinterpret_cast<f32x4*>(logits + (row0 + r0 + k) * row_stride) + j, o);
-          }
+          if (r0 + k < rows)
+            stream_store(reinterpret_cast<VecT*>(logits + (row0 + r0 + k) * row_stride) + j,
+                         slab_bias(buf[k], delta, dec[k]));
         }
       }
     }
@@ -608,8 +654,8 @@ watermark_ss_slab_kernel(float* __restrict__ logits, int64_t row_stride, uint32_
       for (int r = 0; r < rows; ++r) {
         const RowSeed<1> rs = row_seed<kSelfSalt, 1>(key, context + row0 + r, 1);
         for (uint32_t e = 0; e < tail; ++e)
-          bias_one<float, kSelfSalt>(logits + (row0 + r) * row_stride, full * 4u + e, rs, tm1,
-                                     delta, vbase);
+          bias_one<T, kSelfSalt>(logits + (row0 + r) * row_stride, full * kPer + e, rs, tm1,
+                                 delta, vbase);
       }
     }
     __builtin_amdgcn_wave_barrier();  // the next slab rewrites the map
@@ -1632,18 +1678,18 @@ void launch_watermark(void* logits, int64_t B, uint32_t V, int64_t row_stride,
     const uint64_t vectors = (static_cast<uint64_t>(V) + kPer - 1) / kPer;
     const uint32_t tiles = static_cast<uint32_t>((vectors + kThreads * kU - 1) / (kThreads * kU));
     if constexpr (kSeeding == kSelfSalt) {
-      if constexpr (SBW_SELF_SALT_SLAB && kW == 1 && std::is_same<T, float>::value) {
+      if constexpr (SBW_SELF_SALT_SLAB && kW == 1) {
         const uint32_t tiles1 = static_cast<uint32_t>((vectors + kThreads - 1) / kThreads);
         const int64_t slabs12 = (B + 11) / 12, slabs8 = (B + 7) / 8;
         if (static_cast<int64_t>(tiles1) * slabs12 >= int64_t{SBW_SLAB_MIN_GROUPS}) {
           const dim3 grid(tiles1, static_cast<uint32_t>(slabs12 < kMaxGridY ? slabs12 : kMaxGridY));
-          hipLaunchKernelGGL((watermark_ss_slab_kernel<12>), grid, dim3(kThreads), 0, stream, p,
+          hipLaunchKernelGGL((watermark_ss_slab_kernel<T, 12>), grid, dim3(kThreads), 0, stream, p,
                              row_stride, V, B, context, key, tm1, delta, vbase);
           return;
         }
         if (static_cast<int64_t>(tiles1) * slabs8 >= int64_t{SBW_SLAB_MIN_GROUPS}) {
           const dim3 grid(tiles1, static_cast<uint32_t>(slabs8 < kMaxGridY ? slabs8 : kMaxGridY));
-          hipLaunchKernelGGL((watermark_ss_slab_kernel<8>), grid, dim3(kThreads), 0, stream, p,
+          hipLaunchKernelGGL((watermark_ss_slab_kernel<T, 8>), grid, dim3(kThreads), 0, stream, p,
                              row_stride, V, B, context, key, tm1, delta, vbase);
           return;
         }

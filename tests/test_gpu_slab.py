@@ -1,4 +1,4 @@
-"""GPU parity of the self-salt split-term slab kernel (fp32, window of one token).
+"""GPU parity of the self-salt split-term slab kernel (fp32 and bf16, window of one token).
 
 Large fp32 self-salt launches take a kernel that draws each column's self-term block
 once per slab of 12 rows (8 for launches that 12-row slabs would leave with too few
@@ -21,6 +21,7 @@ import numpy as np
 import pytest
 
 import oracle
+import workloads
 from test_gpu_parity import (KEY, WIDE, _from_device, _to_device, assert_logits_equal, env,  # noqa: F401
                              say, special_logits)
 
@@ -30,10 +31,11 @@ SLAB_ROWS = 12
 MIN_GROUPS = 2000   # workgroups below which the next slab height (or kernel) is taken
 
 
-def slab_rows(B, V):
-    """The launch rule of the fp32 self-salt watermark (rows 16-byte aligned): the slab
-    height the launch takes, or 0 for the row-group kernel."""
-    tiles = -(-(-(-V // 4)) // 256)
+def slab_rows(B, V, dtype="f32"):
+    """The launch rule of the self-salt watermark, window of one token (rows 16-byte
+    aligned): the slab height the launch takes, or 0 for the row-group kernel."""
+    per = 4 if dtype == "f32" else 8     # tokens in a 16-byte vector
+    tiles = -(-(-(-V // per)) // 256)
     for rows in (12, 8):
         if tiles * -(-B // rows) >= MIN_GROUPS:
             return rows
@@ -51,7 +53,8 @@ def run(env, x, prev, key, gamma, delta, stride=None, v_offset=None):
         t = _to_device(torch, dev, x)
         view = t
     else:
-        t = torch.zeros((B, stride), dtype=torch.float32, device=dev)
+        dt = torch.bfloat16 if x.dtype == np.uint16 else torch.float32
+        t = torch.zeros((B, stride), dtype=dt, device=dev)
         t[:, :V] = _to_device(torch, dev, x)
         view = t[:, :V]
     p = torch.from_numpy(prev).to(dev)
@@ -164,9 +167,46 @@ def test_slab_eight_rows(env, B, V):
                         f"B={B} V={V}")
 
 
+@pytest.mark.parametrize("B,V,stride,rows", [
+    (2400, 20483, None, 12),      # V mod 8 = 3, a tile of 1 vector at the end
+    (2407, 20480, 20488, 12),     # padded rows, a last slab of 7 rows
+    (256, 152064, None, 8),       # the c4 shape in bf16: 8-row slabs
+    (263, 152061, None, 8),       # a last slab of 7 rows, V mod 8 = 5
+])
+def test_slab_bf16(env, B, V, stride, rows):
+    """bf16 logits: 8 tokens a vector, two Philox counters a lane, 8 map bytes a row."""
+    assert slab_rows(B, V, "bf16") == rows
+    rng = np.random.default_rng(1616 + B + V)
+    x = special_logits(rng, B, V, "bf16")
+    prev = rng.integers(0, 1 << 31, B).astype(np.int32)
+    prev[:2] = [0, -1]
+    say(f"slab bf16 B={B} V={V} stride={stride}")
+    got, pad = run(env, x, prev, WIDE, 0.25, 2.0, stride)
+    assert_logits_equal(got, oracle.watermark(x, prev, WIDE, 0.25, 2.0, "self_salt"),
+                        f"bf16 B={B} V={V}")
+    if pad is not None:
+        assert not pad.any(), "the padding columns were written"
+
+
+def test_slab_bf16_shard(env):
+    """A bf16 vocabulary shard whose first token id is a multiple of 8 (not of 16)."""
+    a, n, V, B = 57024 + 8, 19000, 152064, 2600
+    assert slab_rows(B, n, "bf16") == 12
+    rng = np.random.default_rng(4343)
+    x = workloads.f32_to_bf16_bits(rng.standard_normal((B, n)).astype(np.float32) * np.float32(2))
+    prev = rng.integers(0, V, B).astype(np.int32)
+    say("slab bf16 shard 57032+19000, B=2600")
+    got, _ = run(env, x, prev, KEY, 0.5, -1.5, v_offset=a)
+    green = oracle.is_green_many(KEY, np.repeat(prev, n), np.tile(np.arange(a, a + n), B), 0.5,
+                                 "self_salt").reshape(B, n)
+    expect = np.where(green, oracle.bias_bf16_many(x, -1.5), x)
+    assert_logits_equal(got, expect, "bf16 shard")
+
+
 def test_launch_rule_cases():
     """The c4 configurations take 12-row slabs, B = 128 of a 128256-token vocabulary
     8-row ones; c3 and small batches take the row-group kernel."""
     assert slab_rows(256, 152064) == 12 and slab_rows(1024, 152064) == 12
     assert slab_rows(128, 128256) == 8
     assert slab_rows(64, 128256) == 0 and slab_rows(16, 152064) == 0
+    assert slab_rows(256, 152064, "bf16") == 8 and slab_rows(1024, 152064, "bf16") == 12
