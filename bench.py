@@ -537,6 +537,23 @@ def other_configs(torch, sbw, dev, steps, c5_tokens):
     res["c4_B1024_decode"] = dec
     del bufs
     torch.cuda.empty_cache()
+
+    progress("B=1024 done")
+    # c4's shape with bf16 logits (its fp32 logits rounded to nearest even), both seedings
+    # (not a configuration of its own: the bf16 path at the main step's size)
+    xb, pb = workloads.watermark_inputs("c4")
+    bufs = rotating(workloads.f32_to_bf16_bits(xb))
+    p = torch.from_numpy(pb).to(dev)
+    n = c["B"] * c["V"]
+    half = {}
+    for seeding in ("self_salt", "context"):
+        us = _mean_us(torch, lambda i, s=seeding: sbw.watermark(bufs[i % len(bufs)], p, key,
+                                                                c["gamma"], c["delta"], s), steps)
+        half[seeding] = {"us": us, "gelem_per_s": n / us / 1e3,
+                         "hbm_gbps": 4 * n / us / 1e3, "hbm_frac": 4 * n / us / 1e3 / HBM_PEAK_GBPS}
+    res["c4_bf16"] = half
+    del bufs
+    torch.cuda.empty_cache()
     return res
 
 
