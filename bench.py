@@ -267,7 +267,7 @@ def philox_roof(torch, warm_ms=50.0, reps=10):
     for kind, name, per_link in ((1, "v_mad_u64_u32", 1), (2, "v_bitop3_b32", 1),
                                  (3, "v_add_u32", 1), (4, "mix: mad + bitop3 + add", 3),
                                  (5, "v_bitop3_b32, one scalar operand", 1),
-                                 (6, "v_add_u32, scalar operand", 1)):
+                                 (6, "v_add_u32, scalar operand", 1), (7, "v_mul_lo_u32", 1)):
         ops = lanes * op_iters * 16 * chains * per_link
         r, m = measure(lambda k=kind: check(lib.sbw_rate_op(k, out_buf.data_ptr(), clk.data_ptr(),
                                                             workgroups, op_iters, 1, stream)), ops)

@@ -136,7 +136,8 @@ philox_sched_kernel(uint32_t* __restrict__ out, uint64_t* __restrict__ clocks, i
 }
 
 enum OpKind : int {
-  kOpMad64 = 1, kOpBitop3 = 2, kOpAdd = 3, kOpPhiloxMix = 4, kOpBitop3Scalar = 5, kOpAddScalar = 6
+  kOpMad64 = 1, kOpBitop3 = 2, kOpAdd = 3, kOpPhiloxMix = 4, kOpBitop3Scalar = 5, kOpAddScalar = 6,
+  kOpMulLo = 7
 };
 
 // kChains chains of `iters` x 16 links of one instruction kind per lane.  kOpPhiloxMix
@@ -185,6 +186,10 @@ op_rate_kernel(uint32_t* __restrict__ out, uint64_t* __restrict__ clocks, int it
           b[c] = b[c] + static_cast<uint32_t>(p);
         } else if constexpr (kKind == kOpBitop3Scalar) {
           a[c] = xor3(a[c], b[c], m);
+        } else if constexpr (kKind == kOpMulLo) {
+          // low half of a 32x32 product, alternating as the adds do
+          if (l & 1) b[c] = b[c] * a[c];
+          else a[c] = a[c] * b[c];
         } else {
           // a scalar operand (written out: the compiler would fold a chain of adds of
           // one uniform value into one product)
@@ -239,7 +244,8 @@ int sbw_rate_philox(uint32_t* out, uint64_t* clocks, int workgroups, int iters, 
 }
 
 // The single-kind chains: kind 1 products, 2 three-input xors, 3 adds, 4 the mix of
-// one of each per link, 5 three-input xors and 6 adds with one scalar operand.  Each
+// one of each per link, 5 three-input xors and 6 adds with one scalar operand, 7 the
+// low halves of 32x32 products.  Each
 // lane runs iters * 16 * sbw_rate_chains() links (the mix: three instructions per
 // link).  Same buffers as sbw_rate_philox.
 int sbw_rate_op(int kind, uint32_t* out, uint64_t* clocks, int workgroups, int iters,
@@ -269,6 +275,9 @@ int sbw_rate_op(int kind, uint32_t* out, uint64_t* clocks, int workgroups, int i
     case kOpAddScalar:
       hipLaunchKernelGGL(op_rate_kernel<kOpAddScalar>, grid, block, 0, st, out, clocks, iters,
                          salt);
+      break;
+    case kOpMulLo:
+      hipLaunchKernelGGL(op_rate_kernel<kOpMulLo>, grid, block, 0, st, out, clocks, iters, salt);
       break;
     default:
       return static_cast<int>(hipErrorInvalidValue);
