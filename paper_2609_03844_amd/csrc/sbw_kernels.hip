@@ -9,7 +9,7 @@
 //             counter; self-salt needs one block per token, and its workgroups
 //             share each candidate's hash and self term across up to 4 rows.  Large
 //             self-salt launches (window of one token) instead draw each
-//             column's self-term block once per slab of 12 or 8 rows and queue in
+//             column's self-term block once per slab of 12, 8 or 6 rows and queue in
 //             LDS only the pairs whose row term is the smaller one (about half).
 // argmax      greedy decoding of the watermarked logits without writing them: one
 //             read of each logit, a per-segment (value, index) partial, a read-out
@@ -77,9 +77,9 @@ namespace {
 #define SBW_SELF_SALT_NARROW 1
 #endif
 // Self-salt, width 1 (fp32 and bf16): the split-term slab kernel when it makes at least
-// SBW_SLAB_MIN_GROUPS workgroups with 12-row slabs, else with 8-row slabs (below that
-// its long-lived waves leave the chip underfilled and the row-group kernel is
-// faster).  0 = off.
+// SBW_SLAB_MIN_GROUPS workgroups with 12-row slabs, else with 8-row, else with 6-row
+// slabs (below that its long-lived waves leave the chip underfilled and the row-group
+// kernel is faster).  0 = off.
 #ifndef SBW_SELF_SALT_SLAB
 #define SBW_SELF_SALT_SLAB 1
 #endif
@@ -1680,7 +1680,7 @@ void launch_watermark(void* logits, int64_t B, uint32_t V, int64_t row_stride,
     if constexpr (kSeeding == kSelfSalt) {
       if constexpr (SBW_SELF_SALT_SLAB && kW == 1) {
         const uint32_t tiles1 = static_cast<uint32_t>((vectors + kThreads - 1) / kThreads);
-        const int64_t slabs12 = (B + 11) / 12, slabs8 = (B + 7) / 8;
+        const int64_t slabs12 = (B + 11) / 12, slabs8 = (B + 7) / 8, slabs6 = (B + 5) / 6;
         if (static_cast<int64_t>(tiles1) * slabs12 >= int64_t{SBW_SLAB_MIN_GROUPS}) {
           const dim3 grid(tiles1, static_cast<uint32_t>(slabs12 < kMaxGridY ? slabs12 : kMaxGridY));
           hipLaunchKernelGGL((watermark_ss_slab_kernel<T, 12>), grid, dim3(kThreads), 0, stream, p,
@@ -1690,6 +1690,12 @@ void launch_watermark(void* logits, int64_t B, uint32_t V, int64_t row_stride,
         if (static_cast<int64_t>(tiles1) * slabs8 >= int64_t{SBW_SLAB_MIN_GROUPS}) {
           const dim3 grid(tiles1, static_cast<uint32_t>(slabs8 < kMaxGridY ? slabs8 : kMaxGridY));
           hipLaunchKernelGGL((watermark_ss_slab_kernel<T, 8>), grid, dim3(kThreads), 0, stream, p,
+                             row_stride, V, B, context, key, tm1, delta, vbase);
+          return;
+        }
+        if (static_cast<int64_t>(tiles1) * slabs6 >= int64_t{SBW_SLAB_MIN_GROUPS}) {
+          const dim3 grid(tiles1, static_cast<uint32_t>(slabs6 < kMaxGridY ? slabs6 : kMaxGridY));
+          hipLaunchKernelGGL((watermark_ss_slab_kernel<T, 6>), grid, dim3(kThreads), 0, stream, p,
                              row_stride, V, B, context, key, tm1, delta, vbase);
           return;
         }

@@ -333,14 +333,15 @@ def test_bf16_rounding_every_pattern(env, layout):
 
 
 @pytest.mark.parametrize("dtype,B,V,width,rows", [
-    ("f32", 219, 152063, 1, 4),     # 75 tiles x 219 rows: 4 rows per workgroup, last group of 3
-    ("f32", 63, 152061, 1, 2),      # 2 rows per workgroup, last group of 1
-    ("bf16", 219, 152063, 1, 2),    # bf16 takes at most 2 rows
+    ("f32", 75, 152063, 1, 4),      # 75 tiles x 19 / 20 groups of 4 rows, last group of 3 / 1;
+    ("f32", 77, 152061, 1, 4),      #   6-row slabs would make 13 x 149 < 2000 workgroups
+    ("bf16", 151, 152063, 1, 2),    # bf16 takes at most 2 rows; 4 groups per workgroup (the
+                                    #   next one loaded while the current one is drawn)
     ("f32", 221, 151937, 4, 1),     # width 4 (SBW-ss-V) keeps one row per workgroup
     ("f32", 63, 128256, 1, 4),      # too few tiles at two vectors per lane: one vector per
     ("f32", 33, 128256, 1, 4),      #   lane and 4-row groups, last group of 3 / of 1
-    ("bf16", 67, 128256, 1, 2),     # 2-row groups, two per workgroup (the next one loaded
-])                                  #   while the current one is drawn), last group of 1
+    ("bf16", 67, 128256, 1, 2),     # 2-row groups, two per workgroup, last group of 1
+])
 def test_self_salt_row_groups(env, dtype, B, V, width, rows):
     """Self-salt launches of the sizes at which a workgroup shares the candidate terms
     across `rows` rows (width 1 with enough workgroups), with a partial last vector

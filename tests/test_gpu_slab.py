@@ -1,7 +1,7 @@
 """GPU parity of the self-salt split-term slab kernel (fp32 and bf16, window of one token).
 
-Large fp32 self-salt launches take a kernel that draws each column's self-term block
-once per slab of 12 rows (8 for launches that 12-row slabs would leave with too few
+Large self-salt launches take a kernel that draws each column's self-term block once
+per slab of 12 rows (8, then 6, for launches that taller slabs would leave with too few
 workgroups) and queues in LDS only the (row, token) pairs whose row term is the
 smaller one.  Every case here is sized to take that kernel (the launch rule is
 mirrored in `slab_rows` and asserted), and is compared with the oracle bit for bit:
@@ -36,7 +36,7 @@ def slab_rows(B, V, dtype="f32"):
     aligned): the slab height the launch takes, or 0 for the row-group kernel."""
     per = 4 if dtype == "f32" else 8     # tokens in a 16-byte vector
     tiles = -(-(-(-V // per)) // 256)
-    for rows in (12, 8):
+    for rows in (12, 8, 6):
         if tiles * -(-B // rows) >= MIN_GROUPS:
             return rows
     return 0
@@ -167,11 +167,30 @@ def test_slab_eight_rows(env, B, V):
                         f"B={B} V={V}")
 
 
+@pytest.mark.parametrize("B,V", [
+    (96, 128256),     # whole 6-row slabs
+    (101, 128255),    # a last slab of 5 rows, V mod 4 = 3
+    (80, 152064),
+])
+def test_slab_six_rows(env, B, V):
+    """Launches that 8-row slabs would leave with too few workgroups take 6-row ones."""
+    assert slab_rows(B, V) == 6
+    rng = np.random.default_rng(606 + B)
+    x = special_logits(rng, B, V, "f32")
+    prev = rng.integers(0, V, B).astype(np.int32)
+    say(f"slab 6 rows B={B} V={V}")
+    got, _ = run(env, x, prev, KEY, 0.5, -2.0)
+    assert_logits_equal(got, oracle.watermark(x, prev, KEY, 0.5, -2.0, "self_salt"),
+                        f"B={B} V={V}")
+
+
 @pytest.mark.parametrize("B,V,stride,rows", [
     (2400, 20483, None, 12),      # V mod 8 = 3, a tile of 1 vector at the end
     (2407, 20480, 20488, 12),     # padded rows, a last slab of 7 rows
     (256, 152064, None, 8),       # the c4 shape in bf16: 8-row slabs
     (263, 152061, None, 8),       # a last slab of 7 rows, V mod 8 = 5
+    (192, 152064, None, 6),       # 6-row slabs
+    (197, 152061, None, 6),       # a last slab of 5 rows, V mod 8 = 5
 ])
 def test_slab_bf16(env, B, V, stride, rows):
     """bf16 logits: 8 tokens a vector, two Philox counters a lane, 8 map bytes a row."""
@@ -205,8 +224,9 @@ def test_slab_bf16_shard(env):
 
 def test_launch_rule_cases():
     """The c4 configurations take 12-row slabs, B = 128 of a 128256-token vocabulary
-    8-row ones; c3 and small batches take the row-group kernel."""
+    8-row ones, B = 96 6-row ones; c3 and small batches take the row-group kernel."""
     assert slab_rows(256, 152064) == 12 and slab_rows(1024, 152064) == 12
-    assert slab_rows(128, 128256) == 8
+    assert slab_rows(128, 128256) == 8 and slab_rows(96, 128256) == 6
     assert slab_rows(64, 128256) == 0 and slab_rows(16, 152064) == 0
     assert slab_rows(256, 152064, "bf16") == 8 and slab_rows(1024, 152064, "bf16") == 12
+    assert slab_rows(192, 152064, "bf16") == 6 and slab_rows(151, 152063, "bf16") == 0
