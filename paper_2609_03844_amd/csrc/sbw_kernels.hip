@@ -71,11 +71,6 @@ namespace {
 #ifndef SBW_SELF_SALT_PREFETCH_BF16
 #define SBW_SELF_SALT_PREFETCH_BF16 1
 #endif
-// Self-salt fp32, width 1: one vector per lane when that is what it takes to group 4 rows
-// per workgroup (batches of 64 rows of a 128K vocabulary).  0 = off.
-#ifndef SBW_SELF_SALT_NARROW
-#define SBW_SELF_SALT_NARROW 1
-#endif
 // Self-salt, width 1 (fp32 and bf16): the split-term slab kernel when it makes at least
 // SBW_SLAB_MIN_GROUPS workgroups with 12-row slabs, else with 8-row, else with 6-row
 // slabs (below that its long-lived waves leave the chip underfilled and the row-group
@@ -1702,12 +1697,12 @@ void launch_watermark(void* logits, int64_t B, uint32_t V, int64_t row_stride,
       }
       constexpr int kMaxRows = kW > 1 ? 1 : (sizeof(T) == 4 ? 4 : 2);
       const int64_t work = static_cast<int64_t>(tiles) * B;
-      if constexpr (SBW_SELF_SALT_NARROW && kMaxRows == 4 && kU > 1) {
-        // Too few tiles for 4-row groups at kU vectors per lane, enough at one: the
-        // narrower tiles keep the candidate terms shared by 4 rows.
+      if constexpr (kMaxRows == 4) {
+        // fp32, width 1: 4-row groups take one vector per lane, whenever that makes
+        // SBW_SELF_SALT_MIN_GROUPS workgroups (the narrower tiles keep more of them
+        // resident at once than two vectors per lane do)
         const uint32_t tiles1 = static_cast<uint32_t>((vectors + kThreads - 1) / kThreads);
-        if (work < 4 * int64_t{SBW_SELF_SALT_MIN_GROUPS} &&
-            static_cast<int64_t>(tiles1) * B >= 4 * int64_t{SBW_SELF_SALT_MIN_GROUPS}) {
+        if (static_cast<int64_t>(tiles1) * B >= 4 * int64_t{SBW_SELF_SALT_MIN_GROUPS}) {
           const int64_t groups = (B + 3) / 4;
           const dim3 grid(tiles1, static_cast<uint32_t>(groups < kMaxGridY ? groups : kMaxGridY));
           hipLaunchKernelGGL((watermark_ss_rows_kernel<T, 1, kW, 4, false>), grid, dim3(kThreads),
@@ -1716,10 +1711,8 @@ void launch_watermark(void* logits, int64_t B, uint32_t V, int64_t row_stride,
           return;
         }
       }
-      const int rows_per_group = work >= kMaxRows * int64_t{SBW_SELF_SALT_MIN_GROUPS} ? kMaxRows
-                                 : (kMaxRows >= 2 && work >= 2 * int64_t{SBW_SELF_SALT_MIN_GROUPS})
-                                     ? 2
-                                     : 1;
+      const int rows_per_group =
+          (kMaxRows >= 2 && work >= 2 * int64_t{SBW_SELF_SALT_MIN_GROUPS}) ? 2 : 1;
       const int64_t groups = (B + rows_per_group - 1) / rows_per_group;
       // Each workgroup takes up to kIters groups while that still leaves
       // SBW_SELF_SALT_MIN_GROUPS workgroups.
@@ -1731,11 +1724,7 @@ void launch_watermark(void* logits, int64_t B, uint32_t V, int64_t row_stride,
       }
       const dim3 grid(tiles, static_cast<uint32_t>(slots < kMaxGridY ? slots : kMaxGridY));
       constexpr bool kPf = (sizeof(T) == 4 ? SBW_SELF_SALT_PREFETCH : SBW_SELF_SALT_PREFETCH_BF16) != 0;
-      if (kMaxRows == 4 && rows_per_group == 4)
-        hipLaunchKernelGGL((watermark_ss_rows_kernel<T, kU, kW, (kMaxRows > 2 ? kMaxRows : 1), kPf>),
-                           grid, dim3(kThreads), 0, stream, p, row_stride, V, B, context, width,
-                           key, tm1, delta, vbase);
-      else if (kMaxRows >= 2 && rows_per_group == 2)
+      if (kMaxRows >= 2 && rows_per_group == 2)
         hipLaunchKernelGGL((watermark_ss_rows_kernel<T, kU, kW, (kMaxRows >= 2 ? 2 : 1), kPf>), grid,
                            dim3(kThreads), 0, stream, p, row_stride, V, B, context, width, key, tm1,
                            delta, vbase);

@@ -333,27 +333,33 @@ def test_bf16_rounding_every_pattern(env, layout):
 
 
 @pytest.mark.parametrize("dtype,B,V,width,rows", [
-    ("f32", 75, 152063, 1, 4),      # 75 tiles x 19 / 20 groups of 4 rows, last group of 3 / 1;
+    ("f32", 75, 152063, 1, 4),      # 149 tiles x 19 / 20 groups of 4 rows, last group of 3 / 1;
     ("f32", 77, 152061, 1, 4),      #   6-row slabs would make 13 x 149 < 2000 workgroups
     ("bf16", 151, 152063, 1, 2),    # bf16 takes at most 2 rows; 4 groups per workgroup (the
                                     #   next one loaded while the current one is drawn)
     ("f32", 221, 151937, 4, 1),     # width 4 (SBW-ss-V) keeps one row per workgroup
-    ("f32", 63, 128256, 1, 4),      # too few tiles at two vectors per lane: one vector per
-    ("f32", 33, 128256, 1, 4),      #   lane and 4-row groups, last group of 3 / of 1
+    ("f32", 63, 128256, 1, 4),      # c3's launch, last group of 3
+    ("f32", 33, 128256, 1, 4),      # last group of 1
     ("bf16", 67, 128256, 1, 2),     # 2-row groups, two per workgroup, last group of 1
 ])
 def test_self_salt_row_groups(env, dtype, B, V, width, rows):
     """Self-salt launches of the sizes at which a workgroup shares the candidate terms
     across `rows` rows (width 1 with enough workgroups), with a partial last vector
-    and a partial last row group."""
+    (rows padded to a multiple of 16 bytes, so that the vector kernels take them) and a
+    partial last row group."""
     rng = np.random.default_rng(230 + B + width)
     x = special_logits(rng, B, V, dtype)
     ctx = workloads.context_tokens(B, width, V, rng)
     say(f"self-salt row groups {dtype} B={B} V={V} h={width} rows={rows}")
     torch, sbw, dev = env
-    t = _to_device(torch, dev, x)
+    stride = -(-V // 8) * 8
+    t = torch.zeros((B, stride), dtype=torch.bfloat16 if dtype == "bf16" else torch.float32,
+                    device=dev)
+    t[:, :V] = _to_device(torch, dev, x)
     c = torch.from_numpy(ctx).to(dev)
-    sbw.watermark(t, c if width > 1 else c[:, 0].contiguous(), WIDE, 0.25, 2.0, "self_salt")
+    sbw.watermark(t[:, :V], c if width > 1 else c[:, 0].contiguous(), WIDE, 0.25, 2.0, "self_salt")
     torch.cuda.synchronize()
     expect = oracle.watermark_w(x, ctx, WIDE, 0.25, 2.0, "self_salt")
-    assert_logits_equal(_from_device(torch, t), expect, f"{dtype} B={B} V={V} h={width}")
+    out = _from_device(torch, t)
+    assert_logits_equal(out[:, :V], expect, f"{dtype} B={B} V={V} h={width}")
+    assert not out[:, V:].any(), "the padding columns were written"
