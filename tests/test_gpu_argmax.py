@@ -73,7 +73,7 @@ def test_argmax_small(env, dtype, seeding, width, B, V):
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("seeding", ["context", "self_salt"])
-@pytest.mark.parametrize("offset,stride_pad", [(1, 0), (0, 3), (8, 8)])
+@pytest.mark.parametrize("offset,stride_pad", [(1, 0), (0, 3), (8, 8), (0, 7)])   # 9008: aligned in both dtypes
 def test_argmax_layouts(env, dtype, seeding, offset, stride_pad):
     rng = np.random.default_rng(80 + offset + stride_pad)
     B, V = 5, 9001

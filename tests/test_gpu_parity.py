@@ -154,9 +154,12 @@ def test_watermark_small(env, dtype, seeding, B, V):
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("seeding", ["context", "self_salt"])
-@pytest.mark.parametrize("stride_pad,offset", [(1, 0), (3, 0), (8, 0), (0, 1), (5, 3), (0, 8)])
+@pytest.mark.parametrize("stride_pad,offset", [(1, 0), (3, 0), (8, 0), (0, 1), (5, 3), (0, 8),
+                                               (5, 0), (13, 8)])
 def test_watermark_layouts(env, dtype, seeding, stride_pad, offset):
-    # padded rows, unaligned row starts (element kernel) and aligned-but-offset starts
+    # padded rows, unaligned row starts (element kernel) and aligned-but-offset starts;
+    # strides of 5008 and 5016 keep rows 16-byte aligned in both dtypes (the vector
+    # kernels with a 3-token row tail)
     rng = np.random.default_rng(77 + stride_pad * 10 + offset)
     B, V = 6, 5003
     x = special_logits(rng, B, V, dtype)

@@ -55,7 +55,7 @@ def test_sample_small(env, dtype, seeding, width, B, V):
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("seeding", ["context", "self_salt"])
-@pytest.mark.parametrize("offset,stride_pad", [(1, 0), (0, 3)])
+@pytest.mark.parametrize("offset,stride_pad", [(1, 0), (0, 3), (0, 7)])   # 9008: aligned in both dtypes
 def test_sample_layouts(env, dtype, seeding, offset, stride_pad):
     rng = np.random.default_rng(410 + offset + stride_pad)
     B, V = 5, 9001

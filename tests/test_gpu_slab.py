@@ -47,8 +47,13 @@ def takes_slab(B, V):
 
 
 def run(env, x, prev, key, gamma, delta, stride=None, v_offset=None):
+    """Watermarks x in a device buffer of rows `stride` elements apart: by default V when
+    that keeps every row 16-byte aligned, else V rounded up to a multiple of 8 (rows that
+    are not aligned take the element-wise kernel instead)."""
     torch, sbw, dev = env
     B, V = x.shape
+    if stride is None and (V * x.itemsize) % 16 != 0:
+        stride = -(-V // 8) * 8
     if stride is None:
         t = _to_device(torch, dev, x)
         view = t
