@@ -1,6 +1,7 @@
 """GPU parity when rows (or row groups) outnumber the 65535 workgroups of a grid's y
 dimension, so every row-parallel kernel runs its grid-stride loop: many short rows
-for the watermark (both seedings, the self-salt row groups), greedy decoding,
+for the watermark (both seedings; self-salt through the slab kernel with a window of
+one token and through the row-group kernel with a window of 4), greedy decoding,
 sampling, candidates and both detection kernels."""
 import numpy as np
 import pytest
@@ -25,6 +26,21 @@ def test_watermark_many_rows(env, seeding, B, V):
     sbw.watermark(t, torch.from_numpy(prev).to(dev), WIDE, 0.5, 1.5, seeding)
     torch.cuda.synchronize()
     assert_logits_equal(_from_device(torch, t), oracle.watermark(x, prev, WIDE, 0.5, 1.5, seeding))
+
+
+def test_watermark_window_many_rows(env):
+    """Self-salt with a window of 4 keeps one row per workgroup: 70001 aligned rows of
+    40 logits run the row-group kernel's grid-stride loop."""
+    torch, sbw, dev = env
+    rng = np.random.default_rng(245)
+    B, V = 70001, 40
+    x = rng.standard_normal((B, V)).astype(np.float32)
+    ctx = workloads.context_tokens(B, 4, V, rng)
+    say(f"watermark many rows, window 4, B={B} V={V}")
+    t = _to_device(torch, dev, x)
+    sbw.watermark(t, torch.from_numpy(ctx).to(dev), WIDE, 0.5, 1.5, "self_salt")
+    torch.cuda.synchronize()
+    assert_logits_equal(_from_device(torch, t), oracle.watermark_w(x, ctx, WIDE, 0.5, 1.5, "self_salt"))
 
 
 @pytest.mark.parametrize("seeding", ["context", "self_salt"])
