@@ -457,7 +457,7 @@ template <int kE, int kRows, int kPer>
 __device__ __forceinline__ void slab_drain(SlabLds<kRows, kPer>& s, uint32_t n, uint32_t pending,
                                            uint32_t lane, uint32_t jid0, uint32_t tm1) {
   const SlabEntry e = s.queue[lane];
-  SlabEntry e2 = SlabEntry{0u, 0u, 0u, 0u};
+  SlabEntry e2;  // read and written back only where `move` holds
   const bool move = lane + 64u < pending;
   if (move) e2 = s.queue[lane + 64u];
   // the pair's token is kPer * (jid0 + lane that queued it) + kE: Philox counter
@@ -501,21 +501,31 @@ template <int kE, int kRows, int kPer>
 __device__ __forceinline__ void slab_position(SlabLds<kRows, kPer>& s, int rows, uint32_t jv, uint64_t bound,
                                               uint32_t lane, uint32_t jid0, uint32_t tm1) {
   uint32_t pending = 0u;  // wave-uniform
-  // two rows per iteration; their key * J(p) by one broadcast LDS read, the next
-  // pair's read ahead (entries past the last row are spares: read, never used)
+  // four rows per iteration, their key * J(p) by two broadcast LDS reads of two rows
+  // each, each pair read one pair ahead into the registers the pair before it has
+  // just freed (entries past the last row are spares: read, never used)
   typedef uint64_t u64x2 __attribute__((ext_vector_type(2)));
-  u64x2 kjp = *reinterpret_cast<const u64x2*>(&s.kjp[0]);
+  u64x2 a = *reinterpret_cast<const u64x2*>(&s.kjp[0]);
   int r = 0;
 #pragma nounroll
-  for (; r + 1 < rows; r += 2) {
-    const u64x2 next = *reinterpret_cast<const u64x2*>(&s.kjp[r + 2]);
+  for (; r + 3 < rows; r += 4) {
+    const u64x2 b = *reinterpret_cast<const u64x2*>(&s.kjp[r + 2]);
     const uint32_t w0 = static_cast<uint32_t>(r) * kSlabMapStride + lane;
-    slab_enqueue<kE, kRows, kPer>(s, pending, kjp.x, jv, bound, w0, lane, jid0, tm1);
-    slab_enqueue<kE, kRows, kPer>(s, pending, kjp.y, jv, bound, w0 + kSlabMapStride, lane, jid0, tm1);
-    kjp = next;
+    slab_enqueue<kE, kRows, kPer>(s, pending, a.x, jv, bound, w0, lane, jid0, tm1);
+    slab_enqueue<kE, kRows, kPer>(s, pending, a.y, jv, bound, w0 + kSlabMapStride, lane, jid0, tm1);
+    a = *reinterpret_cast<const u64x2*>(&s.kjp[r + 4]);
+    slab_enqueue<kE, kRows, kPer>(s, pending, b.x, jv, bound, w0 + 2 * kSlabMapStride, lane, jid0, tm1);
+    slab_enqueue<kE, kRows, kPer>(s, pending, b.y, jv, bound, w0 + 3 * kSlabMapStride, lane, jid0, tm1);
+  }
+  if (r + 1 < rows) {
+    const uint32_t w0 = static_cast<uint32_t>(r) * kSlabMapStride + lane;
+    slab_enqueue<kE, kRows, kPer>(s, pending, a.x, jv, bound, w0, lane, jid0, tm1);
+    slab_enqueue<kE, kRows, kPer>(s, pending, a.y, jv, bound, w0 + kSlabMapStride, lane, jid0, tm1);
+    r += 2;
+    a = *reinterpret_cast<const u64x2*>(&s.kjp[r]);
   }
   if (r < rows)
-    slab_enqueue<kE, kRows, kPer>(s, pending, kjp.x, jv, bound,
+    slab_enqueue<kE, kRows, kPer>(s, pending, a.x, jv, bound,
                                   static_cast<uint32_t>(r) * kSlabMapStride + lane, lane, jid0, tm1);
   if (pending != 0u) slab_drain<kE, kRows, kPer>(s, pending, pending, lane, jid0, tm1);
   __builtin_amdgcn_wave_barrier();
