@@ -397,25 +397,25 @@ watermark_ss_rows_kernel(T* __restrict__ logits, int64_t row_stride, uint32_t V,
 }
 
 // ---------------------------------------------------------------------------
-// Self-salt watermark, fp32, window of one token, by split terms over a slab of
-// rows.  The seed of (row, v) is the smaller of the row term key*J(p)*J(v) and the
+// Self-salt watermark, fp32 or bf16, window of one token, by split terms over a slab
+// of rows.  The seed of (row, v) is the smaller of the row term key*J(p)*J(v) and the
 // self term key*J(v)*J(v) (Sec. 2.3 with the window {p, v}); the self term, and so
 // the draw whenever it is the smaller one (about half of the pairs), is the same in
-// every row.  A wave owns 256 columns (one 16-byte vector per lane) of a slab of up
-// to kRows rows (12, or 8 for launches that 12-row slabs would leave with too few
-// workgroups):
-//  1. each lane draws its four columns' self-term blocks once and writes those
+// every row.  A wave owns 64 16-byte vectors of a row (one per lane: 256 fp32 or 512
+// bf16 columns) over a slab of up to kRows rows (12, or 8 or 6 for launches that
+// taller slabs would leave with too few workgroups):
+//  1. each lane draws its vector's self-term blocks (4 or 8) once and writes those
 //     decisions into the slab's decision map (a byte per row and column, a lane's
-//     four columns in one word) for every row;
-//  2. one word position q at a time, the lanes whose row term is smaller append
-//     (row term, map word, lane) to the wave's queue (ballot + mbcnt give
-//     consecutive entries), and a queue holding 64 pairs is drained at once: 64
+//     columns in one word, or two for bf16) for every row;
+//  2. one token position q of the vector at a time, the lanes whose row term is
+//     smaller append (row term, map word, lane) to the wave's queue (ballot + mbcnt
+//     give consecutive entries), and a queue holding 64 pairs is drained at once: 64
 //     Philox draws side by side, each decision written over its map byte; the last
 //     partial chunk is drained after the slab's last row;
 //  3. each row's vector is biased from its map word and stored.
-// The Philox word is a compile-time choice in every draw (q is a template
-// argument), so each block keeps only the work its word needs.  Per logit this
-// draws about 0.57 blocks instead of 1; the queueing costs about 11 instructions.
+// The Philox counter and word are compile-time functions of q in every draw (q is a
+// template argument), so each block keeps only the work its word needs.  Per logit this
+// draws about 0.57 blocks instead of 1; the queueing costs about 9 instructions.
 // ---------------------------------------------------------------------------
 constexpr uint32_t kSlabQueue = 128;   // queue entries: fewer than 64 left + one row's 64
 // Map words per row: one more than the lanes, so that the same lane's words in
