@@ -71,15 +71,21 @@ namespace {
 #ifndef SBW_SELF_SALT_PREFETCH_BF16
 #define SBW_SELF_SALT_PREFETCH_BF16 1
 #endif
-// Self-salt, width 1 (fp32 and bf16): the split-term slab kernel when it makes at least
-// SBW_SLAB_MIN_GROUPS workgroups with 12-row slabs, else with 8-row, else with 6-row
-// slabs (below that its long-lived waves leave the chip underfilled and the row-group
-// kernel is faster).  0 = off.
+// Self-salt, width 1 (fp32 and bf16): the split-term slab kernel with 12-row slabs when
+// that makes at least SBW_SLAB12_MIN_GROUPS workgroups, else with 8-row, else with 6-row
+// slabs when that makes at least SBW_SLAB_MIN_GROUPS (below that its long-lived waves
+// leave the chip underfilled and the row-group kernel is faster).  12-row slabs need
+// more workgroups than the others: with fewer than ~1.7 rounds of the ~1800 that fit
+// at once, the last round's tail costs more than the shorter slabs' extra self terms.
+// 0 = off.
 #ifndef SBW_SELF_SALT_SLAB
 #define SBW_SELF_SALT_SLAB 1
 #endif
 #ifndef SBW_SLAB_MIN_GROUPS
 #define SBW_SLAB_MIN_GROUPS 2000
+#endif
+#ifndef SBW_SLAB12_MIN_GROUPS
+#define SBW_SLAB12_MIN_GROUPS 3000
 #endif
 #ifndef SBW_SELF_SALT_MIN_GROUPS
 #define SBW_SELF_SALT_MIN_GROUPS 1024  // 2048 measured 5 % slower for B * V of 5-10 M logits
@@ -1686,7 +1692,7 @@ void launch_watermark(void* logits, int64_t B, uint32_t V, int64_t row_stride,
       if constexpr (SBW_SELF_SALT_SLAB && kW == 1) {
         const uint32_t tiles1 = static_cast<uint32_t>((vectors + kThreads - 1) / kThreads);
         const int64_t slabs12 = (B + 11) / 12, slabs8 = (B + 7) / 8, slabs6 = (B + 5) / 6;
-        if (static_cast<int64_t>(tiles1) * slabs12 >= int64_t{SBW_SLAB_MIN_GROUPS}) {
+        if (static_cast<int64_t>(tiles1) * slabs12 >= int64_t{SBW_SLAB12_MIN_GROUPS}) {
           const dim3 grid(tiles1, static_cast<uint32_t>(slabs12 < kMaxGridY ? slabs12 : kMaxGridY));
           hipLaunchKernelGGL((watermark_ss_slab_kernel<T, 12>), grid, dim3(kThreads), 0, stream, p,
                              row_stride, V, B, context, key, tm1, delta, vbase);

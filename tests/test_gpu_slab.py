@@ -28,7 +28,8 @@ from test_gpu_parity import (KEY, WIDE, _from_device, _to_device, assert_logits_
 pytestmark = pytest.mark.gpu
 
 SLAB_ROWS = 12
-MIN_GROUPS = 2000   # workgroups below which the next slab height (or kernel) is taken
+MIN_GROUPS_12 = 3000  # workgroups below which 12-row slabs give way to 8-row ones
+MIN_GROUPS = 2000     # workgroups below which 8- and 6-row slabs give way
 
 
 def slab_rows(B, V, dtype="f32"):
@@ -36,7 +37,9 @@ def slab_rows(B, V, dtype="f32"):
     aligned): the slab height the launch takes, or 0 for the row-group kernel."""
     per = 4 if dtype == "f32" else 8     # tokens in a 16-byte vector
     tiles = -(-(-(-V // per)) // 256)
-    for rows in (12, 8, 6):
+    if tiles * -(-B // 12) >= MIN_GROUPS_12:
+        return 12
+    for rows in (8, 6):
         if tiles * -(-B // rows) >= MIN_GROUPS:
             return rows
     return 0
@@ -73,10 +76,10 @@ def run(env, x, prev, key, gamma, delta, stride=None, v_offset=None):
 
 
 @pytest.mark.parametrize("B,V,stride", [
-    (3001, 8195, None),      # slab of 1 row at the end, V mod 4 = 3, 2049 vectors (tile of 1)
-    (2400, 10241, 10248),    # whole slabs, padded rows, V mod 4 = 1
-    (1417, 16386, None),     # V mod 4 = 2, last tile partly past the row
-    (605, 40000, 40004),     # whole vectors, padded rows, slab of 5 rows at the end
+    (4501, 8195, None),      # slab of 1 row at the end, V mod 4 = 3, 2049 vectors (tile of 1)
+    (3600, 10241, 10248),    # whole slabs, padded rows, V mod 4 = 1
+    (2125, 16386, None),     # V mod 4 = 2, last tile partly past the row
+    (893, 40000, 40004),     # whole vectors, padded rows, slab of 5 rows at the end
 ])
 def test_slab_shapes(env, B, V, stride):
     assert takes_slab(B, V)
@@ -100,7 +103,7 @@ def test_slab_shapes(env, B, V, stride):
     (1.0, 4.0, WIDE),        # every token green
 ])
 def test_slab_parameters(env, gamma, delta, key):
-    B, V = 1850, 12292
+    B, V = 2762, 12292
     assert takes_slab(B, V)
     rng = np.random.default_rng(int(gamma * 1e6) + int(delta * 10) + 5)
     x = rng.standard_normal((B, V)).astype(np.float32)
@@ -113,13 +116,13 @@ def test_slab_parameters(env, gamma, delta, key):
 
 def test_slab_shard(env):
     """Columns [57024, 57024 + 19008) of a 152064-token vocabulary (one of 8 shards) at
-    B = 1300: token ids from 57024, the draws those of the full row."""
-    a, n, V, B = 57024, 19008, 152064, 1300
+    B = 1900: token ids from 57024, the draws those of the full row."""
+    a, n, V, B = 57024, 19008, 152064, 1900
     assert takes_slab(B, n)
     rng = np.random.default_rng(4242)
     x = rng.standard_normal((B, n)).astype(np.float32) * np.float32(3)
     prev = rng.integers(0, V, B).astype(np.int32)
-    say("slab shard 57024+19008, B=1300")
+    say("slab shard 57024+19008, B=1900")
     got, _ = run(env, x, prev, WIDE, 0.25, 2.0, v_offset=a)
     # the oracle's membership of tokens a .. a+n-1 in each row, and its fp32 bias
     green = oracle.is_green_many(WIDE, np.repeat(prev, n), np.tile(np.arange(a, a + n), B), 0.25,
@@ -132,7 +135,7 @@ def test_slab_twice_in_a_row(env):
     """Two launches back to back, the second smaller, on fresh inputs each: nothing a
     launch leaves in LDS or in the logits changes the next one's result."""
     rng = np.random.default_rng(99)
-    for B, V in ((2000, 12300), (1900, 12299)):
+    for B, V in ((3000, 12300), (2900, 12299)):
         assert takes_slab(B, V)
         x = rng.standard_normal((B, V)).astype(np.float32)
         prev = rng.integers(0, V, B).astype(np.int32)
@@ -161,7 +164,8 @@ def test_slab_grid_stride(env):
     (131, 128255),    # a last slab of 3 rows, V mod 4 = 3
 ])
 def test_slab_eight_rows(env, B, V):
-    """Launches that 12-row slabs would leave with too few workgroups take 8-row ones."""
+    """Launches that 12-row slabs would leave with too few workgroups (here under 2000;
+    below 3000 as well) take 8-row ones."""
     assert slab_rows(B, V) == 8
     rng = np.random.default_rng(808 + B)
     x = special_logits(rng, B, V, "f32")
@@ -190,8 +194,8 @@ def test_slab_six_rows(env, B, V):
 
 
 @pytest.mark.parametrize("B,V,stride,rows", [
-    (2400, 20483, None, 12),      # V mod 8 = 3, a tile of 1 vector at the end
-    (2407, 20480, 20488, 12),     # padded rows, a last slab of 7 rows
+    (3600, 20483, None, 12),      # V mod 8 = 3, a tile of 1 vector at the end
+    (3607, 20480, 20488, 12),     # padded rows, a last slab of 7 rows
     (256, 152064, None, 8),       # the c4 shape in bf16: 8-row slabs
     (263, 152061, None, 8),       # a last slab of 7 rows, V mod 8 = 5
     (192, 152064, None, 6),       # 6-row slabs
@@ -214,12 +218,12 @@ def test_slab_bf16(env, B, V, stride, rows):
 
 def test_slab_bf16_shard(env):
     """A bf16 vocabulary shard whose first token id is a multiple of 8 (not of 16)."""
-    a, n, V, B = 57024 + 8, 19000, 152064, 2600
+    a, n, V, B = 57024 + 8, 19000, 152064, 3600
     assert slab_rows(B, n, "bf16") == 12
     rng = np.random.default_rng(4343)
     x = workloads.f32_to_bf16_bits(rng.standard_normal((B, n)).astype(np.float32) * np.float32(2))
     prev = rng.integers(0, V, B).astype(np.int32)
-    say("slab bf16 shard 57032+19000, B=2600")
+    say("slab bf16 shard 57032+19000, B=3600")
     got, _ = run(env, x, prev, KEY, 0.5, -1.5, v_offset=a)
     green = oracle.is_green_many(KEY, np.repeat(prev, n), np.tile(np.arange(a, a + n), B), 0.5,
                                  "self_salt").reshape(B, n)
@@ -228,9 +232,11 @@ def test_slab_bf16_shard(env):
 
 
 def test_launch_rule_cases():
-    """The c4 configurations take 12-row slabs, B = 128 of a 128256-token vocabulary
-    8-row ones, B = 96 6-row ones; c3 and small batches take the row-group kernel."""
+    """The c4 configurations take 12-row slabs, B = 160-240 of 152064 tokens and B = 128
+    of 128256 8-row ones, B = 96 6-row ones; c3 and small batches take the row-group
+    kernel."""
     assert slab_rows(256, 152064) == 12 and slab_rows(1024, 152064) == 12
+    assert slab_rows(160, 152064) == 8 and slab_rows(240, 152064) == 8
     assert slab_rows(128, 128256) == 8 and slab_rows(96, 128256) == 6
     assert slab_rows(64, 128256) == 0 and slab_rows(16, 152064) == 0
     assert slab_rows(256, 152064, "bf16") == 8 and slab_rows(1024, 152064, "bf16") == 12
