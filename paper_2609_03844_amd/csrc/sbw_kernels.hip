@@ -81,6 +81,16 @@ namespace {
 #ifndef SBW_SELF_SALT_SLAB
 #define SBW_SELF_SALT_SLAB 1
 #endif
+// Context seeding: launches of at least SBW_XCD_ROWS_MIN rows (a multiple of 8) and
+// SBW_XCD_ROWS_MIN_BYTES of logits, more than the 256 MB Infinity Cache holds, give
+// each XCD whole rows (fp32 B = 512 / 1024 of 152064: 1 / 3 % faster, bf16 B = 1024:
+// 3 %; B = 256 even, B = 128 and bf16 B = 512 of 128256 up to 1 % slower).
+#ifndef SBW_XCD_ROWS_MIN
+#define SBW_XCD_ROWS_MIN 512
+#endif
+#ifndef SBW_XCD_ROWS_MIN_BYTES
+#define SBW_XCD_ROWS_MIN_BYTES (int64_t{256} << 20)
+#endif
 #ifndef SBW_SLAB_MIN_GROUPS
 #define SBW_SLAB_MIN_GROUPS 2000
 #endif
@@ -223,19 +233,29 @@ __device__ __forceinline__ void bias_one(T* row, uint32_t v, const RowSeed<kW>& 
 // Context-seeded watermark for rows whose start is 16-byte aligned.  Grid: x = tile
 // of kThreads * kU vectors within a row, y = row (grid-stride over rows beyond
 // 65535).  Each lane issues its logits load before reading the row's window, so the
-// scalar loads of the window overlap the HBM stream.
+// scalar loads of the window overlap the HBM stream.  With xcd_rows (one row per y,
+// B a multiple of 8) the workgroups are renumbered so that each of the 8 XCDs, which
+// take workgroups in turn, streams whole rows: workgroup n goes to row
+// 8 * (n / 8 / tiles) + n % 8, tile n / 8 % tiles.
 template <typename T, int kU, int kW>
 __global__ void __launch_bounds__(kThreads)
 watermark_vec_kernel(T* __restrict__ logits, int64_t row_stride, uint32_t V, int64_t B,
                      const int32_t* __restrict__ context, int width, uint64_t key, uint32_t tm1,
-                     float delta, uint32_t vbase) {
+                     float delta, uint32_t vbase, uint32_t xcd_rows) {
   using VecT = typename std::conditional<sizeof(T) == 4, f32x4, u32x4>::type;
   constexpr uint32_t kPer = 16u / sizeof(T);  // elements per 16-byte vector
   const uint32_t full = V / kPer;             // complete vectors in a row
   const uint32_t tail = V % kPer;
   const uint32_t jbase = vbase / kPer;        // vector index of the first column (vbase % 8 == 0)
-  const uint32_t first = blockIdx.x * (kThreads * kU);
-  for (int64_t row = blockIdx.y; row < B; row += gridDim.y) {
+  uint32_t first = blockIdx.x * (kThreads * kU);
+  int64_t row0 = blockIdx.y;
+  if (xcd_rows != 0u) {
+    const uint32_t n = blockIdx.y * gridDim.x + blockIdx.x;
+    const uint32_t q = n >> 3;
+    row0 = static_cast<int64_t>(q / gridDim.x) * 8 + (n & 7u);
+    first = (q % gridDim.x) * (kThreads * kU);
+  }
+  for (int64_t row = row0; row < B; row += gridDim.y) {
     T* row_ptr = logits + row * row_stride;
     VecT* vec = reinterpret_cast<VecT*>(row_ptr);
     const int32_t* window = context + row * width;
@@ -1748,9 +1768,17 @@ void launch_watermark(void* logits, int64_t B, uint32_t V, int64_t row_stride,
         hipLaunchKernelGGL((watermark_ss_rows_kernel<T, kU, kW, 1, kPf>), grid, dim3(kThreads), 0,
                            stream, p, row_stride, V, B, context, width, key, tm1, delta, vbase);
     } else {
+      // whole rows per XCD for large launches (one launch row per grid row, workgroup
+      // numbers below 2^32)
+      const uint32_t xcd_rows =
+          B >= SBW_XCD_ROWS_MIN && B % 8 == 0 && B <= kMaxGridY &&
+                  B * static_cast<int64_t>(V) * static_cast<int64_t>(sizeof(T)) >= SBW_XCD_ROWS_MIN_BYTES &&
+                  static_cast<uint64_t>(tiles) * static_cast<uint64_t>(B) < (uint64_t{1} << 32)
+              ? 1u
+              : 0u;
       hipLaunchKernelGGL((watermark_vec_kernel<T, kU, kW>), dim3(tiles, rows),
                          dim3(kThreads), 0, stream, p, row_stride, V, B, context, width, key, tm1,
-                         delta, vbase);
+                         delta, vbase, xcd_rows);
     }
   } else {
     const uint32_t tiles = static_cast<uint32_t>((static_cast<uint64_t>(V) + kThreads - 1) / kThreads);

@@ -335,6 +335,32 @@ def test_bf16_rounding_every_pattern(env, layout):
                             f"bf16 delta={delta!r}")
 
 
+@pytest.mark.parametrize("dtype,B,V", [
+    ("f32", 512, 131075),     # 268.4 MB of logits, just past 256 MiB: whole rows per XCD
+    ("bf16", 1024, 131075),   # the same bytes in bf16
+    ("f32", 515, 1000),       # not a multiple of 8 rows: the plain order
+])
+def test_context_xcd_rows(env, dtype, B, V):
+    """Context-seeded launches of at least 512 rows, a multiple of 8, and more logit
+    bytes than the Infinity Cache holds renumber their workgroups so that each XCD takes
+    whole rows; rows padded to 16 bytes so that the vector kernel takes them."""
+    rng = np.random.default_rng(5120 + B + V)
+    x = special_logits(rng, B, V, dtype)
+    prev = rng.integers(0, 1 << 31, B).astype(np.int32)
+    say(f"context xcd rows {dtype} B={B} V={V}")
+    torch, sbw, dev = env
+    stride = -(-V // 8) * 8
+    t = torch.zeros((B, stride), dtype=torch.bfloat16 if dtype == "bf16" else torch.float32,
+                    device=dev)
+    t[:, :V] = _to_device(torch, dev, x)
+    sbw.watermark(t[:, :V], torch.from_numpy(prev).to(dev), WIDE, 0.25, 2.0, "context")
+    torch.cuda.synchronize()
+    out = _from_device(torch, t)
+    assert_logits_equal(out[:, :V], oracle.watermark(x, prev, WIDE, 0.25, 2.0, "context"),
+                        f"{dtype} B={B} V={V}")
+    assert not out[:, V:].any(), "the padding columns were written"
+
+
 @pytest.mark.parametrize("dtype,B,V,width,rows", [
     ("f32", 75, 152063, 1, 4),      # 149 tiles x 19 / 20 groups of 4 rows, last group of 3 / 1;
     ("f32", 77, 152061, 1, 4),      #   6-row slabs would make 13 x 149 < 2000 workgroups
